@@ -1,0 +1,24 @@
+"""CPU oracle for the additively-quantized (AQ) layer forward.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this package.  The GPU library never
+calls it and shares no code with it: it is the plain, slow, fp64 statement of
+what the layer computes, used to judge the GPU kernels.
+"""
+from .aq_oracle import (  # noqa: F401
+    to_f64,
+    dequantize,
+    activations_f64,
+    im2col,
+    linear_forward,
+    conv_forward,
+    forward,
+    forward_sampled,
+    decode_emulate,
+    f32_to_bf16_bits,
+    bf16_bits_to_f32,
+    rel_err_inf,
+    dense_conv_flops,
+    lut_conv_flops,
+    lut_breakpoint_cout,
+)
