@@ -1,0 +1,169 @@
+"""Benchmark of the AQ layer forward on one MI355X.
+
+One step = one forward of the whole hot path (dispatch, activation staging,
+weight decode or table build, contraction, epilogue) over the workload's
+synthetic inputs, which are resident in HBM before timing starts.  Prints ONE
+JSON line with dense-equivalent TFLOP/s (2 FLOP per multiply-accumulate), the
+algorithmic HBM GB/s, the roofline fraction of the dominant kernel and the
+CPU oracle timed on this host.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config conv64]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16/bf16 matrix-core peak
+PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
+PEAK_F32_VALU_TFLOPS = 157.3
+
+
+def _dtype_bytes(name: str) -> int:
+    return {"f32": 4, "f16": 2, "bf16": 2, "i8": 1}[name]
+
+
+def algorithmic_bytes(spec) -> int:
+    """Bytes the layer must move at least once: codes, codebooks, scales, X, Y.
+
+    Convolutions count the NCHW input once (implicit im2col), not the im2col
+    matrix.  int8 activations add their per-token scales.
+    """
+    code_b = 1 if spec.B <= 8 else 2
+    codes = spec.C_out * spec.G * spec.M * code_b
+    cbs = spec.M * (1 << spec.B) * spec.g * _dtype_bytes(spec.codebook_dtype)
+    scales = 4 * spec.C_out
+    if spec.conv is None:
+        x = spec.n * spec.K * _dtype_bytes(spec.x_dtype)
+    else:
+        c = spec.conv
+        x = spec.n * c.cin * c.H * c.W * _dtype_bytes(spec.x_dtype)
+    xs = 4 * spec.tokens if spec.x_dtype == "i8" else 0
+    y = spec.tokens * spec.C_out * _dtype_bytes(spec.y_dtype)
+    return codes + cbs + scales + x + xs + y
+
+
+def cpu_baseline(spec, inp, budget_s: float = 12.0):
+    """Time the fp64 oracle on this host's cores (bounded number of repetitions)."""
+    import numpy as np
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    O.forward(spec, inp)       # warm-up
+    first = time.perf_counter() - t0
+    reps = max(1, min(5, int(budget_s / max(first, 1e-3))))
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        O.forward(spec, inp)
+        times.append(time.perf_counter() - t0)
+    t = statistics.median(times)
+    return {
+        "value": round(spec.dense_flops / t / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": f"whole layer ({spec.name}): fp64 dequantize + im2col + BLAS matmul, "
+                  f"median of {reps} runs after 1 warm-up, {t:.3f} s per forward",
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="conv64")
+    ap.add_argument("--path", default="auto", choices=["auto", "lut", "decode"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    a = ap.parse_args(argv)
+
+    if a.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {a.gpus}); the AQ layer forward is not sharded "
+              "across GPUs in this build", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2506_05960_amd as P
+    import workloads as W
+
+    P.load_library()
+    torch.cuda.set_device(0)
+    spec = W.config_spec(a.config)
+    inp = W.config_inputs(a.config)
+    layer = P.AQLayer(spec, inp)
+    if a.path != "auto":
+        layer.set_path(a.path)
+    path = layer.choose_path(spec.tokens)
+    x = torch.from_numpy(np.ascontiguousarray(inp["x"])).cuda()
+    xs = None if inp["x_scales"] is None else torch.from_numpy(inp["x_scales"]).cuda()
+    y = torch.empty(layer.out_shape(spec.n), dtype=torch.float16 if spec.y_dtype == "f16" else torch.float32,
+                    device="cuda")
+
+    for _ in range(a.warmup):
+        layer.forward(x, xs, out=y)
+    torch.cuda.synchronize()
+
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(a.steps):
+        layer.forward(x, xs, out=y)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / a.steps
+
+    flops = spec.dense_flops
+    tflops = flops / (ms * 1e-3) / 1e12
+    gbs = algorithmic_bytes(spec) / (ms * 1e-3) / 1e9
+    if path == "decode" and spec.tile_dtype != "f32":
+        roof = {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_MFMA_F16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tflops / PEAK_MFMA_F16_TFLOPS, 4), "traffic": None}
+    else:
+        roof = {"bound": "hbm", "achieved": round(gbs, 3), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None}
+
+    out = {
+        "metric": "dense-equivalent TFLOP/s of the AQ layer forward",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": spec.tile_dtype if path == "decode" else "f32",
+        "data": "synthetic (seeded; LDM-4-shaped layer, random codebooks/codes/activations)",
+        "config": {"workload": spec.name, "path": path, "tokens": spec.tokens, "K": spec.K, "C_out": spec.C_out,
+                   "g": spec.g, "M": spec.M, "B": spec.B, "x_dtype": spec.x_dtype, "y_dtype": spec.y_dtype},
+        "hbm_gbs_algorithmic": round(gbs, 3),
+        "algorithmic_bytes": algorithmic_bytes(spec),
+        "dense_flops": flops,
+        "roofline": roof,
+    }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(spec, inp)
+    layer.close()
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,133 @@
+/*
+ * aq.h -- C ABI of the additively-quantized (AQ) layer forward for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * Operation (AQUATIC-Diff, arXiv 2506.05960, Sec. 2.4 eq. (4) and Sec. 3.1.1):
+ * the weight matrix W [C_out][K] of a linear or im2col-lowered convolution
+ * layer is split along K into G = K/g groups of g consecutive weights.  Group
+ * j of output row i is stored as M integer codes b[i][j][m] < 2^B, and
+ *
+ *     W[i][j*g + t] = s[i] * sum_{m<M} C[m][ b[i][j][m] ][t]
+ *
+ * with M codebooks C[m] of 2^B rows of g values and one scale s[i] per output
+ * channel.  The forward computes Y = X * W^T (tokens as rows) without ever
+ * writing W to memory.  A convolution runs on NCHW input; its token order is
+ * (image, output row, output column) and its K order is (input channel,
+ * kernel row, kernel column) with the channel outermost (Sec. 3.1.1).
+ *
+ * Two device paths implement the forward:
+ *   - LUT: per token and group, tabulate x_g . C[m][k] for every codeword k,
+ *     then sum code-indexed table entries (the appendix's rearrangement,
+ *     eq. (12)).  Needs B <= 8.
+ *   - DECODE: expand code tiles into fp16/bf16 (or fp32) weight tiles on chip
+ *     and contract them with matrix-core instructions.
+ * aq_layer_forward picks one per call (AQ_PATH_AUTO) unless a path is forced.
+ *
+ * Conventions for every entry point:
+ *   - Return value is an aq_status; nothing aborts or throws across the ABI.
+ *     On failure aq_last_error() returns a message (thread-local, valid until
+ *     the next failing call on the same thread).
+ *   - Arguments are validated on the host before any HIP call.
+ *   - "host" pointers are read synchronously during the call; "device"
+ *     pointers must be HIP device allocations on the layer's device.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ */
+#ifndef AQ_H
+#define AQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct aq_layer aq_layer; /* opaque, owned by the library */
+
+typedef enum {
+    AQ_OK = 0,
+    AQ_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size, dtype, alignment or code value */
+    AQ_ERR_UNSUPPORTED = 2,      /* valid request this build has no kernel for       */
+    AQ_ERR_OUT_OF_MEMORY = 3,    /* device allocation failed                          */
+    AQ_ERR_DEVICE = 4            /* any other HIP error (or no GPU present)           */
+} aq_status;
+
+typedef enum { AQ_F32 = 0, AQ_F16 = 1, AQ_BF16 = 2, AQ_I8 = 3 } aq_dtype;
+
+typedef enum { AQ_PATH_AUTO = 0, AQ_PATH_LUT = 1, AQ_PATH_DECODE = 2 } aq_path;
+
+typedef struct {
+    int32_t  out_features;   /* C_out >= 1                                                  */
+    int32_t  in_features;    /* K = G*g; for a convolution K = conv_cin*conv_kh*conv_kw      */
+    int32_t  codebook_dtype; /* aq_dtype: F32 | F16 | BF16                                   */
+    int32_t  x_dtype;        /* aq_dtype: F32 | F16 | BF16 | I8 (I8: linear only, x_scales)  */
+    int32_t  y_dtype;        /* aq_dtype: F32 | F16                                          */
+    int32_t  tile_dtype;     /* aq_dtype: F16 | BF16 (matrix-core decode path) | F32         */
+    int32_t  conv_kh, conv_kw;  /* 0,0 => linear layer: X [n][K], Y [n][C_out] row-major      */
+    int32_t  conv_cin, conv_stride, conv_pad, in_h, in_w; /* conv: X NCHW [n][cin][in_h][in_w],
+                                                              Y NCHW [n][C_out][OH][OW]         */
+    int64_t  max_tokens;     /* workspace sizing: every forward needs tokens <= max_tokens    */
+} aq_layer_desc;
+
+/*
+ * Create a layer: validate, copy and repack the quantized weights into
+ * library-owned device memory on the current HIP device, and allocate the
+ * workspace for up to desc->max_tokens tokens.  Synchronous; the caller may
+ * free its buffers on return.
+ *   codebooks  host, [M][2^B][g] in desc->codebook_dtype (bf16 as raw bits)
+ *   codes      host, [C_out][K/g][M], uint8 when B <= 8, uint16 otherwise;
+ *              every code must be < 2^B (scanned; AQ_ERR_INVALID_ARGUMENT)
+ *   scales     host, [C_out] fp32, the per-output-channel scale s[i]
+ *   g, M, B    group size 1..16, codebooks 1..8, index bits 1..16
+ *   out        receives the handle (set to NULL on failure)
+ * Supported: the LUT path needs B <= 8; the fp16/bf16 decode path needs
+ * g == 8; the fp32 decode path takes any g.  A layer with no usable path
+ * returns AQ_ERR_UNSUPPORTED.  Without a GPU: AQ_ERR_DEVICE.
+ */
+aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, const void* codes,
+                          const float* scales, int g, int M, int B, aq_layer** out);
+
+/*
+ * Forward Y = X * W^T on `stream`; asynchronous, allocates nothing and never
+ * synchronises.  The layer's workspace makes concurrent forwards on one layer
+ * a race: serialise them on one stream.
+ *   X          device; linear: [n][K] row-major; conv: NCHW [n][cin][in_h][in_w];
+ *              dtype desc->x_dtype; 16-byte aligned
+ *   x_scales   device [n] fp32 per-token scales, required iff x_dtype == I8
+ *              (x[t][k] = x_scales[t] * q[t][k]); otherwise ignored
+ *   Y          device; linear [n][C_out]; conv NCHW [n][C_out][OH][OW];
+ *              dtype desc->y_dtype; 16-byte aligned
+ *   n          tokens (linear) or images (conv); 1 <= tokens <= max_tokens
+ */
+aq_status aq_layer_forward(aq_layer* layer, const void* X, const float* x_scales, void* Y, int64_t n,
+                           void* stream);
+
+/*
+ * Decoded weights W [C_out][K] in desc->tile_dtype (device, caller-owned),
+ * computed as the decode path does: an fp32 sum of the M codewords in
+ * ascending m, times s[i] in fp32, then one round-to-nearest-even to the tile
+ * dtype (eq. (4) with the per-channel scale).  Asynchronous on `stream`.
+ * A test hook for bit-exact checks; the forward never materialises W.
+ */
+aq_status aq_layer_decode(aq_layer* layer, void* W, void* stream);
+
+/* Force a path for later forwards (AUTO restores the dispatcher).  Forcing an
+ * unavailable path returns AQ_ERR_UNSUPPORTED and leaves the setting as is. */
+aq_status aq_layer_set_path(aq_layer* layer, aq_path path);
+
+/* The path a forward over `tokens` tokens would take (pure host function). */
+aq_status aq_layer_choose_path(const aq_layer* layer, int64_t tokens, aq_path* out);
+
+/* Release the layer's device memory (synchronises the device).  NULL is a no-op. */
+aq_status aq_layer_destroy(aq_layer* layer);
+
+/* Message for the last failing call on this thread ("" if none). */
+const char* aq_last_error(void);
+
+/* Library version string. */
+const char* aq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AQ_H */

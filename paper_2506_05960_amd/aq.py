@@ -1,0 +1,215 @@
+"""ctypes binding of ``libaq.so`` (the C ABI declared in ``include/aq.h``).
+
+Argument marshalling only: every step of the forward runs in the library's
+HIP kernels.  PyTorch supplies device memory and the current stream.  If the
+library is not built, loading fails loudly; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libaq.so")
+
+AQ_OK, AQ_ERR_INVALID_ARGUMENT, AQ_ERR_UNSUPPORTED, AQ_ERR_OUT_OF_MEMORY, AQ_ERR_DEVICE = range(5)
+AQ_F32, AQ_F16, AQ_BF16, AQ_I8 = range(4)
+AQ_PATH_AUTO, AQ_PATH_LUT, AQ_PATH_DECODE = range(3)
+
+DTYPE_CODES = {"f32": AQ_F32, "f16": AQ_F16, "bf16": AQ_BF16, "i8": AQ_I8}
+PATH_CODES = {"auto": AQ_PATH_AUTO, "lut": AQ_PATH_LUT, "decode": AQ_PATH_DECODE}
+PATH_NAMES = {v: k for k, v in PATH_CODES.items()}
+STATUS_NAMES = {0: "AQ_OK", 1: "AQ_ERR_INVALID_ARGUMENT", 2: "AQ_ERR_UNSUPPORTED", 3: "AQ_ERR_OUT_OF_MEMORY",
+                4: "AQ_ERR_DEVICE"}
+
+EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_set_path",
+            "aq_layer_choose_path", "aq_layer_destroy", "aq_last_error", "aq_version")
+
+
+class AQError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class aq_layer_desc(ctypes.Structure):
+    _fields_ = [
+        ("out_features", ctypes.c_int32),
+        ("in_features", ctypes.c_int32),
+        ("codebook_dtype", ctypes.c_int32),
+        ("x_dtype", ctypes.c_int32),
+        ("y_dtype", ctypes.c_int32),
+        ("tile_dtype", ctypes.c_int32),
+        ("conv_kh", ctypes.c_int32),
+        ("conv_kw", ctypes.c_int32),
+        ("conv_cin", ctypes.c_int32),
+        ("conv_stride", ctypes.c_int32),
+        ("conv_pad", ctypes.c_int32),
+        ("in_h", ctypes.c_int32),
+        ("in_w", ctypes.c_int32),
+        ("max_tokens", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libaq.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built: run `python -m paper_2506_05960_amd.build` "
+                           "(the AQ layer has no non-HIP fallback)")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+    lib.aq_layer_create.argtypes = [ctypes.POINTER(aq_layer_desc), vp, vp, vp, i32, i32, i32, ctypes.POINTER(vp)]
+    lib.aq_layer_forward.argtypes = [vp, vp, vp, vp, i64, vp]
+    lib.aq_layer_decode.argtypes = [vp, vp, vp]
+    lib.aq_layer_set_path.argtypes = [vp, i32]
+    lib.aq_layer_choose_path.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_int)]
+    lib.aq_layer_destroy.argtypes = [vp]
+    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_set_path",
+              "aq_layer_choose_path", "aq_layer_destroy"):
+        getattr(lib, f).restype = ctypes.c_int
+    lib.aq_last_error.restype = ctypes.c_char_p
+    lib.aq_last_error.argtypes = []
+    lib.aq_version.restype = ctypes.c_char_p
+    lib.aq_version.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _check(status: int) -> None:
+    if status != AQ_OK:
+        raise AQError(status, load_library().aq_last_error().decode())
+
+
+def make_desc(C_out: int, K: int, codebook_dtype: str, x_dtype: str, y_dtype: str, tile_dtype: str,
+              max_tokens: int, conv=None) -> aq_layer_desc:
+    d = aq_layer_desc()
+    d.out_features, d.in_features = C_out, K
+    d.codebook_dtype = DTYPE_CODES[codebook_dtype]
+    d.x_dtype = DTYPE_CODES[x_dtype]
+    d.y_dtype = DTYPE_CODES[y_dtype]
+    d.tile_dtype = DTYPE_CODES[tile_dtype]
+    if conv is not None:
+        d.conv_kh, d.conv_kw, d.conv_cin = conv.kh, conv.kw, conv.cin
+        d.conv_stride, d.conv_pad, d.in_h, d.in_w = conv.stride, conv.pad, conv.H, conv.W
+    d.max_tokens = max_tokens
+    return d
+
+
+# ---- thin wrappers with the C names ----
+
+def aq_layer_create(desc: aq_layer_desc, codebooks: np.ndarray, codes: np.ndarray, scales: np.ndarray,
+                    g: int, M: int, B: int) -> int:
+    lib = load_library()
+    cb = np.ascontiguousarray(codebooks)
+    cd = np.ascontiguousarray(codes)
+    sc = np.ascontiguousarray(scales, dtype=np.float32)
+    h = ctypes.c_void_p()
+    _check(lib.aq_layer_create(ctypes.byref(desc), cb.ctypes.data, cd.ctypes.data, sc.ctypes.data,
+                               g, M, B, ctypes.byref(h)))
+    return h.value
+
+
+def aq_layer_forward(handle: int, X: int, x_scales: int, Y: int, n: int, stream: int) -> None:
+    _check(load_library().aq_layer_forward(handle, X, x_scales, Y, n, stream))
+
+
+def aq_layer_decode(handle: int, W: int, stream: int) -> None:
+    _check(load_library().aq_layer_decode(handle, W, stream))
+
+
+def aq_layer_set_path(handle: int, path: str) -> None:
+    _check(load_library().aq_layer_set_path(handle, PATH_CODES[path]))
+
+
+def aq_layer_choose_path(handle: int, tokens: int) -> str:
+    out = ctypes.c_int()
+    _check(load_library().aq_layer_choose_path(handle, tokens, ctypes.byref(out)))
+    return PATH_NAMES[out.value]
+
+
+def aq_layer_destroy(handle: Optional[int]) -> None:
+    _check(load_library().aq_layer_destroy(handle))
+
+
+def aq_version() -> str:
+    return load_library().aq_version().decode()
+
+
+# ---- convenience object over the same calls ----
+
+_TORCH_DT = None
+
+
+def _torch_dtype(name: str):
+    import torch
+    return {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8}[name]
+
+
+class AQLayer:
+    """A device-resident AQ layer.
+
+    ``spec`` carries C_out, K, g, M, B, the dtypes and ``conv`` geometry (or
+    None); ``inputs`` carries host numpy ``codebooks``, ``codes`` and ``scales``.
+    """
+
+    def __init__(self, spec, inputs, max_tokens: Optional[int] = None):
+        self.spec = spec
+        mt = max_tokens if max_tokens is not None else spec.tokens
+        self.desc = make_desc(spec.C_out, spec.K, spec.codebook_dtype, spec.x_dtype, spec.y_dtype,
+                              spec.tile_dtype, mt, spec.conv)
+        self.handle = aq_layer_create(self.desc, inputs["codebooks"], inputs["codes"], inputs["scales"],
+                                      spec.g, spec.M, spec.B)
+
+    def out_shape(self, n: int):
+        s = self.spec
+        if s.conv is None:
+            return (n, s.C_out)
+        return (n, s.C_out, s.conv.OH, s.conv.OW)
+
+    def forward(self, x, x_scales=None, out=None, stream=None):
+        """Y for device tensor ``x`` (token-major [n, K] or NCHW); returns ``out``."""
+        import torch
+        n = x.shape[0]
+        if out is None:
+            out = torch.empty(self.out_shape(n), dtype=_torch_dtype(self.spec.y_dtype), device=x.device)
+        st = stream if stream is not None else torch.cuda.current_stream(x.device).cuda_stream
+        xs = 0 if x_scales is None else x_scales.data_ptr()
+        aq_layer_forward(self.handle, x.data_ptr(), xs, out.data_ptr(), n, st)
+        return out
+
+    __call__ = forward
+
+    def decode(self, out=None, stream=None):
+        import torch
+        s = self.spec
+        dt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.int16}[s.tile_dtype]
+        if out is None:
+            out = torch.empty((s.C_out, s.K), dtype=dt, device="cuda")
+        st = stream if stream is not None else torch.cuda.current_stream().cuda_stream
+        aq_layer_decode(self.handle, out.data_ptr(), st)
+        return out
+
+    def set_path(self, path: str) -> None:
+        aq_layer_set_path(self.handle, path)
+
+    def choose_path(self, tokens: int) -> str:
+        return aq_layer_choose_path(self.handle, tokens)
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            aq_layer_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,63 @@
+// Internal declarations shared by the host entry points and the kernel
+// launchers.  Nothing here crosses the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "aq.h"
+
+namespace aq {
+
+// Geometry of one forward call, resolved on the host.
+struct Geom {
+    int C_out, K, G, g, M, B;
+    int64_t tokens;               // rows of the (implicit) X matrix
+    bool conv;
+    int cin, kh, kw, stride, pad, H, W, OH, OW;
+};
+
+// Device-resident copy of a layer's quantized weights.
+struct DeviceWeights {
+    const void* codebooks;        // [M][2^B][g] in codebook dtype
+    const float* cb32;            // [M][2^B][g] fp32 (exact widening of codebooks)
+    const void* cbtile;           // [2^B][g] codebook rounded to the tile dtype (M == 1, B > 8), else null
+    const void* codes;            // [C_out][G][M] uint8 | uint16
+    const uint8_t* codes_lut;     // [nchunk][C_out][jc][M] uint8 (B <= 8), zero padded
+    const float* scales;          // [C_out]
+    int cb_dtype;                 // aq_dtype
+};
+
+// LUT-path blocking chosen at create time.
+struct LutPlan {
+    int jc;                       // groups per chunk
+    int nchunk;                   // ceil(G / jc)
+    int tok_block;                // tokens per launch (workspace rows)
+};
+
+constexpr int kLutTokTile = 4;    // tokens per LUT entry (one 16-byte table read)
+
+// ---- launchers (each returns the launch's hipError_t) ----
+
+hipError_t launch_decode_to_global(const Geom& geo, const DeviceWeights& w, int tile_dtype, void* W,
+                                   hipStream_t stream);
+
+hipError_t launch_lut_forward(const Geom& geo, const DeviceWeights& w, const LutPlan& plan, const void* X,
+                              int x_dtype, const float* x_scales, void* Y, int y_dtype, float* ws,
+                              hipStream_t stream);
+
+hipError_t launch_mfma_forward(const Geom& geo, const DeviceWeights& w, const void* X, int x_dtype,
+                               const float* x_scales, void* Y, int y_dtype, int tile_dtype,
+                               hipStream_t stream);
+
+// Codebook preparation at create time: fp32 widening and tile-dtype rounding.
+hipError_t launch_codebook_prep(const void* cb, int cb_dtype, int64_t n, float* cb32, void* cbtile, int tile_dtype,
+                                hipStream_t stream);
+
+size_t lut_lds_bytes(const Geom& geo, const LutPlan& plan);
+
+hipError_t launch_f32_forward(const Geom& geo, const DeviceWeights& w, const void* X, int x_dtype,
+                              const float* x_scales, void* Y, int y_dtype, hipStream_t stream);
+
+}  // namespace aq

@@ -1,0 +1,318 @@
+// C ABI entry points: argument validation (host only, before any HIP call),
+// device copies and repacking of the quantized weights, path dispatch.
+#include <algorithm>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "aq_internal.h"
+
+using aq::DeviceWeights;
+using aq::Geom;
+using aq::LutPlan;
+
+struct aq_layer {
+    aq_layer_desc desc;
+    int g, M, B, G;
+    int device;
+    void* d_cb;
+    float* d_cb32;
+    void* d_cbtile;
+    void* d_codes;
+    uint8_t* d_codes_lut;
+    float* d_scales;
+    float* d_ws;
+    LutPlan plan;
+    bool lut_ok, dec_ok;
+    aq_path path;
+    int64_t lut_max_tokens;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+aq_status fail(aq_status s, const std::string& msg) {
+    g_err = msg;
+    return s;
+}
+
+aq_status hip_fail(hipError_t e, const char* what) {
+    if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+        return fail(AQ_ERR_OUT_OF_MEMORY, std::string(what) + ": " + hipGetErrorString(e));
+    return fail(AQ_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+size_t dtype_bytes(int dt) {
+    switch (dt) {
+    case AQ_F32: return 4;
+    case AQ_F16:
+    case AQ_BF16: return 2;
+    default: return 1;
+    }
+}
+
+bool is_conv(const aq_layer_desc& d) { return d.conv_kh != 0 || d.conv_kw != 0; }
+
+int conv_out(int in, int pad, int k, int stride) { return (in + 2 * pad - k) / stride + 1; }
+
+aq_status validate_desc(const aq_layer_desc* d, int g, int M, int B) {
+    if (g < 1 || g > 16) return fail(AQ_ERR_INVALID_ARGUMENT, "g must be in [1, 16]");
+    if (M < 1 || M > 8) return fail(AQ_ERR_INVALID_ARGUMENT, "M must be in [1, 8]");
+    if (B < 1 || B > 16) return fail(AQ_ERR_INVALID_ARGUMENT, "B must be in [1, 16]");
+    if (d->out_features < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "out_features must be >= 1");
+    if (d->in_features < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "in_features must be >= 1");
+    if (d->in_features % g != 0) return fail(AQ_ERR_INVALID_ARGUMENT, "in_features must be a multiple of g");
+    if (d->codebook_dtype != AQ_F32 && d->codebook_dtype != AQ_F16 && d->codebook_dtype != AQ_BF16)
+        return fail(AQ_ERR_INVALID_ARGUMENT, "codebook_dtype must be F32, F16 or BF16");
+    if (d->x_dtype < AQ_F32 || d->x_dtype > AQ_I8) return fail(AQ_ERR_INVALID_ARGUMENT, "bad x_dtype");
+    if (d->y_dtype != AQ_F32 && d->y_dtype != AQ_F16) return fail(AQ_ERR_INVALID_ARGUMENT, "y_dtype must be F32 or F16");
+    if (d->tile_dtype != AQ_F32 && d->tile_dtype != AQ_F16 && d->tile_dtype != AQ_BF16)
+        return fail(AQ_ERR_INVALID_ARGUMENT, "tile_dtype must be F32, F16 or BF16");
+    if (d->max_tokens < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "max_tokens must be >= 1");
+    if (is_conv(*d)) {
+        if (d->conv_kh < 1 || d->conv_kw < 1 || d->conv_cin < 1 || d->conv_stride < 1 || d->conv_pad < 0 ||
+            d->in_h < 1 || d->in_w < 1)
+            return fail(AQ_ERR_INVALID_ARGUMENT, "bad convolution geometry");
+        if ((int64_t)d->conv_cin * d->conv_kh * d->conv_kw != d->in_features)
+            return fail(AQ_ERR_INVALID_ARGUMENT, "in_features must equal conv_cin*conv_kh*conv_kw");
+        if (d->in_h + 2 * d->conv_pad < d->conv_kh || d->in_w + 2 * d->conv_pad < d->conv_kw)
+            return fail(AQ_ERR_INVALID_ARGUMENT, "convolution output would be empty");
+        if (d->x_dtype == AQ_I8)
+            return fail(AQ_ERR_UNSUPPORTED, "int8 activations are supported for linear layers only");
+    }
+    return AQ_OK;
+}
+
+Geom make_geom(const aq_layer* L, int64_t n) {
+    Geom geo{};
+    const aq_layer_desc& d = L->desc;
+    geo.C_out = d.out_features;
+    geo.K = d.in_features;
+    geo.g = L->g;
+    geo.M = L->M;
+    geo.B = L->B;
+    geo.G = L->G;
+    geo.conv = is_conv(d);
+    if (geo.conv) {
+        geo.cin = d.conv_cin;
+        geo.kh = d.conv_kh;
+        geo.kw = d.conv_kw;
+        geo.stride = d.conv_stride;
+        geo.pad = d.conv_pad;
+        geo.H = d.in_h;
+        geo.W = d.in_w;
+        geo.OH = conv_out(d.in_h, d.conv_pad, d.conv_kh, d.conv_stride);
+        geo.OW = conv_out(d.in_w, d.conv_pad, d.conv_kw, d.conv_stride);
+        geo.tokens = n * (int64_t)geo.OH * geo.OW;
+    } else {
+        geo.tokens = n;
+    }
+    return geo;
+}
+
+aq_path choose(const aq_layer* L, int64_t tokens) {
+    if (L->path != AQ_PATH_AUTO) return L->path;
+    if (L->lut_ok && (!L->dec_ok || tokens <= L->lut_max_tokens)) return AQ_PATH_LUT;
+    return AQ_PATH_DECODE;
+}
+
+void free_layer(aq_layer* L) {
+    if (!L) return;
+    void* ptrs[] = {L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, L->d_ws};
+    for (void* p : ptrs)
+        if (p) (void)hipFree(p);
+    delete L;
+}
+
+template <typename T>
+aq_status dev_upload(T** dst, const void* src, size_t bytes, const char* what) {
+    hipError_t e = hipMalloc(reinterpret_cast<void**>(dst), bytes);
+    if (e != hipSuccess) {
+        *dst = nullptr;
+        return hip_fail(e, what);
+    }
+    if (src) {
+        e = hipMemcpy(*dst, src, bytes, hipMemcpyHostToDevice);
+        if (e != hipSuccess) return hip_fail(e, what);
+    }
+    return AQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* aq_last_error(void) { return g_err.c_str(); }
+
+const char* aq_version(void) { return "aq-mi355x 0.1.0 (gfx950)"; }
+
+aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, const void* codes, const float* scales,
+                          int g, int M, int B, aq_layer** out) {
+    g_err.clear();
+    if (out) *out = nullptr;
+    if (!desc || !codebooks || !codes || !scales || !out)
+        return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    aq_status st = validate_desc(desc, g, M, B);
+    if (st != AQ_OK) return st;
+
+    const int C_out = desc->out_features;
+    const int K = desc->in_features;
+    const int G = K / g;
+    const int64_t nk = (int64_t)1 << B;
+    const int64_t ncodes = (int64_t)C_out * G * M;
+    if (B <= 8) {
+        const uint8_t* c = static_cast<const uint8_t*>(codes);
+        for (int64_t i = 0; i < ncodes; ++i)
+            if (c[i] >= nk) return fail(AQ_ERR_INVALID_ARGUMENT, "code value >= 2^B at index " + std::to_string(i));
+    } else {
+        const uint16_t* c = static_cast<const uint16_t*>(codes);
+        for (int64_t i = 0; i < ncodes; ++i)
+            if (c[i] >= nk) return fail(AQ_ERR_INVALID_ARGUMENT, "code value >= 2^B at index " + std::to_string(i));
+    }
+    const bool lut_ok = B <= 8;
+    const bool dec_ok = desc->tile_dtype == AQ_F32 || g == 8;
+    if (!lut_ok && !dec_ok)
+        return fail(AQ_ERR_UNSUPPORTED, "no kernel for this format: LUT needs B <= 8, fp16/bf16 decode needs g == 8");
+
+    int ndev = 0;
+    hipError_t e = hipGetDeviceCount(&ndev);
+    if (e != hipSuccess || ndev < 1) return fail(AQ_ERR_DEVICE, "no HIP device available");
+
+    aq_layer* L = new aq_layer();
+    L->desc = *desc;
+    L->g = g;
+    L->M = M;
+    L->B = B;
+    L->G = G;
+    L->lut_ok = lut_ok;
+    L->dec_ok = dec_ok;
+    L->path = AQ_PATH_AUTO;
+    L->lut_max_tokens = 16;
+    if (const char* s = std::getenv("AQ_LUT_MAX_TOKENS")) L->lut_max_tokens = std::atoll(s);
+    e = hipGetDevice(&L->device);
+    if (e != hipSuccess) {
+        free_layer(L);
+        return hip_fail(e, "hipGetDevice");
+    }
+
+    const size_t cb_elems = (size_t)M * nk * g;
+    const size_t code_bytes = (size_t)ncodes * (B <= 8 ? 1 : 2);
+#define AQ_TRY(x)                \
+    do {                         \
+        aq_status s_ = (x);      \
+        if (s_ != AQ_OK) {       \
+            free_layer(L);       \
+            return s_;           \
+        }                        \
+    } while (0)
+    AQ_TRY(dev_upload(&L->d_cb, codebooks, cb_elems * dtype_bytes(desc->codebook_dtype), "codebooks"));
+    AQ_TRY(dev_upload(&L->d_cb32, nullptr, cb_elems * sizeof(float), "codebooks fp32"));
+    const bool want_tile_cb = B > 8 && M == 1 && desc->tile_dtype != AQ_F32;
+    if (want_tile_cb) AQ_TRY(dev_upload(&L->d_cbtile, nullptr, cb_elems * 2, "codebook tile"));
+    AQ_TRY(dev_upload(&L->d_codes, codes, code_bytes, "codes"));
+    AQ_TRY(dev_upload(&L->d_scales, scales, (size_t)C_out * sizeof(float), "scales"));
+
+    if (lut_ok) {
+        LutPlan& p = L->plan;
+        const int64_t per_group = (int64_t)M * nk;                   // table entries per group
+        int jc = (int)std::max<int64_t>(1, 4096 / per_group);
+        jc = std::min(jc, G);
+        jc = std::min(jc, 64);
+        p.jc = jc;
+        p.nchunk = (G + jc - 1) / jc;
+        int64_t tb = std::min<int64_t>(desc->max_tokens, 256);
+        tb = (tb + aq::kLutTokTile - 1) / aq::kLutTokTile * aq::kLutTokTile;
+        p.tok_block = (int)tb;
+        // codes regrouped per chunk: [nchunk][C_out][jc][M], zero padded past G
+        std::vector<uint8_t> rep((size_t)p.nchunk * C_out * jc * M, 0);
+        const uint8_t* c = static_cast<const uint8_t*>(codes);
+        for (int i = 0; i < C_out; ++i)
+            for (int j = 0; j < G; ++j) {
+                const int ch = j / jc, jj = j - ch * jc;
+                for (int m = 0; m < M; ++m)
+                    rep[(((size_t)ch * C_out + i) * jc + jj) * M + m] = c[((size_t)i * G + j) * M + m];
+            }
+        AQ_TRY(dev_upload(&L->d_codes_lut, rep.data(), rep.size(), "LUT codes"));
+        AQ_TRY(dev_upload(&L->d_ws, nullptr, (size_t)p.nchunk * p.tok_block * C_out * sizeof(float), "workspace"));
+    }
+
+    e = aq::launch_codebook_prep(L->d_cb, desc->codebook_dtype, (int64_t)cb_elems, L->d_cb32, L->d_cbtile,
+                                 desc->tile_dtype, nullptr);
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) {
+        free_layer(L);
+        return hip_fail(e, "codebook preparation");
+    }
+#undef AQ_TRY
+
+    if (const char* s = std::getenv("AQ_PATH")) {
+        if (!std::strcmp(s, "lut") && lut_ok) L->path = AQ_PATH_LUT;
+        else if (!std::strcmp(s, "decode") && dec_ok) L->path = AQ_PATH_DECODE;
+    }
+    *out = L;
+    return AQ_OK;
+}
+
+aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, void* Y, int64_t n, void* stream) {
+    if (!L || !X || !Y) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    if (n < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "n must be >= 1");
+    const aq_layer_desc& d = L->desc;
+    const Geom geo = make_geom(L, n);
+    if (geo.tokens > d.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens");
+    if (d.x_dtype == AQ_I8 && !x_scales) return fail(AQ_ERR_INVALID_ARGUMENT, "int8 activations need x_scales");
+    if ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 15)
+        return fail(AQ_ERR_INVALID_ARGUMENT, "X and Y must be 16-byte aligned");
+    const float* xs = d.x_dtype == AQ_I8 ? x_scales : nullptr;
+    const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, d.codebook_dtype};
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (choose(L, geo.tokens) == AQ_PATH_LUT)
+        e = aq::launch_lut_forward(geo, w, L->plan, X, d.x_dtype, xs, Y, d.y_dtype, L->d_ws, st);
+    else if (d.tile_dtype == AQ_F32)
+        e = aq::launch_f32_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, st);
+    else
+        e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
+    return AQ_OK;
+}
+
+aq_status aq_layer_decode(aq_layer* L, void* W, void* stream) {
+    if (!L || !W) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    const Geom geo = make_geom(L, 1);
+    const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales,
+                          L->desc.codebook_dtype};
+    hipError_t e = aq::launch_decode_to_global(geo, w, L->desc.tile_dtype, W, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "decode launch");
+    return AQ_OK;
+}
+
+aq_status aq_layer_set_path(aq_layer* L, aq_path path) {
+    if (!L) return fail(AQ_ERR_INVALID_ARGUMENT, "null layer");
+    if (path != AQ_PATH_AUTO && path != AQ_PATH_LUT && path != AQ_PATH_DECODE)
+        return fail(AQ_ERR_INVALID_ARGUMENT, "bad path");
+    if (path == AQ_PATH_LUT && !L->lut_ok) return fail(AQ_ERR_UNSUPPORTED, "LUT path needs B <= 8");
+    if (path == AQ_PATH_DECODE && !L->dec_ok)
+        return fail(AQ_ERR_UNSUPPORTED, "fp16/bf16 decode path needs g == 8");
+    L->path = path;
+    return AQ_OK;
+}
+
+aq_status aq_layer_choose_path(const aq_layer* L, int64_t tokens, aq_path* out) {
+    if (!L || !out) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    if (tokens < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens must be >= 1");
+    *out = choose(L, tokens);
+    return AQ_OK;
+}
+
+aq_status aq_layer_destroy(aq_layer* L) {
+    if (!L) return AQ_OK;
+    hipError_t e = hipDeviceSynchronize();
+    free_layer(L);
+    if (e != hipSuccess) return hip_fail(e, "destroy");
+    return AQ_OK;
+}
+
+}  // extern "C"

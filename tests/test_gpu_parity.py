@@ -1,0 +1,274 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Tolerances: infinity-norm relative error <= 2e-3 when weights are rounded to
+fp16/bf16 tiles, <= 1e-5 for fp32 tiles and fp32 LUT accumulation; decoded
+weights bit-exact against the fp32 decode emulation.
+"""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from workloads import ConvGeom, LayerSpec, generate
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f16": 2e-3, "bf16": 2e-3, "f32": 1e-5}
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU tests need an MI355X; none is visible")
+    import paper_2506_05960_amd as P
+    P.load_library()
+    yield
+
+
+def _dev(a, dtype_name):
+    if dtype_name == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _run(spec, inp, path="auto", max_tokens=None, stream=None):
+    import paper_2506_05960_amd as P
+    layer = P.AQLayer(spec, inp, max_tokens=max_tokens)
+    if path != "auto":
+        layer.set_path(path)
+    x = _dev(inp["x"], spec.x_dtype)
+    xs = None if inp["x_scales"] is None else torch.from_numpy(inp["x_scales"]).cuda()
+    if stream is not None:
+        with torch.cuda.stream(stream):
+            y = layer.forward(x, xs)
+    else:
+        y = layer.forward(x, xs)
+    torch.cuda.synchronize()
+    out = y.float().cpu().numpy().astype(np.float64)
+    layer.close()
+    return out
+
+
+def _tol(spec, path):
+    if path == "lut":
+        return 1e-5 if spec.y_dtype == "f32" else 2e-3
+    return TOL[spec.tile_dtype]
+
+
+# ---------------------------------------------------------------------------
+# decoded weights, bit-exact
+# ---------------------------------------------------------------------------
+
+DECODE_CASES = [
+    W.config_spec("tiny"),
+    W.config_spec("conv64"),
+    W.config_spec("qkv16"),
+    W.config_spec("conv8"),
+    LayerSpec(name="bf16tile", C_out=40, K=64, g=8, M=3, B=7, n=4, codebook_dtype="bf16", tile_dtype="bf16"),
+    LayerSpec(name="g9", C_out=17, K=27, g=9, M=2, B=5, n=4, tile_dtype="f32", codebook_dtype="f32"),
+    LayerSpec(name="b12", C_out=33, K=48, g=8, M=2, B=12, n=4),
+]
+
+
+@pytest.mark.parametrize("spec", DECODE_CASES, ids=lambda s: s.name)
+def test_decode_bit_exact(spec):
+    import paper_2506_05960_amd as P
+    _say(f"decode {spec.name}")
+    inp = generate(spec, 77)
+    layer = P.AQLayer(spec, inp, max_tokens=max(spec.tokens, 1))
+    w = layer.decode()
+    torch.cuda.synchronize()
+    got = w.cpu().numpy()
+    ref = O.decode_emulate(inp["codebooks"], inp["codes"], inp["scales"], spec.g, spec.codebook_dtype,
+                           spec.tile_dtype, scaled=True)
+    layer.close()
+    if spec.tile_dtype == "f32":
+        gb, rb = got.view(np.uint32), ref.view(np.uint32)
+    elif spec.tile_dtype == "f16":
+        gb, rb = got.view(np.uint16), ref.view(np.uint16)
+    else:
+        gb, rb = got.view(np.uint16), ref
+    bad = np.argwhere(gb != rb)
+    for i, k in bad[:8]:
+        _say(f"  mismatch W[{i},{k}] got=0x{int(gb[i, k]):x} ref=0x{int(rb[i, k]):x}")
+    assert len(bad) == 0, f"{len(bad)} of {gb.size} decoded weights differ"
+
+
+# ---------------------------------------------------------------------------
+# the four single-layer workloads, both paths where the format allows
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name,path", [
+    ("tiny", "lut"), ("tiny", "decode"), ("tiny", "auto"),
+    ("conv64", "decode"), ("conv64", "lut"),
+    ("qkv16", "decode"), ("qkv16", "lut"),
+    ("conv8", "decode"),
+])
+def test_config_parity(name, path):
+    spec = W.config_spec(name)
+    _say(f"config {name} path {path}")
+    inp = W.config_inputs(name)
+    y = _run(spec, inp, path)
+    y_ref = O.forward(spec, inp)
+    err = O.rel_err_inf(y, y_ref)
+    _say(f"  rel_err_inf={err:.3e}")
+    assert y.shape == y_ref.shape
+    assert err <= _tol(spec, path)
+
+
+# ---------------------------------------------------------------------------
+# odd shapes, formats and dtypes
+# ---------------------------------------------------------------------------
+
+ODD = [
+    LayerSpec(name="n1", C_out=70, K=64, g=8, M=2, B=8, n=1),
+    LayerSpec(name="ragged", C_out=131, K=200, g=8, M=3, B=6, n=37),
+    LayerSpec(name="cout1", C_out=1, K=96, g=8, M=2, B=8, n=130),
+    LayerSpec(name="k_eq_g", C_out=65, K=8, g=8, M=1, B=4, n=70),
+    LayerSpec(name="b1", C_out=64, K=64, g=8, M=4, B=1, n=66),
+    LayerSpec(name="b12_m2", C_out=96, K=128, g=8, M=2, B=12, n=150),
+    LayerSpec(name="b16_m1_lin", C_out=80, K=256, g=8, M=1, B=16, n=200),
+    LayerSpec(name="m8", C_out=64, K=64, g=8, M=8, B=8, n=64),
+    LayerSpec(name="f32x_f16tile", C_out=100, K=120, g=8, M=2, B=8, n=90, x_dtype="f32", codebook_dtype="f32"),
+    LayerSpec(name="bf16_all", C_out=72, K=64, g=8, M=2, B=8, n=77, x_dtype="bf16", codebook_dtype="bf16",
+              tile_dtype="bf16"),
+    LayerSpec(name="i8_bf16tile", C_out=72, K=64, g=8, M=2, B=8, n=77, x_dtype="i8", tile_dtype="bf16"),
+    LayerSpec(name="f32y", C_out=50, K=64, g=8, M=2, B=8, n=33, y_dtype="f32"),
+    LayerSpec(name="g9_f32", C_out=20, K=27, g=9, M=2, B=5, n=30, x_dtype="f32", y_dtype="f32",
+              codebook_dtype="f32", tile_dtype="f32"),
+    LayerSpec(name="conv_s2", C_out=48, K=64 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(64, 3, 3, 2, 1, 15, 13)),
+    LayerSpec(name="conv1x1", C_out=40, K=48, g=8, M=2, B=8, n=2, conv=ConvGeom(48, 1, 1, 1, 0, 9, 7)),
+    LayerSpec(name="conv_rect", C_out=24, K=16 * 6, g=8, M=2, B=8, n=2, conv=ConvGeom(16, 2, 3, 1, 0, 6, 5)),
+    LayerSpec(name="conv_b16", C_out=36, K=32 * 9, g=8, M=1, B=16, n=2, conv=ConvGeom(32, 3, 3, 1, 1, 5, 6)),
+    LayerSpec(name="conv_g9_lut", C_out=16, K=8 * 9, g=9, M=2, B=6, n=2, conv=ConvGeom(8, 3, 3, 1, 1, 6, 6),
+              tile_dtype="f32", y_dtype="f32", x_dtype="f32", codebook_dtype="f32"),
+]
+
+
+def _paths(spec):
+    p = []
+    if spec.B <= 8:
+        p.append("lut")
+    if spec.tile_dtype == "f32" or spec.g == 8:
+        p.append("decode")
+    return p
+
+
+@pytest.mark.parametrize("spec", ODD, ids=lambda s: s.name)
+def test_odd_shapes(spec):
+    inp = generate(spec, 1234)
+    y_ref = O.forward(spec, inp)
+    for path in _paths(spec):
+        _say(f"odd {spec.name} path {path}")
+        y = _run(spec, inp, path)
+        err = O.rel_err_inf(y, y_ref)
+        _say(f"  rel_err_inf={err:.3e}")
+        tol = 1e-5 if (path == "lut" or spec.tile_dtype == "f32") and spec.y_dtype == "f32" else 2e-3
+        assert err <= tol, (spec.name, path, err)
+
+
+# ---------------------------------------------------------------------------
+# exact checks through the fused path
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("M,B", [(3, 8), (2, 12), (1, 16)])
+def test_one_hot_rows_read_back_decoded_tile(M, B):
+    """X = identity (fp16) through the matrix-core path returns fl32(W_tile * s) exactly."""
+    spec = LayerSpec(name="onehot", C_out=160, K=256, g=8, M=M, B=B, n=256, y_dtype="f32")
+    inp = generate(spec, 99)
+    inp["x"] = np.eye(256, dtype=np.float16)
+    _say(f"onehot M={M} B={B}")
+    y = _run(spec, inp, "decode").astype(np.float32)
+    wt = O.decode_emulate(inp["codebooks"], inp["codes"], inp["scales"], 8, "f16", "f16", scaled=False)
+    ref = (wt.astype(np.float32) * inp["scales"][:, None]).astype(np.float32)   # [C_out, K]
+    assert np.array_equal(y.view(np.uint32), ref.T.copy().view(np.uint32))
+
+
+@pytest.mark.parametrize("path", ["decode", "lut"])
+def test_codebook_doubling_is_exact(path):
+    """Codebook values on a 2^-10 grid: every decode sum is exact, so Y(2C) == 2 Y(C) bitwise."""
+    spec = LayerSpec(name="alpha", C_out=96, K=128, g=8, M=2, B=8, n=100, y_dtype="f32")
+    inp = generate(spec, 5)
+    rng = np.random.default_rng(6)
+    inp["codebooks"] = (rng.integers(-512, 512, size=inp["codebooks"].shape) / 1024.0).astype(np.float16)
+    y1 = _run(spec, inp, path)
+    inp2 = dict(inp)
+    inp2["codebooks"] = (inp["codebooks"].astype(np.float32) * 2).astype(np.float16)
+    y2 = _run(spec, inp2, path)
+    assert np.array_equal(y2, 2.0 * y1)
+
+
+def test_repeat_runs_are_bitwise_deterministic():
+    spec = W.config_spec("qkv16").with_n(512)
+    inp = generate(spec, 3)
+    for path in ("decode", "lut"):
+        a = _run(spec, inp, path)
+        b = _run(spec, inp, path)
+        assert np.array_equal(a, b)
+
+
+def test_non_default_stream():
+    spec = LayerSpec(name="stream", C_out=128, K=256, g=8, M=2, B=8, n=300)
+    inp = generate(spec, 8)
+    s = torch.cuda.Stream()
+    y = _run(spec, inp, "decode", stream=s)
+    assert O.rel_err_inf(y, O.forward(spec, inp)) <= 2e-3
+
+
+def test_dispatch_choice():
+    import paper_2506_05960_amd as P
+    spec = LayerSpec(name="disp", C_out=128, K=256, g=8, M=2, B=8, n=4096)
+    inp = generate(spec, 1)
+    layer = P.AQLayer(spec, inp)
+    assert layer.choose_path(1) == "lut"
+    assert layer.choose_path(4096) == "decode"
+    layer.set_path("decode")
+    assert layer.choose_path(1) == "decode"
+    layer.close()
+    spec16 = LayerSpec(name="disp16", C_out=64, K=64, g=8, M=1, B=16, n=8)
+    layer = P.AQLayer(spec16, generate(spec16, 1))
+    assert layer.choose_path(1) == "decode"
+    with pytest.raises(P.AQError):
+        layer.set_path("lut")
+    layer.close()
+
+
+# ---------------------------------------------------------------------------
+# LDM-4-shaped sweep: sampled outputs at full size
+# ---------------------------------------------------------------------------
+
+def _sweep_sample():
+    layers = W.sweep_layers(full=True)
+    pick = ["down0.0.conv1", "down0.downsample", "down1.0.skip", "down1.0.tf.attn1.qkv",
+            "mid.tf.ff.in", "up3.0.conv1", "up1.0.tf.attn2.kv", "up0.2.conv2"]
+    by = {l.name: l for l in layers}
+    return [by[p] for p in pick]
+
+
+@pytest.mark.parametrize("layer", _sweep_sample(), ids=lambda l: l.name)
+@pytest.mark.parametrize("M", [2, 4])
+def test_sweep_layer_sampled(layer, M):
+    spec = W.sweep_spec(layer, M)
+    inp = generate(spec, 4242)
+    _say(f"sweep {spec.name} tokens={spec.tokens}")
+    y = _run(spec, inp, "auto")
+    rng = np.random.default_rng(0)
+    tok = rng.integers(0, spec.tokens, size=64)
+    ch = rng.integers(0, spec.C_out, size=48)
+    ref = O.forward_sampled(spec, inp, tok, ch)
+    if spec.conv is None:
+        got = y[np.ix_(tok, ch)]
+    else:
+        flat = y.transpose(0, 2, 3, 1).reshape(spec.tokens, spec.C_out)
+        got = flat[np.ix_(tok, ch)]
+    assert O.rel_err_inf(got, ref) <= 2e-3
