@@ -1,0 +1,615 @@
+// Fused decode + matrix-core forward (fp16 tiles, group size 8), gfx950.
+//
+// Work split.  A workgroup owns a BM (tokens) x BN (output channels) tile of Y
+// and its four waves split the reduction dimension: wave w takes K chunks
+// w, w+4, w+8, ... and accumulates the whole tile for them, so the main loop
+// needs no workgroup barrier.  At the end the four partial tiles meet in LDS
+// and each wave sums (in a fixed order) and stores a quarter of the tile.
+//
+// Operands.  v_mfma_f32_32x32x16_f16 takes 8 fp16 values per lane for each
+// operand; lane l holds row (l % 32) and a k-slice of 8 chosen by (l / 32).
+// Any assignment of the 16 logical k values of a step to (lane half, slot)
+// works as long as both operands use the same one.
+//  * Weights: each lane decodes its own groups straight into registers.  The
+//    codes a lane needs (one output channel, one half of a chunk's k-slices)
+//    are stored contiguously at create time, as byte offsets into the LDS
+//    codebook; a group is the sum of its M codewords (fp32 in ascending m, or
+//    an exact packed fp16 add when M = 2) rounded once to fp16.  The
+//    per-channel scale multiplies the fp32 accumulator in the epilogue.
+//  * Activations sit in a per-wave, double-buffered LDS staging area split
+//    into planes of 8 channels (or 8 consecutive k), 16 bytes per pixel (or
+//    token), so that one lane's 8 operand values are one 16-byte read and 16
+//    lanes read 256 contiguous bytes.
+//  * Linear layer: a chunk is 64 consecutive k (4 MFMA steps).
+//  * Convolution (implicit im2col): the staging area holds the input rows the
+//    token tile touches, with zero padding columns.  A 3x3 chunk is 16 input
+//    channels and one MFMA step is one kernel position (kh, kw) over them.
+//    The weight groups of a chunk run over (channel, kh, kw) with the channel
+//    outermost, so a lane decodes the 9 groups of its 8 channels and regroups
+//    the 72 values per position with byte permutes.  A 1x1 chunk is 64
+//    channels (4 steps).
+#pragma once
+
+#include <type_traits>
+
+#include "aq_device.h"
+
+namespace aq {
+
+constexpr int kWaves = 4;
+
+// Orders this wave's LDS accesses at the compiler level.  LDS instructions of
+// one wave execute in issue order, so no hardware wait is needed (a memory
+// fence here would also wait for the global prefetches in flight).
+__device__ __forceinline__ void wave_sync() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_wave_barrier();
+    asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ floatx16 mfma_f16(const u32x4& a, const u32x4& b, const floatx16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c, 0, 0,
+                                                  0);
+}
+
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t add_f16x2(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, a) + __builtin_bit_cast(half2v, b));
+}
+
+// Dword made of fp16 half `hlo` of xlo (low half) and half `hhi` of xhi (high half).
+__device__ __forceinline__ uint32_t pick2(uint32_t xlo, int hlo, uint32_t xhi, int hhi) {
+    const uint32_t sel = (uint32_t)(2 * hlo) | ((uint32_t)(2 * hlo + 1) << 8) | ((uint32_t)(4 + 2 * hhi) << 16) |
+                         ((uint32_t)(5 + 2 * hhi) << 24);
+    return __builtin_amdgcn_perm(xhi, xlo, sel);
+}
+
+// Raw buffer resource over `bytes` bytes; loads at offsets >= bytes return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0,
+                                             (int)(uint32_t)(bytes < 0xFFFFFFFFull ? bytes : 0xFFFFFFFFull), 0x00020000);
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;   // byte offset past every buffer this kernel reads
+
+// Quotient of non-negative a < 2^24 by d >= 1 through an fp32 reciprocal,
+// corrected to the exact integer quotient.
+__device__ __forceinline__ int fdiv(int a, int d, float inv_d) {
+    int qt = (int)((float)a * inv_d);
+    qt += (qt + 1) * d <= a;
+    qt -= qt * d > a;
+    return qt;
+}
+
+// Raw codewords of one group as read from the codebook: M x 16 bytes (fp16)
+// or M x 32 bytes (fp32).
+template <int DEC, int MC>
+struct GroupRaw {
+    u32x4 w[DEC == FUSED_DEC_F32L ? 2 * MC : MC];
+};
+
+// Issue the codebook reads of one group.  With an LDS codebook `ent` holds M
+// byte offsets into LDS; with a global codebook it holds the code.
+template <int DEC, int MC, typename EntT>
+__device__ __forceinline__ void gather_group(GroupRaw<DEC, MC>& g, const EntT* ent, const uint8_t* cb_lds,
+                                             const void* cb_glob) {
+    if constexpr (DEC == FUSED_DEC_T16G) {
+        g.w[0] = static_cast<const u32x4*>(cb_glob)[ent[0]];
+    } else if constexpr (DEC == FUSED_DEC_F32L) {
+#pragma unroll
+        for (int m = 0; m < MC; ++m) {
+            const u32x4* p = reinterpret_cast<const u32x4*>(cb_lds + ent[m]);
+            g.w[2 * m] = p[0];
+            g.w[2 * m + 1] = p[1];
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < MC; ++m) g.w[m] = *reinterpret_cast<const u32x4*>(cb_lds + ent[m]);
+    }
+}
+
+// Sum the gathered codewords of one group and round once to fp16 (4 dwords).
+template <int DEC, int MC>
+__device__ __forceinline__ u32x4 combine_group(const GroupRaw<DEC, MC>& g) {
+    if constexpr (DEC == FUSED_DEC_PK16) {
+        // exact: for two fp16 addends the fp16 sum equals the fp32 sum rounded to fp16
+        u32x4 r;
+        r[0] = add_f16x2(g.w[0][0], g.w[1][0]);
+        r[1] = add_f16x2(g.w[0][1], g.w[1][1]);
+        r[2] = add_f16x2(g.w[0][2], g.w[1][2]);
+        r[3] = add_f16x2(g.w[0][3], g.w[1][3]);
+        return r;
+    } else if constexpr (DEC == FUSED_DEC_F32L) {
+        float s[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            s[e] = __uint_as_float(g.w[0][e]);
+            s[4 + e] = __uint_as_float(g.w[1][e]);
+        }
+#pragma unroll
+        for (int m = 1; m < MC; ++m)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                s[e] = __fadd_rn(s[e], __uint_as_float(g.w[2 * m][e]));
+                s[4 + e] = __fadd_rn(s[4 + e], __uint_as_float(g.w[2 * m + 1][e]));
+            }
+        u32x4 r;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            const float a = opaque_f32(s[2 * d]), b = opaque_f32(s[2 * d + 1]);
+            r[d] = (uint32_t)f32_to_f16(a) | ((uint32_t)f32_to_f16(b) << 16);
+        }
+        return r;
+    } else {   // M == 1: the codeword is already the fp16 weight
+        return g.w[0];
+    }
+}
+
+// 8 fp16 values from 8 int8 values, exactly: the fp16 bit pattern
+// 0x6400 | (x ^ 0x80) encodes 1024 + (x + 128), and subtracting 1152 (exact for
+// integers below 2048) leaves x.
+__device__ __forceinline__ u32x4 i8x8_to_f16(uint64_t q) {
+    const uint32_t lo = (uint32_t)q ^ 0x80808080u, hi = (uint32_t)(q >> 32) ^ 0x80808080u;
+    const uint32_t k64 = 0x64646464u;
+    const uint32_t bias = 0xE480E480u;   // fp16 -1152 in both halves
+    u32x4 r;
+    r[0] = add_f16x2(__builtin_amdgcn_perm(k64, lo, 0x04010400u), bias);
+    r[1] = add_f16x2(__builtin_amdgcn_perm(k64, lo, 0x04030402u), bias);
+    r[2] = add_f16x2(__builtin_amdgcn_perm(k64, hi, 0x04010400u), bias);
+    r[3] = add_f16x2(__builtin_amdgcn_perm(k64, hi, 0x04030402u), bias);
+    return r;
+}
+
+// KIND: 0 linear, 1 conv 3x3, 2 conv 1x1.
+template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL>
+__global__ void __launch_bounds__(256, 1)
+fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const uint8_t* __restrict__ crec,
+                 const float* __restrict__ scales, const void* __restrict__ X, const float* __restrict__ x_scales,
+                 void* __restrict__ Y, int y_dtype) {
+    constexpr bool CONV = KIND != 0;
+    constexpr int KH = KIND == 1 ? 3 : 1;
+    constexpr int NS = KIND == 1 ? 9 : CM;         // MFMA steps per chunk (= groups per lane)
+    constexpr int AM = BM / 32, AN = BN / 32;
+    using EntT = uint16_t;                         // LDS byte offset, or a code (global codebook)
+    static_assert(KIND != 1 || CM == 1, "3x3 chunks are 16 channels");
+    static_assert(DEC != FUSED_DEC_PK16 || MC == 2, "packed fp16 decode is for M = 2");
+
+    extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int l32 = lane & 31;
+    const int q = lane >> 5;
+    const int T0 = (int)blockIdx.x * BM;            // token and element counts fit in 31 bits (host check)
+    const int N0 = (int)blockIdx.y * BN;
+    const int tokens = (int)geo.tokens;
+
+    // ---- codebook: global -> registers (stored to LDS once the first chunk's loads are in flight) ----
+    uint8_t* cb_lds = lds;
+    constexpr int CB_PER_T = DEC == FUSED_DEC_F32L ? (4 * 256 * 32) / (16 * 256) : (2 * 256 * 16) / (16 * 256);
+    u32x4 cbr[CB_PER_T];
+    if constexpr (DEC != FUSED_DEC_T16G) {
+        const int n16 = plan.cb_bytes / 16;
+        const u32x4* src = static_cast<const u32x4*>(cb);
+#pragma unroll
+        for (int i = 0; i < CB_PER_T; ++i) {
+            const int idx = tid + 256 * i;
+            cbr[i] = idx < n16 ? src[idx] : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
+    uint8_t* pbuf0 = lds + plan.cb_bytes + wave * 2 * plan.pbuf_bytes;
+    uint8_t* pbuf1 = pbuf0 + plan.pbuf_bytes;
+
+    // ---- per-lane addressing, computed once (a chunk only adds a uniform offset) ----
+    const int HW = CONV ? geo.H * geo.W : 0;
+    uint32_t a_base[AM];            // byte offset of this lane's A slice in a staging buffer
+    uint32_t g_off[UPL];            // element offset of the unit's first value for chunk 0
+    uint32_t l_off[UPL];            // byte offset of the unit's destination in a staging buffer
+    bool g_ok[UPL];                 // the unit loads data (false: zeros)
+    bool l_ok[UPL];                 // the unit exists
+    int k_first[UPL];               // linear: first k of the unit for chunk 0
+    if constexpr (CONV) {
+        const float inv_ow = 1.0f / (float)geo.OW, inv_oh = 1.0f / (float)geo.OH;
+        const float inv_pr = 1.0f / (float)plan.pr;
+        const int gr0 = fdiv(T0, geo.OW, inv_ow);
+#pragma unroll
+        for (int a = 0; a < AM; ++a) {
+            const int T = T0 + 32 * a + l32;
+            const int gT = fdiv(T, geo.OW, inv_ow);
+            const int r = gT - gr0;
+            const int ow = T - gT * geo.OW;
+            a_base[a] = (uint32_t)(q * plan.ps + ((r * KH) * plan.pw + ow * geo.stride) * 16);
+        }
+        const int wp = geo.W >> 1;  // pixel pairs per row
+        const float inv_wp = 1.0f / (float)wp;
+#pragma unroll
+        for (int j = 0; j < UPL; ++j) {
+            const int u = lane + 64 * j;
+            const int t = fdiv(u, wp, inv_wp);
+            const int pp = u - t * wp;
+            const int o = fdiv(t, plan.pr, inv_pr);
+            const int pr = t - o * plan.pr;
+            const int r = pr / KH, kh = pr - r * KH;
+            const int gr = gr0 + r;
+            const int b = fdiv(gr, geo.OH, inv_oh), oh = gr - b * geo.OH;
+            const int ih = oh * geo.stride - geo.pad + kh;
+            l_ok[j] = u < plan.units;
+            g_ok[j] = l_ok[j] && gr < plan.total_rows && ih >= 0 && ih < geo.H;
+            g_off[j] = g_ok[j] ? (uint32_t)(((b * geo.cin + 8 * o) * geo.H + ih) * geo.W + 2 * pp) : 0u;
+            l_off[j] = l_ok[j] ? (uint32_t)(o * plan.ps + (pr * plan.pw + 2 * pp + geo.pad) * 16)
+                               : (uint32_t)(plan.pbuf_bytes - 32);
+            k_first[j] = 0;
+        }
+        // zero the padding columns of both buffers once: (buffer, plane, row, pad column)
+        const int padc = plan.pw - geo.W;
+        const int nrow = 2 * 2 * CM * plan.pr;
+        for (int i = lane; i < nrow * padc; i += 64) {
+            const int row = i / padc, pcx = i - row * padc;       // padc is 2 * pad, a small constant
+            const int bsel = row & 1, rest = row >> 1;
+            const int o = fdiv(rest, plan.pr, inv_pr), pr = rest - o * plan.pr;
+            const int pcol = pcx < geo.pad ? pcx : geo.W + pcx;
+            uint8_t* dst = (bsel ? pbuf1 : pbuf0) + o * plan.ps + (pr * plan.pw + pcol) * 16;
+            *reinterpret_cast<u32x4*>(dst) = u32x4{0u, 0u, 0u, 0u};
+        }
+    } else {
+#pragma unroll
+        for (int a = 0; a < AM; ++a) a_base[a] = (uint32_t)(q * plan.ps + (32 * a + l32) * 16);
+#pragma unroll
+        for (int j = 0; j < UPL; ++j) {
+            const int u = lane + 64 * j;
+            const int o = u % (2 * CM);
+            const int tt = u / (2 * CM);
+            const int T = T0 + tt;
+            l_ok[j] = u < plan.units;
+            g_ok[j] = l_ok[j] && T < tokens;
+            k_first[j] = 8 * o;
+            g_off[j] = g_ok[j] ? (uint32_t)(T * geo.K + 8 * o) : 0u;
+            l_off[j] = l_ok[j] ? (uint32_t)(o * plan.ps + tt * 16) : (uint32_t)(plan.pbuf_bytes - 32);
+        }
+    }
+    uint32_t c_off[AN];
+    bool c_ok[AN];
+#pragma unroll
+    for (int b = 0; b < AN; ++b) {
+        const int n = N0 + 32 * b + l32;
+        c_ok[b] = n < geo.C_out;
+        c_off[b] = c_ok[b] ? (uint32_t)((n * 2 + q) * plan.rec_bytes) : 0u;
+    }
+    const uint32_t chunk_rec_stride = (uint32_t)geo.C_out * 2u * (uint32_t)plan.rec_bytes;
+
+    // ---- staging of one chunk: global -> registers (out-of-range offsets read zeros) ----
+    constexpr int SREG = CONV ? 8 : 4;    // dwords per unit
+    constexpr int XB = XT == AQ_I8 ? 1 : 2;   // bytes per activation
+    const uint64_t xbytes = CONV ? (uint64_t)plan.total_rows / geo.OH * geo.cin * HW * 2
+                                 : (uint64_t)geo.tokens * geo.K * XB;
+    const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(X, xbytes);
+    uint32_t stage[UPL][SREG];
+    auto stage_load = [&](int chunk) {
+#pragma unroll
+        for (int j = 0; j < UPL; ++j) {
+            if constexpr (CONV) {
+                // 8 channels x 2 pixels
+                const uint32_t base = g_ok[j] ? (g_off[j] + (uint32_t)(chunk * 16 * CM) * HW) * 2u : kOutOfRange;
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    stage[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, 0);
+            } else {
+                const int k = chunk * 16 * CM + k_first[j];
+                const bool ok = g_ok[j] && k < geo.K;
+                const uint32_t off = ok ? (g_off[j] + (uint32_t)(chunk * 16 * CM)) * XB : kOutOfRange;
+                if constexpr (XT == AQ_I8) {
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 0);
+                    stage[j][0] = v[0];
+                    stage[j][1] = v[1];
+                } else {
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+                    stage[j][0] = v[0]; stage[j][1] = v[1]; stage[j][2] = v[2]; stage[j][3] = v[3];
+                }
+            }
+        }
+    };
+    // registers -> LDS buffer (channel transpose for a convolution)
+    auto stage_store = [&](uint8_t* buf) {
+#pragma unroll
+        for (int j = 0; j < UPL; ++j) {
+            uint8_t* dst = buf + l_off[j];   // units past the end write a spare slot
+            if constexpr (CONV) {
+                u32x4 p0, p1;   // pixel 0 / pixel 1, channels 0..7
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    p0[d] = pick2(stage[j][2 * d], 0, stage[j][2 * d + 1], 0);
+                    p1[d] = pick2(stage[j][2 * d], 1, stage[j][2 * d + 1], 1);
+                }
+                reinterpret_cast<u32x4*>(dst)[0] = p0;
+                reinterpret_cast<u32x4*>(dst)[1] = p1;
+            } else {
+                u32x4 v;
+                if constexpr (XT == AQ_I8) v = i8x8_to_f16((uint64_t)stage[j][0] | ((uint64_t)stage[j][1] << 32));
+                else v = u32x4{stage[j][0], stage[j][1], stage[j][2], stage[j][3]};
+                *reinterpret_cast<u32x4*>(dst) = v;
+            }
+        }
+    };
+
+    // ---- code records of one chunk: global -> registers ----
+    constexpr int REC_DW = (NS * MC * 2 + 15) / 16 * 4;   // record dwords
+    const __amdgpu_buffer_rsrc_t cr = buffer_rsrc(crec, (uint64_t)plan.nchunk * chunk_rec_stride);
+    uint32_t crg[AN][REC_DW];
+    auto codes_load = [&](int chunk) {
+#pragma unroll
+        for (int b = 0; b < AN; ++b) {
+            const uint32_t off = c_ok[b] ? c_off[b] + (uint32_t)chunk * chunk_rec_stride : kOutOfRange;
+#pragma unroll
+            for (int d = 0; d < REC_DW; d += 4) {
+                const auto v = __builtin_amdgcn_raw_buffer_load_b128(cr, off + 4 * d, 0, 0);
+                crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2]; crg[b][d + 3] = v[3];
+            }
+        }
+    };
+
+    // scales of this thread's epilogue task (one task per thread for every tile used)
+    constexpr int EROWS = CONV ? BN : BM, ECOLS = CONV ? BM : BN;
+    float esc[8];
+    float exs[4];
+    {
+        const int task = tid;
+        const int c8 = (task / (EROWS / 4)) * 8;
+        const int rq = task - (task / (EROWS / 4)) * (EROWS / 4);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) esc[i] = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) exs[e] = 1.0f;
+        if (task < (EROWS / 4) * (ECOLS / 8)) {
+            if constexpr (CONV) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int co = N0 + 4 * rq + e;
+                    esc[e] = co < geo.C_out ? scales[co] : 0.0f;
+                }
+            } else {
+#pragma unroll
+                for (int c = 0; c < 8; ++c) {
+                    const int co = N0 + c8 + c;
+                    esc[c] = co < geo.C_out ? scales[co] : 0.0f;
+                }
+                if (x_scales) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int tok = T0 + 4 * rq + e;
+                        exs[e] = tok < tokens ? x_scales[tok] : 1.0f;
+                    }
+                }
+            }
+        }
+    }
+
+    floatx16 acc[AM][AN];
+#pragma unroll
+    for (int a = 0; a < AM; ++a)
+#pragma unroll
+        for (int b = 0; b < AN; ++b)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+
+    int chunk = wave;
+    if (chunk < plan.nchunk) {
+        stage_load(chunk);
+        codes_load(chunk);
+    }
+    if constexpr (DEC != FUSED_DEC_T16G) {
+        const int n16 = plan.cb_bytes / 16;
+#pragma unroll
+        for (int i = 0; i < CB_PER_T; ++i) {
+            const int idx = tid + 256 * i;
+            if (idx < n16) reinterpret_cast<u32x4*>(cb_lds)[idx] = cbr[i];
+        }
+    }
+    __syncthreads();   // codebook and padding visible
+    if (chunk < plan.nchunk) stage_store(pbuf0);
+    int it = 0;
+    for (; chunk < plan.nchunk; chunk += kWaves, ++it) {
+        uint8_t* cur = (it & 1) ? pbuf1 : pbuf0;
+        uint8_t* nxt = (it & 1) ? pbuf0 : pbuf1;
+        const bool more = chunk + kWaves < plan.nchunk;
+
+        if (more) {
+            stage_load(chunk + kWaves);   // next chunk's activations and codes, consumed after this chunk
+        }
+        uint32_t crn[AN][REC_DW];
+#pragma unroll
+        for (int b = 0; b < AN; ++b)
+#pragma unroll
+            for (int d = 0; d < REC_DW; ++d) crn[b][d] = crg[b][d];
+        if (more) codes_load(chunk + kWaves);
+        wave_sync();   // this wave's staging writes are ordered before its reads below
+
+        // Block b + 1's codewords are read and summed while block b's MFMAs run
+        // (when a block of raw codewords fits in registers).
+        constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L;
+        u32x4 dec[NS];
+        if constexpr (LOOKAHEAD) {
+            GroupRaw<DEC, MC> raw[NS];
+            const EntT* ev = reinterpret_cast<const EntT*>(crn[0]);
+#pragma unroll
+            for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
+#pragma unroll
+            for (int g = 0; g < NS; ++g) dec[g] = combine_group<DEC, MC>(raw[g]);
+        }
+#pragma unroll
+        for (int b = 0; b < AN; ++b) {
+            __builtin_amdgcn_sched_barrier(0);
+            u32x4 dnext[NS];
+            if constexpr (LOOKAHEAD) {
+                if (b + 1 < AN) {
+                    GroupRaw<DEC, MC> raw[NS];
+                    const EntT* ev = reinterpret_cast<const EntT*>(crn[b + 1]);
+#pragma unroll
+                    for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
+#pragma unroll
+                    for (int g = 0; g < NS; ++g) dnext[g] = combine_group<DEC, MC>(raw[g]);
+                }
+            } else {
+                GroupRaw<DEC, MC> raw1;
+                const EntT* ev = reinterpret_cast<const EntT*>(crn[b]);
+#pragma unroll
+                for (int g = 0; g < NS; ++g) {
+                    gather_group<DEC, MC, EntT>(raw1, ev + g * MC, cb_lds, cb);
+                    dec[g] = combine_group<DEC, MC>(raw1);
+                }
+            }
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                u32x4 bf;
+                if constexpr (KIND == 1) {
+                    // position s: channel e of the lane's 8 is decoded value 9e + s
+#pragma unroll
+                    for (int d = 0; d < 4; ++d) {
+                        const int v0 = 9 * (2 * d) + s, v1 = 9 * (2 * d + 1) + s;
+                        bf[d] = pick2(dec[v0 >> 3][(v0 & 7) >> 1], v0 & 1, dec[v1 >> 3][(v1 & 7) >> 1], v1 & 1);
+                    }
+                } else {
+                    bf = dec[s];
+                }
+                uint32_t soff;
+                if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
+                else soff = (uint32_t)(2 * s * plan.ps);
+#pragma unroll
+                for (int a = 0; a < AM; ++a) {
+                    const u32x4 af = *reinterpret_cast<const u32x4*>(cur + a_base[a] + soff);
+                    if constexpr (CONV) acc[a][b] = mfma_f16(bf, af, acc[a][b]);   // rows: channels
+                    else acc[a][b] = mfma_f16(af, bf, acc[a][b]);                  // rows: tokens
+                }
+            }
+            if constexpr (LOOKAHEAD) {
+                if (b + 1 < AN) {
+#pragma unroll
+                    for (int g = 0; g < NS; ++g) dec[g] = dnext[g];
+                }
+            }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if (more) {
+            wave_sync();
+            stage_store(nxt);
+        }
+    }
+
+    // ---- epilogue: the four partial tiles meet in LDS, interleaved by 4 along
+    // the MFMA row so that each lane writes float4s; then every thread sums 8
+    // columns x 4 rows over the partials, scales, converts and writes four
+    // 16-byte row segments.  Rows are output channels (convolution) or tokens
+    // (linear); columns are tokens (convolution) or output channels (linear).
+    constexpr int ROWS = CONV ? BN : BM;     // MFMA A rows of the tile
+    constexpr int COLS = CONV ? BM : BN;     // MFMA B columns of the tile
+    __syncthreads();   // every wave is done with its staging buffers
+    // [wave][ROWS / 4][COLS + 1] float4; the padding float4 puts consecutive row
+    // quads 4 banks apart, so the epilogue's reads (row quad fastest across
+    // lanes) are conflict free
+    constexpr int COLSP = COLS + 1;
+    floatx4* red = reinterpret_cast<floatx4*>(lds + plan.cb_bytes);
+#pragma unroll
+    for (int a = 0; a < AM; ++a)
+#pragma unroll
+        for (int b = 0; b < AN; ++b)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                // register quad i holds rows 8 i + 4 q + (0..3) of the 32 x 32 block
+                const int row0 = (CONV ? 32 * b : 32 * a) + 8 * i + 4 * q;
+                const int col = (CONV ? 32 * a : 32 * b) + l32;
+                red[(wave * (ROWS / 4) + row0 / 4) * COLSP + col] =
+                    floatx4{acc[a][b][4 * i], acc[a][b][4 * i + 1], acc[a][b][4 * i + 2], acc[a][b][4 * i + 3]};
+            }
+    __syncthreads();
+    const int ybytes = y_dtype == AQ_F32 ? 4 : 2;
+    const __amdgpu_buffer_rsrc_t yr = buffer_rsrc(Y, (uint64_t)geo.tokens * geo.C_out * ybytes);
+    const int plane = CONV ? geo.OH * geo.OW : 0;
+    constexpr int TASKS = (ROWS / 4) * (COLS / 8);   // (4 rows, 8 columns) per task
+    static_assert(TASKS <= 256, "one epilogue task per thread");
+    const int task = tid;
+    if (task < TASKS) {
+        const int c8 = (task / (ROWS / 4)) * 8;
+        const int rq = task - (task / (ROWS / 4)) * (ROWS / 4);
+        floatx4 pv[kWaves][8];
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w)
+#pragma unroll
+            for (int c = 0; c < 8; ++c) pv[w][c] = red[(w * (ROWS / 4) + rq) * COLSP + c8 + c];
+        floatx4 v[8];
+#pragma unroll
+        for (int c = 0; c < 8; ++c) v[c] = ((pv[0][c] + pv[1][c]) + pv[2][c]) + pv[3][c];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int row = 4 * rq + e;
+            float o[8];
+            int yi0, ncol;
+            if constexpr (CONV) {
+                const int co = N0 + row;
+                const int tok0 = T0 + c8;
+#pragma unroll
+                for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[e];
+                const int bimg = tok0 / plane;
+                yi0 = (bimg * geo.C_out + co) * plane + (tok0 - bimg * plane);
+                ncol = co < geo.C_out ? min(8, tokens - tok0) : 0;
+                if (ncol == 8 && plane % 8 != 0) ncol = -1;   // may cross an image: element stores
+            } else {
+                const int tok = T0 + row;
+                const int co0 = N0 + c8;
+#pragma unroll
+                for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[c] * exs[e];
+                yi0 = tok * geo.C_out + co0;
+                ncol = tok < tokens ? min(8, geo.C_out - co0) : 0;
+                if (ncol == 8 && geo.C_out % 8 != 0) ncol = -1;   // unaligned row: element stores
+            }
+            if (ncol == 8) {
+                if (y_dtype == AQ_F32) {
+                    __builtin_amdgcn_raw_buffer_store_b128(
+                        u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3])},
+                        yr, yi0 * 4, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b128(
+                        u32x4{__float_as_uint(o[4]), __float_as_uint(o[5]), __float_as_uint(o[6]), __float_as_uint(o[7])},
+                        yr, yi0 * 4 + 16, 0, 0);
+                } else {
+                    u32x4 h;
+#pragma unroll
+                    for (int d = 0; d < 4; ++d)
+                        h[d] = (uint32_t)f32_to_f16(o[2 * d]) | ((uint32_t)f32_to_f16(o[2 * d + 1]) << 16);
+                    __builtin_amdgcn_raw_buffer_store_b128(h, yr, yi0 * 2, 0, 0);
+                }
+            } else if (ncol != 0) {
+                const int n = ncol < 0 ? 8 : ncol;
+                for (int c = 0; c < n; ++c) {
+                    int yi;
+                    if constexpr (CONV) {
+                        const int tk = T0 + c8 + c;
+                        if (tk >= tokens) break;
+                        const int bb = tk / plane;
+                        yi = (bb * geo.C_out + N0 + row) * plane + (tk - bb * plane);
+                    } else {
+                        if (N0 + c8 + c >= geo.C_out) break;
+                        yi = yi0 + c;
+                    }
+                    if (y_dtype == AQ_F32) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o[c]), yr, yi * 4, 0, 0);
+                    else __builtin_amdgcn_raw_buffer_store_b16(f32_to_f16(o[c]), yr, yi * 2, 0, 0);
+                }
+            }
+        }
+    }
+}
+
+template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL>
+static hipError_t fused_launch_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
+    auto kern = fused_fwd_kernel<KIND, CM, XT, DEC, MC, BM, BN, UPL>;
+    static size_t attr_bytes = 0;
+    if (plan.lds_bytes > attr_bytes) {
+        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)plan.lds_bytes);
+        if (e != hipSuccess) return e;
+        attr_bytes = plan.lds_bytes;
+    }
+    const dim3 grid((unsigned)((geo.tokens + BM - 1) / BM), (unsigned)((geo.C_out + BN - 1) / BN));
+    kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.cb, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y,
+                                                   fl.y_dtype);
+    return hipGetLastError();
+}
+
+}  // namespace aq

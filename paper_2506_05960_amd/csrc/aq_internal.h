@@ -38,6 +38,49 @@ struct LutPlan {
 
 constexpr int kLutTokTile = 4;    // tokens per LUT entry (one 16-byte table read)
 
+// ---- fused decode + matrix-core path (fp16 tiles, g == 8) ----
+
+enum FusedDec {
+    FUSED_DEC_PK16 = 0,   // M == 2, fp16 codebooks in LDS, packed fp16 add (exact)
+    FUSED_DEC_F32L = 1,   // fp32 codebooks in LDS, fp32 sum in ascending m
+    FUSED_DEC_T16L = 2,   // M == 1, codebook pre-rounded to fp16, in LDS
+    FUSED_DEC_T16G = 3    // M == 1, codebook pre-rounded to fp16, read from global memory (B > 8)
+};
+
+struct FusedPlan {
+    int kind;             // 0 linear, 1 conv 3x3, 2 conv 1x1
+    int cm;               // 16-wide k steps per chunk (per kernel position for a convolution)
+    int nchunk;           // chunks along K
+    int rec_bytes;        // code record bytes per (chunk, output channel, lane half)
+    int dec;              // FusedDec
+    int mc;               // M
+    int cb_bytes;         // LDS codebook bytes (0 when read from global memory)
+    // chosen per forward
+    int bm, bn, upl;      // tile and staging units per lane
+    int units;            // staging units per chunk
+    int pr, pw, ps;       // patch rows, patch width (pixels), pixel / token-row stride (bytes)
+    int pbuf_bytes;       // one staging buffer
+    int total_rows;       // convolution: images * OH
+    size_t lds_bytes;     // dynamic LDS per workgroup
+};
+
+struct FusedLaunch {
+    const void* cb;       // codebook source (LDS copy source or global table)
+    const uint8_t* crec;  // code records
+    const float* scales;
+    const void* X;
+    const float* x_scales;
+    void* Y;
+    int y_dtype;
+    int x_dtype;
+    hipStream_t stream;
+};
+
+hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+hipError_t launch_fused_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+hipError_t launch_fused_conv1(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+hipError_t launch_fused_linear(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+
 // ---- launchers (each returns the launch's hipError_t) ----
 
 hipError_t launch_decode_to_global(const Geom& geo, const DeviceWeights& w, int tile_dtype, void* W,

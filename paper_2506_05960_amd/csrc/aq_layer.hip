@@ -1,6 +1,7 @@
 // C ABI entry points: argument validation (host only, before any HIP call),
 // device copies and repacking of the quantized weights, path dispatch.
 #include <algorithm>
+#include <cstdio>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
@@ -25,7 +26,9 @@ struct aq_layer {
     float* d_scales;
     float* d_ws;
     LutPlan plan;
-    bool lut_ok, dec_ok;
+    aq::FusedPlan fplan;
+    uint8_t* d_crec;          // fused-path code records (null when the fused path does not apply)
+    bool lut_ok, dec_ok, fused_ok;
     aq_path path;
     int64_t lut_max_tokens;
 };
@@ -121,7 +124,7 @@ aq_path choose(const aq_layer* L, int64_t tokens) {
 
 void free_layer(aq_layer* L) {
     if (!L) return;
-    void* ptrs[] = {L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, L->d_ws};
+    void* ptrs[] = {L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, L->d_ws, L->d_crec};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete L;
@@ -139,6 +142,141 @@ aq_status dev_upload(T** dst, const void* src, size_t bytes, const char* what) {
         if (e != hipSuccess) return hip_fail(e, what);
     }
     return AQ_OK;
+}
+
+// ---- fused decode + matrix-core path: eligibility, code records, tiles ----
+
+constexpr size_t kLdsBytes = 160 * 1024;
+
+// Decide whether the fused path applies and fill the create-time part of the plan.
+bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPlan* p) {
+    std::memset(p, 0, sizeof(*p));
+    if (d.tile_dtype != AQ_F16 || g != 8) return false;
+    const bool conv = is_conv(d);
+    if (conv) {
+        if (d.x_dtype != AQ_F16 || d.in_w % 2 != 0) return false;
+        if (d.conv_kh == 3 && d.conv_kw == 3 && d.conv_cin % 16 == 0) {
+            p->kind = 1;
+            p->cm = 1;
+            p->nchunk = d.conv_cin / 16;
+        } else if (d.conv_kh == 1 && d.conv_kw == 1 && d.conv_pad == 0 && d.conv_cin % 64 == 0) {
+            p->kind = 2;
+            p->cm = 4;
+            p->nchunk = d.conv_cin / 64;
+        } else {
+            return false;
+        }
+    } else {
+        if (d.x_dtype != AQ_F16 && d.x_dtype != AQ_I8) return false;
+        p->kind = 0;
+        p->cm = 4;
+        p->nchunk = (d.in_features + 63) / 64;
+    }
+    if (M == 2 && B <= 8 && d.codebook_dtype == AQ_F16) {
+        p->dec = aq::FUSED_DEC_PK16;
+        p->cb_bytes = 2 * (1 << B) * 16;
+    } else if (M == 4 && B <= 8) {
+        p->dec = aq::FUSED_DEC_F32L;
+        p->cb_bytes = 4 * (1 << B) * 32;
+    } else if (M == 1 && B > 8) {
+        p->dec = aq::FUSED_DEC_T16G;
+        p->cb_bytes = 0;
+    } else {
+        return false;
+    }
+    p->mc = M;
+    const int ns = p->kind == 1 ? 9 : p->cm;
+    p->rec_bytes = (ns * M * 2 + 15) / 16 * 16;
+    return true;
+}
+
+// Code records: for chunk c, output channel n and lane half q, one 16-bit
+// entry per (group the lane decodes, codebook m), in decode order.  With an
+// LDS codebook the entry is the codeword's byte offset in LDS; with a global
+// codebook it is the code itself.
+std::vector<uint8_t> fused_records(const aq::FusedPlan& p, const void* codes, int C_out, int G, int M, int B) {
+    const int ns = p.kind == 1 ? 9 : p.cm;
+    const int nk = 1 << B;
+    const int row_bytes = p.dec == aq::FUSED_DEC_F32L ? 32 : 16;   // bytes per LDS codeword
+    std::vector<uint8_t> rec((size_t)p.nchunk * C_out * 2 * p.rec_bytes, 0);
+    for (int c = 0; c < p.nchunk; ++c)
+        for (int n = 0; n < C_out; ++n)
+            for (int q = 0; q < 2; ++q) {
+                uint16_t* r = reinterpret_cast<uint16_t*>(rec.data() + (((size_t)c * C_out + n) * 2 + q) * p.rec_bytes);
+                for (int s = 0; s < ns; ++s) {
+                    const int j = p.kind == 1 ? 18 * c + 9 * q + s : c * 2 * p.cm + 2 * s + q;
+                    for (int m = 0; m < M; ++m) {
+                        uint32_t code = 0;
+                        if (j < G) {
+                            const size_t src = ((size_t)n * G + j) * M + m;
+                            code = B <= 8 ? static_cast<const uint8_t*>(codes)[src]
+                                          : static_cast<const uint16_t*>(codes)[src];
+                        }
+                        const uint32_t ent = p.dec == aq::FUSED_DEC_T16G ? code : ((uint32_t)m * nk + code) * row_bytes;
+                        r[s * M + m] = (uint16_t)ent;
+                    }
+                }
+            }
+    return rec;
+}
+
+struct TileCand {
+    int bm, bn, upl;
+};
+
+// Per-forward tile choice; fills the remaining plan fields.  Returns false when
+// no instantiated tile fits (the caller then uses the generic kernel).
+bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
+    static const TileCand conv3[] = {{64, 96, 3}, {64, 64, 3}, {128, 64, 6}, {64, 64, 6}};
+    static const TileCand conv1[] = {{64, 96, 4}, {64, 64, 4}};
+    static const TileCand lin[] = {{64, 96, 8}, {64, 64, 8}, {32, 128, 4}, {32, 64, 4}};
+    const TileCand* cands = p->kind == 1 ? conv3 : p->kind == 2 ? conv1 : lin;
+    const int ncand = p->kind == 1 ? 4 : p->kind == 2 ? 2 : 4;
+    int want_bm = 0, want_bn = 0;
+    if (const char* s = std::getenv("AQ_FUSED_TILE")) std::sscanf(s, "%dx%d", &want_bm, &want_bn);
+    double best = 0;
+    aq::FusedPlan bestp{};
+    bool found = false;
+    for (int i = 0; i < ncand; ++i) {
+        const TileCand& t = cands[i];
+        if (want_bm && (t.bm != want_bm || t.bn != want_bn)) continue;
+        aq::FusedPlan q = *p;
+        q.bm = t.bm;
+        q.bn = t.bn;
+        q.upl = t.upl;
+        if (p->kind != 0) {
+            if (!(t.bm % geo.OW == 0 || geo.OW % t.bm == 0)) continue;
+            const int tr = t.bm >= geo.OW ? t.bm / geo.OW : 1;
+            const int kh = p->kind == 1 ? 3 : 1;
+            q.pr = tr * kh;
+            q.pw = geo.W + 2 * geo.pad;
+            q.ps = q.pr * q.pw * 16;                    // one plane of 8 channels
+            q.units = 2 * p->cm * q.pr * (geo.W / 2);   // (plane, row, pixel pair)
+            q.total_rows = (int)(geo.tokens / geo.OW);
+        } else {
+            q.pr = q.pw = 0;
+            q.ps = t.bm * 16 + 16;                      // one plane of 8 consecutive k
+            q.units = t.bm * 2 * p->cm;                 // (token, plane)
+            q.total_rows = 0;
+        }
+        q.pbuf_bytes = 2 * p->cm * q.ps + 32;       // + a spare slot for padding units
+        if ((q.units + 63) / 64 > t.upl) continue;
+        const size_t rows = p->kind != 0 ? t.bn : t.bm, cols = p->kind != 0 ? t.bm : t.bn;
+        const size_t red = (size_t)4 * (rows / 4) * (cols + 1) * 16;       // four padded partial tiles
+        q.lds_bytes = (size_t)p->cb_bytes + std::max<size_t>((size_t)8 * q.pbuf_bytes, red);
+        if (q.lds_bytes > kLdsBytes) continue;
+        const int64_t nwg = ((geo.tokens + t.bm - 1) / t.bm) * (int64_t)((geo.C_out + t.bn - 1) / t.bn);
+        const int64_t rounds = (nwg + 255) / 256;
+        // rounds of whole-chip work, weighted by a per-tile overhead term
+        const double cost = (double)rounds * t.bm * t.bn * (1.0 + 48.0 / t.bm + 48.0 / t.bn) * t.upl / (t.upl + 2.0);
+        if (!found || cost < best) {
+            best = cost;
+            bestp = q;
+            found = true;
+        }
+    }
+    if (found) *p = bestp;
+    return found;
 }
 
 }  // namespace
@@ -239,6 +377,12 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
         AQ_TRY(dev_upload(&L->d_ws, nullptr, (size_t)p.nchunk * p.tok_block * C_out * sizeof(float), "workspace"));
     }
 
+    L->fused_ok = fused_plan_create(*desc, g, M, B, &L->fplan);
+    if (L->fused_ok) {
+        std::vector<uint8_t> rec = fused_records(L->fplan, codes, C_out, G, M, B);
+        AQ_TRY(dev_upload(&L->d_crec, rec.data(), rec.size(), "fused code records"));
+    }
+
     e = aq::launch_codebook_prep(L->d_cb, desc->codebook_dtype, (int64_t)cb_elems, L->d_cb32, L->d_cbtile,
                                  desc->tile_dtype, nullptr);
     if (e == hipSuccess) e = hipDeviceSynchronize();
@@ -273,8 +417,21 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
         e = aq::launch_lut_forward(geo, w, L->plan, X, d.x_dtype, xs, Y, d.y_dtype, L->d_ws, st);
     else if (d.tile_dtype == AQ_F32)
         e = aq::launch_f32_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, st);
-    else
-        e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
+    else {
+        aq::FusedPlan fp = L->fplan;
+        // the fused kernel uses 32-bit element and byte offsets
+        const bool fits31 = geo.tokens * (int64_t)std::max(geo.K, geo.C_out) * 4 < (int64_t(1) << 31) &&
+                            (!geo.conv || n * (int64_t)geo.cin * geo.H * geo.W * 2 < (int64_t(1) << 31));
+        if (L->fused_ok && fits31 && !std::getenv("AQ_NO_FUSED") && fused_plan_tile(geo, &fp)) {
+            const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
+                                : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
+                                                               : L->d_cbtile;
+            const aq::FusedLaunch fl{cbsrc, L->d_crec, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
+            e = aq::launch_fused_forward(geo, fp, fl);
+        } else {
+            e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
+        }
+    }
     if (e != hipSuccess) return hip_fail(e, "forward launch");
     return AQ_OK;
 }

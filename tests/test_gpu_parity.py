@@ -178,10 +178,58 @@ def test_odd_shapes(spec):
 
 
 # ---------------------------------------------------------------------------
+# fused decode + matrix-core kernel against the generic kernel and the oracle
+# ---------------------------------------------------------------------------
+
+FUSED = [
+    LayerSpec(name="f_conv3_s1", C_out=80, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 24, 16)),
+    LayerSpec(name="f_conv3_s2", C_out=64, K=48 * 9, g=8, M=2, B=8, n=2, conv=ConvGeom(48, 3, 3, 2, 1, 16, 16)),
+    LayerSpec(name="f_conv3_m4", C_out=100, K=16 * 9, g=8, M=4, B=8, n=2, conv=ConvGeom(16, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="f_conv3_b16", C_out=70, K=64 * 9, g=8, M=1, B=16, n=5, conv=ConvGeom(64, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="f_conv3_wide", C_out=40, K=16 * 9, g=8, M=2, B=8, n=1, conv=ConvGeom(16, 3, 3, 1, 1, 3, 128)),
+    LayerSpec(name="f_conv1", C_out=72, K=128, g=8, M=2, B=8, n=2, conv=ConvGeom(128, 1, 1, 1, 0, 16, 24)),
+    LayerSpec(name="f_conv1_m4", C_out=33, K=64, g=8, M=4, B=7, n=3, conv=ConvGeom(64, 1, 1, 1, 0, 8, 8)),
+    LayerSpec(name="f_lin_tail", C_out=150, K=200, g=8, M=2, B=8, n=77),
+    LayerSpec(name="f_lin_i8", C_out=200, K=136, g=8, M=4, B=8, n=45, x_dtype="i8"),
+    LayerSpec(name="f_lin_b16", C_out=96, K=512, g=8, M=1, B=16, n=300),
+    LayerSpec(name="f_lin_f32y", C_out=64, K=64, g=8, M=2, B=8, n=1000, y_dtype="f32"),
+]
+
+
+@pytest.mark.parametrize("spec", FUSED, ids=lambda s: s.name)
+def test_fused_matches_oracle_and_generic(spec, monkeypatch):
+    inp = generate(spec, 2024)
+    y_ref = O.forward(spec, inp)
+    _say(f"fused {spec.name}")
+    y_fused = _run(spec, inp, "decode")
+    e1 = O.rel_err_inf(y_fused, y_ref)
+    monkeypatch.setenv("AQ_NO_FUSED", "1")
+    y_gen = _run(spec, inp, "decode")
+    monkeypatch.delenv("AQ_NO_FUSED")
+    e2 = O.rel_err_inf(y_gen, y_ref)
+    _say(f"  fused err={e1:.3e} generic err={e2:.3e}")
+    assert e1 <= 2e-3 and e2 <= 2e-3
+
+
+@pytest.mark.parametrize("tile", ["64x96", "64x64", "128x64", "32x128", "32x64"])
+def test_fused_tiles(tile, monkeypatch):
+    """Every instantiated tile of the fused kernel on a conv and a linear layer."""
+    monkeypatch.setenv("AQ_FUSED_TILE", tile)
+    for spec in (LayerSpec(name="t_conv", C_out=200, K=32 * 9, g=8, M=2, B=8, n=2,
+                           conv=ConvGeom(32, 3, 3, 1, 1, 16, 16)),
+                 LayerSpec(name="t_lin", C_out=200, K=192, g=8, M=2, B=8, n=150)):
+        inp = generate(spec, 7)
+        y = _run(spec, inp, "decode")
+        err = O.rel_err_inf(y, O.forward(spec, inp))
+        _say(f"tile {tile} {spec.name} err={err:.3e}")
+        assert err <= 2e-3
+
+
+# ---------------------------------------------------------------------------
 # exact checks through the fused path
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("M,B", [(3, 8), (2, 12), (1, 16)])
+@pytest.mark.parametrize("M,B", [(3, 8), (2, 12), (1, 16), (2, 8), (4, 8), (4, 6)])
 def test_one_hot_rows_read_back_decoded_tile(M, B):
     """X = identity (fp16) through the matrix-core path returns fl32(W_tile * s) exactly."""
     spec = LayerSpec(name="onehot", C_out=160, K=256, g=8, M=M, B=B, n=256, y_dtype="f32")
