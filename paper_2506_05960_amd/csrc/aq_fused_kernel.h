@@ -88,8 +88,9 @@ struct GroupRaw {
     u32x4 w[DEC == FUSED_DEC_F32L ? 2 * MC : MC];
 };
 
-// Issue the codebook reads of one group.  With an LDS codebook `ent` holds M
-// byte offsets into LDS; with a global codebook it holds the code.
+// Issue the codebook reads of one group.  `ent` holds the group's M codes.
+// The LDS codebook keeps 256 rows per codebook (rows past 2^B unused), so
+// codebook m starts at a fixed byte offset and a codeword address is a shift.
 template <int DEC, int MC, typename EntT>
 __device__ __forceinline__ void gather_group(GroupRaw<DEC, MC>& g, const EntT* ent, const uint8_t* cb_lds,
                                              const void* cb_glob) {
@@ -98,13 +99,14 @@ __device__ __forceinline__ void gather_group(GroupRaw<DEC, MC>& g, const EntT* e
     } else if constexpr (DEC == FUSED_DEC_F32L) {
 #pragma unroll
         for (int m = 0; m < MC; ++m) {
-            const u32x4* p = reinterpret_cast<const u32x4*>(cb_lds + ent[m]);
+            const u32x4* p = reinterpret_cast<const u32x4*>(cb_lds + m * 256 * 32 + (uint32_t)ent[m] * 32u);
             g.w[2 * m] = p[0];
             g.w[2 * m + 1] = p[1];
         }
     } else {
 #pragma unroll
-        for (int m = 0; m < MC; ++m) g.w[m] = *reinterpret_cast<const u32x4*>(cb_lds + ent[m]);
+        for (int m = 0; m < MC; ++m)
+            g.w[m] = *reinterpret_cast<const u32x4*>(cb_lds + m * 256 * 16 + (uint32_t)ent[m] * 16u);
     }
 }
 
@@ -170,7 +172,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     constexpr int KH = KIND == 1 ? 3 : 1;
     constexpr int NS = KIND == 1 ? 9 : CM;         // MFMA steps per chunk (= groups per lane)
     constexpr int AM = BM / 32, AN = BN / 32;
-    using EntT = uint16_t;                         // LDS byte offset, or a code (global codebook)
+    using EntT = typename std::conditional<DEC == FUSED_DEC_T16G, uint16_t, uint8_t>::type;   // one code
     static_assert(KIND != 1 || CM == 1, "3x3 chunks are 16 channels");
     static_assert(DEC != FUSED_DEC_PK16 || MC == 2, "packed fp16 decode is for M = 2");
 
@@ -180,21 +182,40 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     const int wave = tid >> 6;
     const int l32 = lane & 31;
     const int q = lane >> 5;
-    const int T0 = (int)blockIdx.x * BM;            // token and element counts fit in 31 bits (host check)
-    const int N0 = (int)blockIdx.y * BN;
+    // XCD-aware tile order: consecutive workgroup ids go to the 8 XCDs in turn,
+    // so id h runs on XCD h % 8.  Giving each XCD a contiguous range of logical
+    // tiles (output-channel tile fastest) keeps the input rows a token tile
+    // shares with its neighbours, and with its other channel tiles, in one L2.
+    int tile_m, tile_n;
+    {
+        const int nwg = (int)gridDim.x, h = (int)blockIdx.x;
+        const int xcd = h & 7, j = h >> 3;
+        const int per = nwg >> 3, rem = nwg & 7;
+        const int L = xcd * per + min(xcd, rem) + j;
+        const int ntn = (geo.C_out + BN - 1) / BN;
+        tile_m = L / ntn;
+        tile_n = L - tile_m * ntn;
+    }
+    const int T0 = tile_m * BM;                     // token and element counts fit in 31 bits (host check)
+    const int N0 = tile_n * BN;
     const int tokens = (int)geo.tokens;
 
     // ---- codebook: global -> registers (stored to LDS once the first chunk's loads are in flight) ----
+    // LDS layout [m][256 rows][row bytes]; the source is [m][2^B rows][row bytes].
     uint8_t* cb_lds = lds;
-    constexpr int CB_PER_T = DEC == FUSED_DEC_F32L ? (4 * 256 * 32) / (16 * 256) : (2 * 256 * 16) / (16 * 256);
-    u32x4 cbr[CB_PER_T];
+    constexpr int ROWB = DEC == FUSED_DEC_F32L ? 32 : 16;
+    constexpr int CB_PER_T = DEC == FUSED_DEC_T16G ? 0 : (MC * 256 * ROWB) / (16 * 256);
+    u32x4 cbr[CB_PER_T > 0 ? CB_PER_T : 1];
+    const int rows_b = 1 << geo.B;
     if constexpr (DEC != FUSED_DEC_T16G) {
-        const int n16 = plan.cb_bytes / 16;
         const u32x4* src = static_cast<const u32x4*>(cb);
 #pragma unroll
         for (int i = 0; i < CB_PER_T; ++i) {
-            const int idx = tid + 256 * i;
-            cbr[i] = idx < n16 ? src[idx] : u32x4{0u, 0u, 0u, 0u};
+            const int idx = tid + 256 * i;                 // 16-byte unit of the LDS layout
+            const int m = idx / (256 * ROWB / 16);
+            const int rem = idx - m * (256 * ROWB / 16);
+            const int row = rem / (ROWB / 16), part = rem - row * (ROWB / 16);
+            cbr[i] = row < rows_b ? src[(m * rows_b + row) * (ROWB / 16) + part] : u32x4{0u, 0u, 0u, 0u};
         }
     }
     uint8_t* pbuf0 = lds + plan.cb_bytes + wave * 2 * plan.pbuf_bytes;
@@ -235,7 +256,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             const int ih = oh * geo.stride - geo.pad + kh;
             l_ok[j] = u < plan.units;
             g_ok[j] = l_ok[j] && gr < plan.total_rows && ih >= 0 && ih < geo.H;
-            g_off[j] = g_ok[j] ? (uint32_t)(((b * geo.cin + 8 * o) * geo.H + ih) * geo.W + 2 * pp) : 0u;
+            g_off[j] = g_ok[j] ? (uint32_t)(__umul24(__umul24(b, geo.cin) + 8 * o, geo.H) + ih) * (uint32_t)geo.W + 2u * pp : 0u;
             l_off[j] = l_ok[j] ? (uint32_t)(o * plan.ps + (pr * plan.pw + 2 * pp + geo.pad) * 16)
                                : (uint32_t)(plan.pbuf_bytes - 32);
             k_first[j] = 0;
@@ -332,7 +353,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     };
 
     // ---- code records of one chunk: global -> registers ----
-    constexpr int REC_DW = (NS * MC * 2 + 15) / 16 * 4;   // record dwords
+    constexpr int REC_DW = (NS * MC * (int)sizeof(EntT) + 3) / 4;   // record dwords
     const __amdgpu_buffer_rsrc_t cr = buffer_rsrc(crec, (uint64_t)plan.nchunk * chunk_rec_stride);
     uint32_t crg[AN][REC_DW];
     auto codes_load = [&](int chunk) {
@@ -341,8 +362,20 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             const uint32_t off = c_ok[b] ? c_off[b] + (uint32_t)chunk * chunk_rec_stride : kOutOfRange;
 #pragma unroll
             for (int d = 0; d < REC_DW; d += 4) {
-                const auto v = __builtin_amdgcn_raw_buffer_load_b128(cr, off + 4 * d, 0, 0);
-                crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2]; crg[b][d + 3] = v[3];
+                if constexpr (true) {
+                    if (d + 4 <= REC_DW) {
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b128(cr, off + 4 * d, 0, 0);
+                        crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2]; crg[b][d + 3] = v[3];
+                    } else if (d + 3 == REC_DW) {
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b96(cr, off + 4 * d, 0, 0);
+                        crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2];
+                    } else if (d + 2 == REC_DW) {
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b64(cr, off + 4 * d, 0, 0);
+                        crg[b][d] = v[0]; crg[b][d + 1] = v[1];
+                    } else {
+                        crg[b][d] = __builtin_amdgcn_raw_buffer_load_b32(cr, off + 4 * d, 0, 0);
+                    }
+                }
             }
         }
     };
@@ -391,71 +424,88 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
 
+    // activation fragments of one chunk: every (step, token block)
+    auto load_af = [&](const uint8_t* buf, u32x4 (&af)[NS][AM]) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            uint32_t soff;
+            if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
+            else soff = (uint32_t)(2 * s * plan.ps);
+#pragma unroll
+            for (int a = 0; a < AM; ++a) af[s][a] = *reinterpret_cast<const u32x4*>(buf + a_base[a] + soff);
+        }
+    };
+    // weights of one 32-channel block of a chunk, decoded into MFMA operands
+    auto decode_block = [&](const uint32_t* codes_dw, u32x4 (&d)[NS]) {
+        const EntT* ev = reinterpret_cast<const EntT*>(codes_dw);
+        if constexpr (DEC != FUSED_DEC_F32L) {
+            GroupRaw<DEC, MC> raw[NS];
+#pragma unroll
+            for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
+#pragma unroll
+            for (int g = 0; g < NS; ++g) d[g] = combine_group<DEC, MC>(raw[g]);
+        } else {
+            GroupRaw<DEC, MC> raw1;
+#pragma unroll
+            for (int g = 0; g < NS; ++g) {
+                gather_group<DEC, MC, EntT>(raw1, ev + g * MC, cb_lds, cb);
+                d[g] = combine_group<DEC, MC>(raw1);
+            }
+        }
+    };
+    // Software pipeline: the next block's codewords (for the last block, block 0
+    // of this wave's next chunk) are read and summed while the current block's
+    // MFMAs run, and the next chunk's activation fragments are read right after
+    // its staging store, so a chunk starts with its operands in flight.  The
+    // fp32-codebook mode keeps no look-ahead (a block of raw fp32 codewords does
+    // not fit in registers).
+    constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L;
     int chunk = wave;
+    u32x4 af[NS][AM];
+    u32x4 dec[NS];
     if (chunk < plan.nchunk) {
         stage_load(chunk);
         codes_load(chunk);
     }
     if constexpr (DEC != FUSED_DEC_T16G) {
-        const int n16 = plan.cb_bytes / 16;
 #pragma unroll
-        for (int i = 0; i < CB_PER_T; ++i) {
-            const int idx = tid + 256 * i;
-            if (idx < n16) reinterpret_cast<u32x4*>(cb_lds)[idx] = cbr[i];
-        }
+        for (int i = 0; i < CB_PER_T; ++i) reinterpret_cast<u32x4*>(cb_lds)[tid + 256 * i] = cbr[i];
     }
     __syncthreads();   // codebook and padding visible
-    if (chunk < plan.nchunk) stage_store(pbuf0);
+    if (chunk < plan.nchunk) {
+        stage_store(pbuf0);
+        wave_sync();
+        load_af(pbuf0, af);
+        if constexpr (LOOKAHEAD) decode_block(crg[0], dec);
+    }
     int it = 0;
     for (; chunk < plan.nchunk; chunk += kWaves, ++it) {
-        uint8_t* cur = (it & 1) ? pbuf1 : pbuf0;
         uint8_t* nxt = (it & 1) ? pbuf0 : pbuf1;
         const bool more = chunk + kWaves < plan.nchunk;
-
-        if (more) {
-            stage_load(chunk + kWaves);   // next chunk's activations and codes, consumed after this chunk
-        }
         uint32_t crn[AN][REC_DW];
 #pragma unroll
         for (int b = 0; b < AN; ++b)
 #pragma unroll
             for (int d = 0; d < REC_DW; ++d) crn[b][d] = crg[b][d];
-        if (more) codes_load(chunk + kWaves);
-        wave_sync();   // this wave's staging writes are ordered before its reads below
-
-        // Block b + 1's codewords are read and summed while block b's MFMAs run
-        // (when a block of raw codewords fits in registers).
-        constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L;
-        u32x4 dec[NS];
-        if constexpr (LOOKAHEAD) {
-            GroupRaw<DEC, MC> raw[NS];
-            const EntT* ev = reinterpret_cast<const EntT*>(crn[0]);
-#pragma unroll
-            for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
-#pragma unroll
-            for (int g = 0; g < NS; ++g) dec[g] = combine_group<DEC, MC>(raw[g]);
+        if (more) {
+            stage_load(chunk + kWaves);   // next chunk's activations and codes
+            codes_load(chunk + kWaves);
         }
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
             __builtin_amdgcn_sched_barrier(0);
             u32x4 dnext[NS];
+            bool have_next = false;
             if constexpr (LOOKAHEAD) {
                 if (b + 1 < AN) {
-                    GroupRaw<DEC, MC> raw[NS];
-                    const EntT* ev = reinterpret_cast<const EntT*>(crn[b + 1]);
-#pragma unroll
-                    for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
-#pragma unroll
-                    for (int g = 0; g < NS; ++g) dnext[g] = combine_group<DEC, MC>(raw[g]);
+                    decode_block(crn[b + 1], dnext);
+                    have_next = true;
+                } else if (more) {
+                    decode_block(crg[0], dnext);   // block 0 of the next chunk
+                    have_next = true;
                 }
             } else {
-                GroupRaw<DEC, MC> raw1;
-                const EntT* ev = reinterpret_cast<const EntT*>(crn[b]);
-#pragma unroll
-                for (int g = 0; g < NS; ++g) {
-                    gather_group<DEC, MC, EntT>(raw1, ev + g * MC, cb_lds, cb);
-                    dec[g] = combine_group<DEC, MC>(raw1);
-                }
+                decode_block(crn[b], dec);
             }
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
@@ -470,27 +520,23 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                 } else {
                     bf = dec[s];
                 }
-                uint32_t soff;
-                if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
-                else soff = (uint32_t)(2 * s * plan.ps);
 #pragma unroll
                 for (int a = 0; a < AM; ++a) {
-                    const u32x4 af = *reinterpret_cast<const u32x4*>(cur + a_base[a] + soff);
-                    if constexpr (CONV) acc[a][b] = mfma_f16(bf, af, acc[a][b]);   // rows: channels
-                    else acc[a][b] = mfma_f16(af, bf, acc[a][b]);                  // rows: tokens
+                    if constexpr (CONV) acc[a][b] = mfma_f16(bf, af[s][a], acc[a][b]);   // rows: channels
+                    else acc[a][b] = mfma_f16(af[s][a], bf, acc[a][b]);                  // rows: tokens
                 }
             }
-            if constexpr (LOOKAHEAD) {
-                if (b + 1 < AN) {
+            if (have_next) {
 #pragma unroll
-                    for (int g = 0; g < NS; ++g) dec[g] = dnext[g];
-                }
+                for (int g = 0; g < NS; ++g) dec[g] = dnext[g];
             }
         }
         __builtin_amdgcn_sched_barrier(0);
         if (more) {
             wave_sync();
             stage_store(nxt);
+            wave_sync();
+            load_af(nxt, af);
         }
     }
 
@@ -537,30 +583,39 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         floatx4 v[8];
 #pragma unroll
         for (int c = 0; c < 8; ++c) v[c] = ((pv[0][c] + pv[1][c]) + pv[2][c]) + pv[3][c];
+        // Columns are tokens (convolution: 8 consecutive tokens stay in one image
+        // plane when the plane size is a multiple of 8) or output channels
+        // (linear: 16-byte aligned when C_out is a multiple of 8).
+        int col0, ncols, rows_left;
+        bool aligned;
+        if constexpr (CONV) {
+            col0 = T0 + c8;
+            ncols = min(8, tokens - col0);
+            rows_left = geo.C_out - (N0 + 4 * rq);
+            aligned = plane % 8 == 0;
+        } else {
+            col0 = N0 + c8;
+            ncols = min(8, geo.C_out - col0);
+            rows_left = tokens - (T0 + 4 * rq);
+            aligned = geo.C_out % 8 == 0;
+        }
+        if (ncols == 8 && aligned) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int row = 4 * rq + e;
-            float o[8];
-            int yi0, ncol;
-            if constexpr (CONV) {
-                const int co = N0 + row;
-                const int tok0 = T0 + c8;
+            for (int e = 0; e < 4; ++e) {
+                if (e >= rows_left) break;
+                int yi0;
+                float o[8];
+                if constexpr (CONV) {
+                    const int co = N0 + 4 * rq + e;
+                    const int bimg = col0 / plane;
+                    yi0 = (bimg * geo.C_out + co) * plane + (col0 - bimg * plane);
 #pragma unroll
-                for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[e];
-                const int bimg = tok0 / plane;
-                yi0 = (bimg * geo.C_out + co) * plane + (tok0 - bimg * plane);
-                ncol = co < geo.C_out ? min(8, tokens - tok0) : 0;
-                if (ncol == 8 && plane % 8 != 0) ncol = -1;   // may cross an image: element stores
-            } else {
-                const int tok = T0 + row;
-                const int co0 = N0 + c8;
+                    for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[e];
+                } else {
+                    yi0 = (T0 + 4 * rq + e) * geo.C_out + col0;
 #pragma unroll
-                for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[c] * exs[e];
-                yi0 = tok * geo.C_out + co0;
-                ncol = tok < tokens ? min(8, geo.C_out - co0) : 0;
-                if (ncol == 8 && geo.C_out % 8 != 0) ncol = -1;   // unaligned row: element stores
-            }
-            if (ncol == 8) {
+                    for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[c] * exs[e];
+                }
                 if (y_dtype == AQ_F32) {
                     __builtin_amdgcn_raw_buffer_store_b128(
                         u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3])},
@@ -575,23 +630,23 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                         h[d] = (uint32_t)f32_to_f16(o[2 * d]) | ((uint32_t)f32_to_f16(o[2 * d + 1]) << 16);
                     __builtin_amdgcn_raw_buffer_store_b128(h, yr, yi0 * 2, 0, 0);
                 }
-            } else if (ncol != 0) {
-                const int n = ncol < 0 ? 8 : ncol;
-                for (int c = 0; c < n; ++c) {
-                    int yi;
-                    if constexpr (CONV) {
-                        const int tk = T0 + c8 + c;
-                        if (tk >= tokens) break;
-                        const int bb = tk / plane;
-                        yi = (bb * geo.C_out + N0 + row) * plane + (tk - bb * plane);
-                    } else {
-                        if (N0 + c8 + c >= geo.C_out) break;
-                        yi = yi0 + c;
-                    }
-                    if (y_dtype == AQ_F32) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o[c]), yr, yi * 4, 0, 0);
-                    else __builtin_amdgcn_raw_buffer_store_b16(f32_to_f16(o[c]), yr, yi * 2, 0, 0);
-                }
             }
+        } else {
+            for (int e = 0; e < 4 && e < rows_left; ++e)
+                for (int c = 0; c < ncols; ++c) {
+                    int yi;
+                    float o;
+                    if constexpr (CONV) {
+                        const int tk = col0 + c, bb = tk / plane;
+                        yi = (bb * geo.C_out + N0 + 4 * rq + e) * plane + (tk - bb * plane);
+                        o = v[c][e] * esc[e];
+                    } else {
+                        yi = (T0 + 4 * rq + e) * geo.C_out + col0 + c;
+                        o = v[c][e] * esc[c] * exs[e];
+                    }
+                    if (y_dtype == AQ_F32) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o), yr, yi * 4, 0, 0);
+                    else __builtin_amdgcn_raw_buffer_store_b16(f32_to_f16(o), yr, yi * 2, 0, 0);
+                }
         }
     }
 }
@@ -606,7 +661,7 @@ static hipError_t fused_launch_cfg(const Geom& geo, const FusedPlan& plan, const
         if (e != hipSuccess) return e;
         attr_bytes = plan.lds_bytes;
     }
-    const dim3 grid((unsigned)((geo.tokens + BM - 1) / BM), (unsigned)((geo.C_out + BN - 1) / BN));
+    const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN)));
     kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.cb, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y,
                                                    fl.y_dtype);
     return hipGetLastError();

@@ -174,10 +174,10 @@ bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPla
     }
     if (M == 2 && B <= 8 && d.codebook_dtype == AQ_F16) {
         p->dec = aq::FUSED_DEC_PK16;
-        p->cb_bytes = 2 * (1 << B) * 16;
+        p->cb_bytes = 2 * 256 * 16;             // LDS keeps 256 rows per codebook
     } else if (M == 4 && B <= 8) {
         p->dec = aq::FUSED_DEC_F32L;
-        p->cb_bytes = 4 * (1 << B) * 32;
+        p->cb_bytes = 4 * 256 * 32;
     } else if (M == 1 && B > 8) {
         p->dec = aq::FUSED_DEC_T16G;
         p->cb_bytes = 0;
@@ -186,34 +186,29 @@ bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPla
     }
     p->mc = M;
     const int ns = p->kind == 1 ? 9 : p->cm;
-    p->rec_bytes = (ns * M * 2 + 15) / 16 * 16;
+    const int ent_b = p->dec == aq::FUSED_DEC_T16G ? 2 : 1;
+    p->rec_bytes = (ns * M * ent_b + 3) / 4 * 4;
     return true;
 }
 
-// Code records: for chunk c, output channel n and lane half q, one 16-bit
-// entry per (group the lane decodes, codebook m), in decode order.  With an
-// LDS codebook the entry is the codeword's byte offset in LDS; with a global
-// codebook it is the code itself.
+// Code records: for chunk c, output channel n and lane half q, the M codes of
+// every group the lane decodes, in decode order (8-bit codes, or 16-bit codes
+// when B > 8), padded to whole dwords.
 std::vector<uint8_t> fused_records(const aq::FusedPlan& p, const void* codes, int C_out, int G, int M, int B) {
     const int ns = p.kind == 1 ? 9 : p.cm;
-    const int nk = 1 << B;
-    const int row_bytes = p.dec == aq::FUSED_DEC_F32L ? 32 : 16;   // bytes per LDS codeword
+    const int ent_b = p.dec == aq::FUSED_DEC_T16G ? 2 : 1;
     std::vector<uint8_t> rec((size_t)p.nchunk * C_out * 2 * p.rec_bytes, 0);
     for (int c = 0; c < p.nchunk; ++c)
         for (int n = 0; n < C_out; ++n)
             for (int q = 0; q < 2; ++q) {
-                uint16_t* r = reinterpret_cast<uint16_t*>(rec.data() + (((size_t)c * C_out + n) * 2 + q) * p.rec_bytes);
+                uint8_t* r = rec.data() + (((size_t)c * C_out + n) * 2 + q) * p.rec_bytes;
                 for (int s = 0; s < ns; ++s) {
                     const int j = p.kind == 1 ? 18 * c + 9 * q + s : c * 2 * p.cm + 2 * s + q;
+                    if (j >= G) continue;
                     for (int m = 0; m < M; ++m) {
-                        uint32_t code = 0;
-                        if (j < G) {
-                            const size_t src = ((size_t)n * G + j) * M + m;
-                            code = B <= 8 ? static_cast<const uint8_t*>(codes)[src]
-                                          : static_cast<const uint16_t*>(codes)[src];
-                        }
-                        const uint32_t ent = p.dec == aq::FUSED_DEC_T16G ? code : ((uint32_t)m * nk + code) * row_bytes;
-                        r[s * M + m] = (uint16_t)ent;
+                        const size_t src = ((size_t)n * G + j) * M + m;
+                        if (ent_b == 1) r[s * M + m] = static_cast<const uint8_t*>(codes)[src];
+                        else std::memcpy(r + 2 * (s * M + m), static_cast<const uint16_t*>(codes) + src, 2);
                     }
                 }
             }

@@ -320,3 +320,32 @@ def test_sweep_layer_sampled(layer, M):
         flat = y.transpose(0, 2, 3, 1).reshape(spec.tokens, spec.C_out)
         got = flat[np.ix_(tok, ch)]
     assert O.rel_err_inf(got, ref) <= 2e-3
+
+
+def test_graph_replay_matches_eager():
+    """Forwards captured in a HIP graph give the eager result on every replay."""
+    import paper_2506_05960_amd as P
+    for spec in (W.config_spec("conv64"), W.config_spec("qkv16").with_n(1000), W.config_spec("tiny")):
+        inp = generate(spec, 31)
+        layer = P.AQLayer(spec, inp)
+        x = _dev(inp["x"], spec.x_dtype)
+        xs = None if inp["x_scales"] is None else torch.from_numpy(inp["x_scales"]).cuda()
+        eager = layer.forward(x, xs).clone()
+        torch.cuda.synchronize()
+        y = torch.zeros_like(eager)
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                layer.forward(x, xs, out=y)
+        torch.cuda.current_stream().wait_stream(s)
+        for rep in range(4):
+            y.zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(y, eager), (spec.name, rep)
+            _ = layer.forward(x, xs)          # eager work between replays
+            torch.cuda.synchronize()
+        layer.close()
