@@ -205,21 +205,33 @@ def decode_emulate(codebooks: np.ndarray, codes: np.ndarray, scales: np.ndarray,
                    codebook_dtype: str, tile_dtype: str, scaled: bool = True) -> np.ndarray:
     """Decoded weights [C_out, K] exactly as the decode kernels produce them.
 
-    Arithmetic, in IEEE fp32 without fused multiply-add:
-    ``acc = C[0, b0]; acc = acc + C[1, b1]; ...`` (ascending m), then, when
-    ``scaled``, ``acc = acc * s[i]``; then one round-to-nearest-even to the
-    tile dtype.  Returns float16 / float32 arrays, or uint16 bf16 bit patterns.
+    * fp16 codebooks with an fp16 tile: the M codewords accumulate in IEEE
+      binary16 in ascending m, rounding to nearest even after every add.  For
+      M <= 2 this equals the fp32 sum rounded once to fp16 (two fp16 addends
+      never double-round), so only M >= 3 differs from the next rule.
+    * otherwise: IEEE fp32 sum in ascending m (no fused multiply-add).
+    Then, when ``scaled``, ``w = fl32(acc * s[i])``; then one
+    round-to-nearest-even to the tile dtype.  Returns float16 / float32 arrays,
+    or uint16 bf16 bit patterns.
     """
-    if codebook_dtype == "bf16":
-        C = bf16_bits_to_f32(codebooks)
-    else:
-        C = np.asarray(codebooks).astype(np.float32)
-    M = C.shape[0]
+    M = np.asarray(codebooks).shape[0]
     C_out, G, _ = codes.shape
     idx = codes.astype(np.int64)
-    acc = C[0][idx[:, :, 0]].astype(np.float32)
-    for m in range(1, M):
-        acc = (acc + C[m][idx[:, :, m]]).astype(np.float32)
+    if codebook_dtype == "f16" and tile_dtype == "f16":
+        C16 = np.asarray(codebooks).astype(np.float16)
+        acc16 = C16[0][idx[:, :, 0]]
+        for m in range(1, M):
+            # an fp16 add: exact fp32 sum of two fp16 values, rounded once to fp16
+            acc16 = (acc16.astype(np.float32) + C16[m][idx[:, :, m]].astype(np.float32)).astype(np.float16)
+        acc = acc16.astype(np.float32)
+    else:
+        if codebook_dtype == "bf16":
+            C = bf16_bits_to_f32(codebooks)
+        else:
+            C = np.asarray(codebooks).astype(np.float32)
+        acc = C[0][idx[:, :, 0]].astype(np.float32)
+        for m in range(1, M):
+            acc = (acc + C[m][idx[:, :, m]]).astype(np.float32)
     if scaled:
         acc = (acc * np.asarray(scales, dtype=np.float32)[:, None, None]).astype(np.float32)
     acc = acc.reshape(C_out, G * g)

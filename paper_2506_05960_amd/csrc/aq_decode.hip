@@ -1,6 +1,8 @@
 // Decode-to-global: writes the dense weight matrix W [C_out][K] in the tile
 // dtype.  Test hook for bit-exact checks of the decode arithmetic used by the
-// matrix-core path (codeword sum in fp32, ascending m; scale; one rounding).
+// matrix-core paths: the codewords are summed in ascending m (in fp16 when
+// both the codebook and the tile are fp16, else in fp32), multiplied by the
+// channel scale in fp32 and rounded once to the tile dtype.
 #include "aq_device.h"
 
 namespace aq {
@@ -19,9 +21,17 @@ decode_to_global_kernel(const void* __restrict__ cb, const CodeT* __restrict__ c
     const int64_t rows = (int64_t)1 << B;
     const int64_t K = (int64_t)G * g;
     for (int t = 0; t < g; ++t) {
-        float acc = load_as_f32<CBT>(cb, (int64_t)b[0] * g + t);
-        for (int m = 1; m < M; ++m)
-            acc = __fadd_rn(acc, load_as_f32<CBT>(cb, ((int64_t)m * rows + b[m]) * g + t));
+        float acc;
+        if constexpr (CBT == AQ_F16 && TILE == AQ_F16) {
+            // fp16 codebooks, fp16 tile: accumulate in fp16, ascending m
+            _Float16 h = (_Float16)load_as_f32<CBT>(cb, (int64_t)b[0] * g + t);
+            for (int m = 1; m < M; ++m) h = h + (_Float16)load_as_f32<CBT>(cb, ((int64_t)m * rows + b[m]) * g + t);
+            acc = (float)h;
+        } else {
+            acc = load_as_f32<CBT>(cb, (int64_t)b[0] * g + t);
+            for (int m = 1; m < M; ++m)
+                acc = __fadd_rn(acc, load_as_f32<CBT>(cb, ((int64_t)m * rows + b[m]) * g + t));
+        }
         acc = opaque_f32(__fmul_rn(acc, s));
         const int64_t o = (int64_t)i * K + (int64_t)j * g + t;
         if constexpr (TILE == AQ_F32) static_cast<float*>(W)[o] = acc;

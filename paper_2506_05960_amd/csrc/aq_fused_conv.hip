@@ -22,8 +22,8 @@ static hipError_t conv_tiles(const Geom& geo, const FusedPlan& p, const FusedLau
 
 template <int KIND, int CM>
 static hipError_t conv_dec(const Geom& geo, const FusedPlan& p, const FusedLaunch& fl) {
-    if (p.dec == FUSED_DEC_PK16) return conv_tiles<KIND, CM, FUSED_DEC_PK16, 2>(geo, p, fl);
-    if (p.dec == FUSED_DEC_F32L && p.mc == 4) return conv_tiles<KIND, CM, FUSED_DEC_F32L, 4>(geo, p, fl);
+    if (p.dec == FUSED_DEC_PK16 && p.mc == 2) return conv_tiles<KIND, CM, FUSED_DEC_PK16, 2>(geo, p, fl);
+    if (p.dec == FUSED_DEC_PK16 && p.mc == 4) return conv_tiles<KIND, CM, FUSED_DEC_PK16, 4>(geo, p, fl);
     if (p.dec == FUSED_DEC_T16G) return conv_tiles<KIND, CM, FUSED_DEC_T16G, 1>(geo, p, fl);
     return hipErrorInvalidConfiguration;
 }

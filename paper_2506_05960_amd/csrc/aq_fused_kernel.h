@@ -12,10 +12,11 @@
 // works as long as both operands use the same one.
 //  * Weights: each lane decodes its own groups straight into registers.  The
 //    codes a lane needs (one output channel, one half of a chunk's k-slices)
-//    are stored contiguously at create time, as byte offsets into the LDS
-//    codebook; a group is the sum of its M codewords (fp32 in ascending m, or
-//    an exact packed fp16 add when M = 2) rounded once to fp16.  The
-//    per-channel scale multiplies the fp32 accumulator in the epilogue.
+//    are stored contiguously at create time as 8-bit codes (16-bit when the
+//    codebook is larger than 256 rows); a group is the sum of its M codewords,
+//    accumulated with packed fp16 adds in ascending m (for M = 2 this equals
+//    the fp32 sum rounded once to fp16).  The per-channel scale multiplies the
+//    fp32 accumulator in the epilogue.
 //  * Activations sit in a per-wave, double-buffered LDS staging area split
 //    into planes of 8 channels (or 8 consecutive k), 16 bytes per pixel (or
 //    token), so that one lane's 8 operand values are one 16-byte read and 16
@@ -114,12 +115,15 @@ __device__ __forceinline__ void gather_group(GroupRaw<DEC, MC>& g, const EntT* e
 template <int DEC, int MC>
 __device__ __forceinline__ u32x4 combine_group(const GroupRaw<DEC, MC>& g) {
     if constexpr (DEC == FUSED_DEC_PK16) {
-        // exact: for two fp16 addends the fp16 sum equals the fp32 sum rounded to fp16
-        u32x4 r;
-        r[0] = add_f16x2(g.w[0][0], g.w[1][0]);
-        r[1] = add_f16x2(g.w[0][1], g.w[1][1]);
-        r[2] = add_f16x2(g.w[0][2], g.w[1][2]);
-        r[3] = add_f16x2(g.w[0][3], g.w[1][3]);
+        // fp16 accumulation in ascending m (for M = 2 identical to the fp32 sum rounded once)
+        u32x4 r = g.w[0];
+#pragma unroll
+        for (int m = 1; m < MC; ++m) {
+            r[0] = add_f16x2(r[0], g.w[m][0]);
+            r[1] = add_f16x2(r[1], g.w[m][1]);
+            r[2] = add_f16x2(r[2], g.w[m][2]);
+            r[3] = add_f16x2(r[3], g.w[m][3]);
+        }
         return r;
     } else if constexpr (DEC == FUSED_DEC_F32L) {
         float s[8];
@@ -174,7 +178,6 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     constexpr int AM = BM / 32, AN = BN / 32;
     using EntT = typename std::conditional<DEC == FUSED_DEC_T16G, uint16_t, uint8_t>::type;   // one code
     static_assert(KIND != 1 || CM == 1, "3x3 chunks are 16 channels");
-    static_assert(DEC != FUSED_DEC_PK16 || MC == 2, "packed fp16 decode is for M = 2");
 
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     const int tid = threadIdx.x;
@@ -435,10 +438,11 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             for (int a = 0; a < AM; ++a) af[s][a] = *reinterpret_cast<const u32x4*>(buf + a_base[a] + soff);
         }
     };
+    constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L && NS * MC <= 18;
     // weights of one 32-channel block of a chunk, decoded into MFMA operands
     auto decode_block = [&](const uint32_t* codes_dw, u32x4 (&d)[NS]) {
         const EntT* ev = reinterpret_cast<const EntT*>(codes_dw);
-        if constexpr (DEC != FUSED_DEC_F32L) {
+        if constexpr (LOOKAHEAD) {
             GroupRaw<DEC, MC> raw[NS];
 #pragma unroll
             for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
@@ -457,9 +461,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // of this wave's next chunk) are read and summed while the current block's
     // MFMAs run, and the next chunk's activation fragments are read right after
     // its staging store, so a chunk starts with its operands in flight.  The
-    // fp32-codebook mode keeps no look-ahead (a block of raw fp32 codewords does
-    // not fit in registers).
-    constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L;
+    // look-ahead is used when a block of raw codewords (groups x M x 16 bytes
+    // per lane) fits in 72 registers.
     int chunk = wave;
     u32x4 af[NS][AM];
     u32x4 dec[NS];

@@ -41,7 +41,7 @@ constexpr int kLutTokTile = 4;    // tokens per LUT entry (one 16-byte table rea
 // ---- fused decode + matrix-core path (fp16 tiles, g == 8) ----
 
 enum FusedDec {
-    FUSED_DEC_PK16 = 0,   // M == 2, fp16 codebooks in LDS, packed fp16 add (exact)
+    FUSED_DEC_PK16 = 0,   // fp16 codebooks in LDS, codewords accumulated with packed fp16 adds
     FUSED_DEC_F32L = 1,   // fp32 codebooks in LDS, fp32 sum in ascending m
     FUSED_DEC_T16L = 2,   // M == 1, codebook pre-rounded to fp16, in LDS
     FUSED_DEC_T16G = 3    // M == 1, codebook pre-rounded to fp16, read from global memory (B > 8)

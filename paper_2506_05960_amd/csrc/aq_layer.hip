@@ -172,12 +172,9 @@ bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPla
         p->cm = 4;
         p->nchunk = (d.in_features + 63) / 64;
     }
-    if (M == 2 && B <= 8 && d.codebook_dtype == AQ_F16) {
+    if ((M == 2 || M == 4) && B <= 8 && d.codebook_dtype == AQ_F16) {
         p->dec = aq::FUSED_DEC_PK16;
-        p->cb_bytes = 2 * 256 * 16;             // LDS keeps 256 rows per codebook
-    } else if (M == 4 && B <= 8) {
-        p->dec = aq::FUSED_DEC_F32L;
-        p->cb_bytes = 4 * 256 * 32;
+        p->cb_bytes = M * 256 * 16;             // LDS keeps 256 rows per codebook
     } else if (M == 1 && B > 8) {
         p->dec = aq::FUSED_DEC_T16G;
         p->cb_bytes = 0;

@@ -6,7 +6,8 @@
 // inputs) and expands the weight tile from its codes: each thread sums the M
 // fp32 codewords of a group in ascending m and rounds once to the tile dtype
 // (the per-channel scale is applied to the fp32 accumulator in the epilogue,
-// which is algebraically the same product).  Four waves then contract the
+// which is algebraically the same product).  With fp16 codebooks and an fp16
+// tile the codeword sum is accumulated in fp16 instead.  Four waves then contract the
 // tiles with v_mfma_f32_32x32x16_{f16,bf16}; one lane's 8 operand values are
 // exactly one decoded group.
 #include <type_traits>
@@ -76,7 +77,7 @@ template <int MODE, int XT, int TILE, bool CONV, int BM, int BN>
 __global__ void __launch_bounds__(kThreads, 2)
 mfma_fwd_kernel(Geom geo, const void* __restrict__ cbdev, const void* __restrict__ codes_v,
                 const float* __restrict__ scales, const void* __restrict__ X, const float* __restrict__ x_scales,
-                void* __restrict__ Y, int y_dtype) {
+                void* __restrict__ Y, int y_dtype, int acc16) {
     static_assert(BM % 64 == 0 && BN % 64 == 0, "tile must split into 2x2 waves of 32x32 blocks");
     constexpr int WM = BM / 2, WN = BN / 2;        // per-wave tile
     constexpr int AM = WM / 32, AN = WN / 32;      // 32x32 blocks per wave
@@ -200,8 +201,13 @@ mfma_fwd_kernel(Geom geo, const void* __restrict__ cbdev, const void* __restrict
                         const floatx4 lo = p[0], hi = p[1];
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            sum[e] = __fadd_rn(sum[e], lo[e]);
-                            sum[4 + e] = __fadd_rn(sum[4 + e], hi[e]);
+                            if (acc16) {   // fp16 codebooks and tile: fp16 accumulation
+                                sum[e] = (float)((_Float16)sum[e] + (_Float16)lo[e]);
+                                sum[4 + e] = (float)((_Float16)sum[4 + e] + (_Float16)hi[e]);
+                            } else {
+                                sum[e] = __fadd_rn(sum[e], lo[e]);
+                                sum[4 + e] = __fadd_rn(sum[4 + e], hi[e]);
+                            }
                         }
                     }
 #pragma unroll
@@ -297,7 +303,8 @@ static hipError_t launch_cfg(const Geom& geo, const DeviceWeights& w, const void
         }
     }
     const dim3 grid((unsigned)((geo.tokens + BM - 1) / BM), (unsigned)((geo.C_out + BN - 1) / BN));
-    kern<<<grid, kThreads, dyn, st>>>(geo, cbdev, w.codes, w.scales, X, x_scales, Y, y_dtype);
+    const int acc16 = w.cb_dtype == AQ_F16 && TILE == AQ_F16;
+    kern<<<grid, kThreads, dyn, st>>>(geo, cbdev, w.codes, w.scales, X, x_scales, Y, y_dtype, acc16);
     return hipGetLastError();
 }
 

@@ -225,13 +225,21 @@ def test_bf16_and_fp16_storage_widening():
 # Decode emulation (bit-exact reference for decoded tiles)
 # ---------------------------------------------------------------------------
 
-def _torch_decode(cb32, codes, s, g, tile, scaled):
-    """Independent emulation with torch CPU tensors and explicit per-m float32 adds."""
-    C = torch.from_numpy(cb32)
+def _torch_decode(cb16, codes, s, g, tile, scaled):
+    """Independent emulation with torch CPU tensors.
+
+    fp16 tiles accumulate in torch.float16 (every add rounded to fp16);
+    other tiles accumulate in float32.
+    """
     idx = torch.from_numpy(codes.astype(np.int64))
+    if tile == "f16":
+        C = torch.from_numpy(cb16)
+    else:
+        C = torch.from_numpy(cb16.astype(np.float32))
     acc = C[0][idx[:, :, 0]]
     for m in range(1, C.shape[0]):
         acc = acc + C[m][idx[:, :, m]]
+    acc = acc.float()
     if scaled:
         acc = acc * torch.from_numpy(s)[:, None, None]
     acc = acc.reshape(codes.shape[0], -1)
@@ -244,7 +252,7 @@ def _torch_decode(cb32, codes, s, g, tile, scaled):
 
 @pytest.mark.parametrize("tile", ["f16", "bf16", "f32"])
 @pytest.mark.parametrize("scaled", [True, False])
-@pytest.mark.parametrize("M", [1, 2, 4])
+@pytest.mark.parametrize("M", [1, 2, 3, 4])
 def test_decode_emulation_matches_torch_casts(tile, scaled, M):
     rng = np.random.default_rng(20 + M)
     B, g = 8, 8
@@ -252,15 +260,50 @@ def test_decode_emulation_matches_torch_casts(tile, scaled, M):
     cb[:, :8, :] *= 1e-4         # push some sums into the fp16 subnormal range
     cb16 = cb.astype(np.float16)
     codes = rng.integers(0, 1 << B, size=(40, 12, M)).astype(np.uint8)
+    codes[:4] = rng.integers(0, 8, size=(4, 12, M))      # sums of tiny codewords only
     s = rng.uniform(0.5, 1.5, size=40).astype(np.float32)
     got = O.decode_emulate(cb16, codes, s, g, "f16", tile, scaled)
-    ref = _torch_decode(cb16.astype(np.float32), codes, s, g, tile, scaled)
+    ref = _torch_decode(cb16, codes, s, g, tile, scaled)
     if tile == "f16":
         assert np.array_equal(got.view(np.uint16), ref.view(np.uint16))
         assert np.any(np.abs(got) < np.float16(6.1e-5))     # subnormals exercised
     else:
         assert np.array_equal(got.view(np.uint32) if tile == "f32" else got,
                               ref.view(np.uint32) if tile == "f32" else ref)
+
+
+def _adversarial_f16_pairs(rng, n):
+    """fp16 pairs spanning every exponent gap, both signs, subnormals and ties."""
+    e1 = rng.integers(-24, 16, size=n)
+    e2 = e1 - rng.integers(0, 30, size=n)
+    m1 = rng.integers(1024, 2048, size=n)
+    m2 = rng.integers(1024, 2048, size=n)
+    a = (np.sign(rng.normal(size=n)) * m1 * np.exp2(e1 - 10.0)).astype(np.float16)
+    b = (np.sign(rng.normal(size=n)) * m2 * np.exp2(np.maximum(e2, -24) - 10.0)).astype(np.float16)
+    return a, b
+
+
+def test_two_fp16_addends_round_once():
+    """For two fp16 addends, rounding the fp32 sum to fp16 equals rounding the exact sum.
+
+    The fp16-tile decode relies on this for M = 2: an fp16 add and an fp32
+    add followed by one rounding give the same bits.  The exact sum is
+    formed in fp64 (fp16 values have 11 significant bits within 40 binades).
+    """
+    rng = np.random.default_rng(123)
+    a, b = _adversarial_f16_pairs(rng, 400000)
+    exact = a.astype(np.float64) + b.astype(np.float64)
+    once = exact.astype(np.float16)                   # one rounding of the exact value
+    via32 = (a.astype(np.float32) + b.astype(np.float32)).astype(np.float16)
+    assert np.array_equal(once.view(np.uint16), via32.view(np.uint16))
+    # three addends can differ: the fp16 chain is a distinct rule for M >= 3
+    c = (rng.normal(0, 0.05, size=200000)).astype(np.float16)
+    x = rng.normal(0, 0.05, size=200000).astype(np.float16)
+    y = rng.normal(0, 0.05, size=200000).astype(np.float16)
+    chain = ((x.astype(np.float32) + y.astype(np.float32)).astype(np.float16).astype(np.float32)
+             + c.astype(np.float32)).astype(np.float16)
+    f32 = (x.astype(np.float32) + y.astype(np.float32) + c.astype(np.float32)).astype(np.float16)
+    assert np.any(chain.view(np.uint16) != f32.view(np.uint16))
 
 
 def test_bf16_rounding_ties_and_carries():
@@ -273,16 +316,36 @@ def test_bf16_rounding_ties_and_carries():
 
 
 def test_decode_emulation_against_float_definition():
-    """The decoded value is within half an ulp of the fp64 dequantized weight."""
+    """fp32 rule: the decoded value is within half an fp16 ulp of the exact scaled weight."""
     rng = np.random.default_rng(21)
+    M, B, g = 4, 8, 8
+    cb32 = rng.normal(0, 0.05, size=(M, 1 << B, g)).astype(np.float16).astype(np.float32)
+    codes = rng.integers(0, 256, size=(30, 10, M)).astype(np.uint8)
+    s = rng.uniform(0.5, 1.5, size=30).astype(np.float32)
+    W = O.dequantize(cb32, codes, s, g, "f32")
+    d = O.decode_emulate(cb32, codes, s, g, "f32", "f16", True).astype(np.float64)
+    ulp = np.spacing(np.abs(d.astype(np.float16))).astype(np.float64)
+    assert np.all(np.abs(d - W) <= 0.5 * ulp + 4 * np.abs(W) * 2.0 ** -24)
+
+
+def test_fp16_chain_rounds_each_partial_sum_once():
+    """fp16 rule: every partial sum is the correctly rounded fp16 sum of the previous one and a codeword."""
+    rng = np.random.default_rng(22)
     M, B, g = 4, 8, 8
     cb16 = rng.normal(0, 0.05, size=(M, 1 << B, g)).astype(np.float16)
     codes = rng.integers(0, 256, size=(30, 10, M)).astype(np.uint8)
-    s = rng.uniform(0.5, 1.5, size=30).astype(np.float32)
-    W = O.dequantize(cb16, codes, s, g, "f16")
-    d = O.decode_emulate(cb16, codes, s, g, "f16", "f16", True).astype(np.float64)
-    ulp = np.spacing(np.abs(d.astype(np.float16))).astype(np.float64)
-    assert np.all(np.abs(d - W) <= 0.5 * ulp + 4 * np.abs(W) * 2.0 ** -24)
+    s = np.ones(30, dtype=np.float32)
+    d = O.decode_emulate(cb16, codes, s, g, "f16", "f16", False).astype(np.float64).reshape(30, 10, g)
+    # re-derive the chain in fp64 with one explicit rounding per step
+    part = cb16[0][codes[:, :, 0]].astype(np.float64)
+    bound = np.zeros_like(part)
+    for m in range(1, M):
+        exact = part + cb16[m][codes[:, :, m]].astype(np.float64)   # exact in fp64
+        part = exact.astype(np.float16).astype(np.float64)
+        bound += 0.5 * np.spacing(np.abs(part).astype(np.float16)).astype(np.float64)
+    assert np.array_equal(d, part)
+    total = sum(cb16[m][codes[:, :, m]].astype(np.float64) for m in range(M))
+    assert np.all(np.abs(d - total) <= bound + 1e-12)
 
 
 # ---------------------------------------------------------------------------
