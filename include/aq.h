@@ -103,9 +103,11 @@ aq_status aq_layer_forward(aq_layer* layer, const void* X, const float* x_scales
 
 /*
  * Decoded weights W [C_out][K] in desc->tile_dtype (device, caller-owned),
- * computed as the decode path does: an fp32 sum of the M codewords in
- * ascending m, times s[i] in fp32, then one round-to-nearest-even to the tile
- * dtype (eq. (4) with the per-channel scale).  Asynchronous on `stream`.
+ * computed as the decode path does (eq. (4) with the per-channel scale): the
+ * M codewords summed in ascending m -- in fp16, rounding each partial sum,
+ * when both codebooks and tile are fp16, otherwise in fp32 -- then times s[i]
+ * in fp32, then one round-to-nearest-even to the tile dtype.  (For M <= 2
+ * the fp16 sum equals the fp32 sum rounded once.)  Asynchronous on `stream`.
  * A test hook for bit-exact checks; the forward never materialises W.
  */
 aq_status aq_layer_decode(aq_layer* layer, void* W, void* stream);

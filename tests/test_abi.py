@@ -1,0 +1,175 @@
+"""Host-side checks of the C ABI: the library loads, exports every function
+include/aq.h declares, and rejects bad arguments before touching a GPU.
+
+No test here launches a kernel; they run on a machine without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2506_05960_amd as P
+from paper_2506_05960_amd import aq as A
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "aq.h")
+
+
+def _lib():
+    if not os.path.exists(A.LIB_PATH):
+        from paper_2506_05960_amd import build
+        build.build()
+    return A.load_library()
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(aq_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_binding_names():
+    assert _declared_functions() == sorted(A.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = _lib()
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+        assert ctypes.cast(getattr(lib, name), ctypes.c_void_p).value
+
+
+def test_version_string():
+    _lib()
+    assert A.aq_version().startswith("aq-mi355x ")
+
+
+def _good_linear(C_out=16, K=32, g=8, M=2, B=4):
+    rng = np.random.default_rng(0)
+    cb = rng.standard_normal((M, 1 << B, g)).astype(np.float32)
+    codes = rng.integers(0, 1 << B, size=(C_out, K // g, M), dtype=np.uint8 if B <= 8 else np.uint16)
+    scales = np.ones(C_out, np.float32)
+    desc = A.make_desc(C_out, K, "f32", "f32", "f32", "f32", 64)
+    return desc, cb, codes, scales, g, M, B
+
+
+def _create_status(desc, cb, codes, scales, g, M, B):
+    lib = _lib()
+    h = ctypes.c_void_p(1234)
+    args = [None if a is None else np.ascontiguousarray(a).ctypes.data for a in (cb, codes, scales)]
+    st = lib.aq_layer_create(ctypes.byref(desc) if desc is not None else None, args[0], args[1], args[2], g, M, B,
+                             ctypes.byref(h))
+    return st, h.value, A.load_library().aq_last_error().decode()
+
+
+@pytest.mark.parametrize("change, status, text", [
+    (dict(g=0), A.AQ_ERR_INVALID_ARGUMENT, "g must be"),
+    (dict(g=17), A.AQ_ERR_INVALID_ARGUMENT, "g must be"),
+    (dict(M=0), A.AQ_ERR_INVALID_ARGUMENT, "M must be"),
+    (dict(M=9), A.AQ_ERR_INVALID_ARGUMENT, "M must be"),
+    (dict(B=0), A.AQ_ERR_INVALID_ARGUMENT, "B must be"),
+    (dict(B=17), A.AQ_ERR_INVALID_ARGUMENT, "B must be"),
+    (dict(g=3), A.AQ_ERR_INVALID_ARGUMENT, "multiple of g"),
+])
+def test_create_rejects_bad_format(change, status, text):
+    desc, cb, codes, scales, g, M, B = _good_linear()
+    kw = dict(g=g, M=M, B=B)
+    kw.update(change)
+    st, h, msg = _create_status(desc, cb, codes, scales, kw["g"], kw["M"], kw["B"])
+    assert st == status and text in msg and h is None
+
+
+def test_create_rejects_null_pointers():
+    desc, cb, codes, scales, g, M, B = _good_linear()
+    for i in range(3):
+        args = [cb, codes, scales]
+        args[i] = None
+        st, h, msg = _create_status(desc, *args, g, M, B)
+        assert st == A.AQ_ERR_INVALID_ARGUMENT and "null" in msg and h is None
+    st, _, _ = _create_status(None, cb, codes, scales, g, M, B)
+    assert st == A.AQ_ERR_INVALID_ARGUMENT
+
+
+def test_create_rejects_out_of_range_code():
+    desc, cb, codes, scales, g, M, B = _good_linear(B=4)
+    codes = codes.copy()
+    codes[3, 1, 1] = 16
+    st, _, msg = _create_status(desc, cb, codes, scales, g, M, B)
+    assert st == A.AQ_ERR_INVALID_ARGUMENT and f"index {(3 * 4 + 1) * 2 + 1}" in msg
+
+
+def test_create_rejects_out_of_range_uint16_code():
+    desc, cb, codes, scales, g, M, B = _good_linear(M=1, B=10)
+    codes = codes.copy()
+    codes[0, 0, 0] = 1024
+    st, _, msg = _create_status(desc, cb, codes, scales, g, M, B)
+    assert st == A.AQ_ERR_INVALID_ARGUMENT and "index 0" in msg
+
+
+@pytest.mark.parametrize("field, value, text", [
+    ("codebook_dtype", A.AQ_I8, "codebook_dtype"),
+    ("y_dtype", A.AQ_BF16, "y_dtype"),
+    ("tile_dtype", A.AQ_I8, "tile_dtype"),
+    ("x_dtype", 7, "x_dtype"),
+    ("max_tokens", 0, "max_tokens"),
+    ("out_features", 0, "out_features"),
+])
+def test_create_rejects_bad_descriptor(field, value, text):
+    desc, cb, codes, scales, g, M, B = _good_linear()
+    setattr(desc, field, value)
+    st, _, msg = _create_status(desc, cb, codes, scales, g, M, B)
+    assert st == A.AQ_ERR_INVALID_ARGUMENT and text in msg
+
+
+def test_create_rejects_bad_conv_geometry():
+    class Conv:
+        kh = kw = 3
+        cin = 4
+        stride = 1
+        pad = 1
+        H = W = 8
+    desc, cb, codes, scales, g, M, B = _good_linear(C_out=8, K=40)
+    d = A.make_desc(8, 40, "f32", "f32", "f32", "f32", 64, Conv)
+    st, _, msg = _create_status(d, cb, codes[:, :5], scales[:8], g, M, B)
+    assert st == A.AQ_ERR_INVALID_ARGUMENT and "conv_cin*conv_kh*conv_kw" in msg
+    Conv.cin, Conv.pad, Conv.H = 4, 0, 2            # 2 + 0 < 3: empty output
+    d = A.make_desc(8, 36, "f32", "f32", "f32", "f32", 64, Conv)
+    st, _, msg = _create_status(d, cb, codes[:, :4], scales[:8], 9, 1, B)
+    assert st == A.AQ_ERR_INVALID_ARGUMENT and "empty" in msg
+    Conv.pad, Conv.H = 1, 8
+    d = A.make_desc(8, 36, "f32", "i8", "f32", "f32", 64, Conv)
+    st, _, msg = _create_status(d, cb, codes[:, :4], scales[:8], 9, 1, B)
+    assert st == A.AQ_ERR_UNSUPPORTED and "linear layers only" in msg
+
+
+def test_create_reports_format_without_kernel():
+    # B > 8 rules out the table path and g != 8 rules out the fp16 decode tile.
+    desc, cb, codes, scales, g, M, B = _good_linear(K=36, g=9, M=1, B=10)
+    desc.tile_dtype = A.AQ_F16
+    st, _, msg = _create_status(desc, cb, codes, scales, g, M, B)
+    assert st == A.AQ_ERR_UNSUPPORTED and "no kernel" in msg
+
+
+def test_null_handles_are_rejected():
+    lib = _lib()
+    assert lib.aq_layer_forward(None, 16, None, 16, 1, None) == A.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layer_decode(None, 16, None) == A.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layer_set_path(None, A.AQ_PATH_LUT) == A.AQ_ERR_INVALID_ARGUMENT
+    out = ctypes.c_int()
+    assert lib.aq_layer_choose_path(None, 4, ctypes.byref(out)) == A.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layer_destroy(None) == A.AQ_OK
+
+
+def test_python_binding_raises_on_error():
+    desc, cb, codes, scales, g, M, B = _good_linear()
+    with pytest.raises(A.AQError, match="AQ_ERR_INVALID_ARGUMENT"):
+        A.aq_layer_create(desc, cb, codes, scales, 0, M, B)
+
+
+def test_package_has_no_host_fallback():
+    # the package exposes the library calls only; nothing computes a forward on the host
+    public = {n for n in dir(P) if not n.startswith("_")}
+    assert {"AQLayer", "load_library"} <= public
+    assert not any("oracle" in n for n in public)
