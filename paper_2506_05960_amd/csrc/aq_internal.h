@@ -24,19 +24,19 @@ struct DeviceWeights {
     const float* cb32;            // [M][2^B][g] fp32 (exact widening of codebooks)
     const void* cbtile;           // [2^B][g] codebook rounded to the tile dtype (M == 1, B > 8), else null
     const void* codes;            // [C_out][G][M] uint8 | uint16
-    const uint8_t* codes_lut;     // [nchunk][C_out][jc][M] uint8 (B <= 8), zero padded
+    const uint8_t* codes_lut;     // [nchunk][C_out][jc*M] uint8 (B <= 8), zero padded past G
     const float* scales;          // [C_out]
     int cb_dtype;                 // aq_dtype
 };
 
 // LUT-path blocking chosen at create time.
 struct LutPlan {
-    int jc;                       // groups per chunk
+    int jc;                       // groups per chunk (jc * M is a multiple of 16)
     int nchunk;                   // ceil(G / jc)
     int tok_block;                // tokens per launch (workspace rows)
+    int nt_max;                   // most tokens per table entry (1, 2 or 4) that fit LDS
+    bool mfma_table;              // table built on the matrix cores (fp16 codebook, fp16/int8 input, g == 8)
 };
-
-constexpr int kLutTokTile = 4;    // tokens per LUT entry (one 16-byte table read)
 
 // ---- fused decode + matrix-core path (fp16 tiles, g == 8) ----
 
@@ -98,7 +98,8 @@ hipError_t launch_mfma_forward(const Geom& geo, const DeviceWeights& w, const vo
 hipError_t launch_codebook_prep(const void* cb, int cb_dtype, int64_t n, float* cb32, void* cbtile, int tile_dtype,
                                 hipStream_t stream);
 
-size_t lut_lds_bytes(const Geom& geo, const LutPlan& plan);
+size_t lut_lds_bytes(const Geom& geo, const LutPlan& plan, int nt);
+int lut_tokens_per_entry(const LutPlan& plan, int ntok);
 
 hipError_t launch_f32_forward(const Geom& geo, const DeviceWeights& w, const void* X, int x_dtype,
                               const float* x_scales, void* Y, int y_dtype, hipStream_t stream);

@@ -149,6 +149,29 @@ aq_status dev_upload(T** dst, const void* src, size_t bytes, const char* what) {
 constexpr size_t kLdsBytes = 160 * 1024;
 
 // Decide whether the fused path applies and fill the create-time part of the plan.
+// LUT blocking: a chunk of jc groups with jc*M a multiple of 16 (one or more
+// 16-byte code runs per row), its table (jc*M slots x 256 entries x NT fp32)
+// within 64 KB at the largest token count per entry that fits, and never
+// above 144 KB.
+bool lut_plan_create(const aq_layer_desc& d, int g, int M, int G, LutPlan* p) {
+    int q = 16;
+    for (int m = M; m % 2 == 0 && q > 1; m /= 2) q /= 2;        // 16 / gcd(M, 16)
+    const size_t slot_bytes = (size_t)256 * sizeof(float);      // per token
+    int nt = 4;
+    while (nt > 1 && (size_t)q * M * slot_bytes * nt > 144 * 1024) nt /= 2;
+    if ((size_t)q * M * slot_bytes * nt > 144 * 1024) return false;
+    int jc = q;
+    while ((size_t)(jc + q) * M * slot_bytes * nt <= 64 * 1024 && jc + q <= (G + q - 1) / q * q) jc += q;
+    p->jc = jc;
+    p->nchunk = (G + jc - 1) / jc;
+    p->nt_max = nt;
+    p->mfma_table = d.codebook_dtype == AQ_F16 && (d.x_dtype == AQ_F16 || d.x_dtype == AQ_I8) && g == 8;
+    int64_t tb = std::min<int64_t>(d.max_tokens, 256);
+    p->tok_block = (int)((tb + 3) / 4 * 4);
+    // 32-bit code offsets in the kernel
+    return (int64_t)p->nchunk * d.out_features * jc * M < (int64_t(1) << 31);
+}
+
 bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPlan* p) {
     std::memset(p, 0, sizeof(*p));
     if (d.tile_dtype != AQ_F16 || g != 8) return false;
@@ -320,7 +343,10 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
     L->lut_ok = lut_ok;
     L->dec_ok = dec_ok;
     L->path = AQ_PATH_AUTO;
-    L->lut_max_tokens = 16;
+    // Measured crossover on MI355X (fp16 layers with 256-entry codebooks): the
+    // table path beats the matrix-core path only when K is large enough that
+    // the latter's few workgroups each walk a long reduction, up to 16 tokens.
+    L->lut_max_tokens = desc->in_features >= 4096 ? 16 : 0;
     if (const char* s = std::getenv("AQ_LUT_MAX_TOKENS")) L->lut_max_tokens = std::atoll(s);
     e = hipGetDevice(&L->device);
     if (e != hipSuccess) {
@@ -347,16 +373,12 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
 
     if (lut_ok) {
         LutPlan& p = L->plan;
-        const int64_t per_group = (int64_t)M * nk;                   // table entries per group
-        int jc = (int)std::max<int64_t>(1, 4096 / per_group);
-        jc = std::min(jc, G);
-        jc = std::min(jc, 64);
-        p.jc = jc;
-        p.nchunk = (G + jc - 1) / jc;
-        int64_t tb = std::min<int64_t>(desc->max_tokens, 256);
-        tb = (tb + aq::kLutTokTile - 1) / aq::kLutTokTile * aq::kLutTokTile;
-        p.tok_block = (int)tb;
-        // codes regrouped per chunk: [nchunk][C_out][jc][M], zero padded past G
+        if (!lut_plan_create(*desc, g, M, G, &p)) {
+            free_layer(L);
+            return fail(AQ_ERR_UNSUPPORTED, "LUT plan: layer too large for the table kernel");
+        }
+        const int jc = p.jc;
+        // codes regrouped per chunk: [nchunk][C_out][jc*M], zero padded past G
         std::vector<uint8_t> rep((size_t)p.nchunk * C_out * jc * M, 0);
         const uint8_t* c = static_cast<const uint8_t*>(codes);
         for (int i = 0; i < C_out; ++i)

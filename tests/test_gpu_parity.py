@@ -178,6 +178,54 @@ def test_odd_shapes(spec):
 
 
 # ---------------------------------------------------------------------------
+# table (LUT) kernel: tokens per table entry, codebook counts, partial chunks
+# ---------------------------------------------------------------------------
+
+LUT_CASES = [
+    # (name, C_out, K, M, B, tokens, x dtype, codebook dtype, y dtype)
+    ("m2_n1", 300, 520, 2, 8, 1, "f16", "f16", "f16"),        # matrix-core table, one token, last chunk partial
+    ("m2_n2", 300, 520, 2, 8, 2, "f16", "f16", "f32"),
+    ("m2_n3", 97, 136, 2, 8, 3, "f16", "f16", "f32"),         # 3 tokens in a 4-token entry
+    ("m2_n9", 130, 64, 2, 8, 9, "i8", "f16", "f16"),          # int8 input, three passes of 4 tokens
+    ("m4_n5", 257, 576, 4, 8, 5, "f16", "f16", "f32"),
+    ("m1_n4", 64, 256, 1, 8, 4, "f16", "f16", "f32"),
+    ("m1_b5", 70, 200, 1, 5, 4, "f16", "f16", "f32"),         # 2^B < 32: zero entries past the codebook
+    ("m3_n4", 50, 392, 3, 8, 4, "f16", "f16", "f32"),         # two tokens per entry, 48-code runs
+    ("m5_n2", 40, 256, 5, 7, 2, "f16", "f16", "f32"),         # one token per entry
+    ("m8_n4", 33, 64, 8, 8, 4, "f16", "f16", "f32"),
+    ("f32_n4", 90, 264, 2, 8, 4, "f32", "f32", "f32"),        # fp32 FMA table
+    ("bf16cb_n1", 90, 264, 2, 8, 1, "f16", "bf16", "f32"),
+    ("bf16x_n6", 90, 264, 4, 6, 6, "bf16", "f16", "f32"),
+    ("n300", 40, 64, 2, 8, 300, "f16", "f16", "f32"),         # two launches of 256 tokens
+    ("long_k", 40, 38400, 2, 8, 1, "f16", "f16", "f32"),      # two chunks per workgroup
+    ("wide_long", 1100, 10944, 2, 8, 1, "f16", "f16", "f32"), # two row steps per workgroup
+    ("wide_long_n4", 1100, 10944, 4, 8, 4, "i8", "f16", "f16"),
+]
+
+
+@pytest.mark.parametrize("case", LUT_CASES, ids=lambda c: c[0])
+def test_lut_kernel(case):
+    name, C_out, K, M, B, n, xd, cbd, yd = case
+    spec = LayerSpec(name=name, C_out=C_out, K=K, g=8, M=M, B=B, n=n, x_dtype=xd, codebook_dtype=cbd, y_dtype=yd)
+    inp = generate(spec, 4321)
+    _say(f"lut {name}")
+    y = _run(spec, inp, "lut")
+    err = O.rel_err_inf(y, O.forward(spec, inp))
+    _say(f"  rel_err_inf={err:.3e}")
+    assert err <= (1e-5 if yd == "f32" else 2e-3)
+
+
+def test_lut_g9_conv_partial_chunk():
+    spec = LayerSpec(name="lut_g9", C_out=24, K=16 * 9, g=9, M=2, B=8, n=1, conv=ConvGeom(16, 3, 3, 1, 1, 3, 3),
+                     x_dtype="f16", codebook_dtype="f16", y_dtype="f32", tile_dtype="f32")
+    inp = generate(spec, 11)
+    y = _run(spec, inp, "lut")
+    err = O.rel_err_inf(y, O.forward(spec, inp))
+    _say(f"lut g9 conv rel_err_inf={err:.3e}")
+    assert err <= 1e-5
+
+
+# ---------------------------------------------------------------------------
 # fused decode + matrix-core kernel against the generic kernel and the oracle
 # ---------------------------------------------------------------------------
 
@@ -278,8 +326,15 @@ def test_dispatch_choice():
     spec = LayerSpec(name="disp", C_out=128, K=256, g=8, M=2, B=8, n=4096)
     inp = generate(spec, 1)
     layer = P.AQLayer(spec, inp)
-    assert layer.choose_path(1) == "lut"
-    assert layer.choose_path(4096) == "decode"
+    assert layer.choose_path(1) == "decode"          # short reduction: the matrix-core path wins
+    layer.set_path("lut")
+    assert layer.choose_path(4096) == "lut"
+    layer.close()
+    spec_k = LayerSpec(name="disp_k", C_out=64, K=8192, g=8, M=2, B=8, n=64)
+    layer = P.AQLayer(spec_k, generate(spec_k, 1))
+    assert layer.choose_path(1) == "lut"             # long reduction, few tokens: the table path
+    assert layer.choose_path(16) == "lut"
+    assert layer.choose_path(17) == "decode"
     layer.set_path("decode")
     assert layer.choose_path(1) == "decode"
     layer.close()
