@@ -115,6 +115,102 @@ def cpu_baseline(spec, inp, budget_s: float = 12.0):
     }
 
 
+def _graph_time_us(torch, fn, reps: int, trials: int = 5) -> float:
+    """Median per-call time of `fn` replayed from a HIP graph of `reps` calls (HIP events)."""
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    fn()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            for _ in range(reps):
+                fn()
+    torch.cuda.current_stream().wait_stream(stream)
+    graph.replay()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(trials):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        graph.replay()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b) * 1e3 / reps)
+    return statistics.median(times)
+
+
+def sweep_bench(a, torch, P, W):
+    """Every layer of the LDM-4-shaped U-Net sweep at batch 8: per-layer and whole-pass time.
+
+    Weights come from the seeded generators (one seed per layer); activations
+    are fp16 N(0, 1) drawn on the device from a seeded generator.  The whole
+    pass runs the layers back to back in one HIP graph, as a U-Net forward
+    would (each layer reads its own input; inter-layer glue is not part of
+    this measurement).
+    """
+    layers = W.sweep_layers(full=a.full)
+    M = {"W2": 2, "W4": 4}[a.variant]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(W.SEED_BASE + 4)
+    rows, calls, total_flops, total_bytes = [], [], 0, 0
+    objs = []
+    for i, lay in enumerate(layers):
+        spec = W.sweep_spec(lay, M, batch=8)
+        wts = W.generate(spec.with_n(1), W.SEED_BASE + 100 + i)       # weights are drawn before activations
+        layer = P.AQLayer(spec, wts, max_tokens=spec.tokens)
+        xshape = (spec.n, spec.K) if spec.conv is None else (spec.n, spec.conv.cin, spec.conv.H, spec.conv.W)
+        x = torch.randn(xshape, generator=gen, device="cuda", dtype=torch.float32).to(torch.float16)
+        y = torch.empty(layer.out_shape(spec.n), dtype=torch.float16, device="cuda")
+        fn = (lambda layer=layer, x=x, y=y: layer.forward(x, None, out=y))
+        us = _graph_time_us(torch, fn, reps=20)
+        flops, nbytes = spec.dense_flops, algorithmic_bytes(spec)
+        total_flops += flops
+        total_bytes += nbytes
+        rows.append((spec.name, lay.kind, spec.tokens, spec.K, spec.C_out, layer.choose_path(spec.tokens), us,
+                     flops / (us * 1e-6) / 1e12, lay.role))
+        calls.append(fn)
+        objs.append((layer, x, y))
+    whole_us = _graph_time_us(torch, lambda: [f() for f in calls], reps=1, trials=7)
+    per_layer_sum = sum(r[6] for r in rows)
+    if a.table:
+        with open(a.table, "w") as f:
+            f.write(f"# U-Net layer sweep, batch 8, {a.variant} (g=8, M={M}, B=8), fp16\n\n")
+            f.write(f"Command: `python bench.py --config sweep --variant {a.variant}"
+                    f"{' --full' if a.full else ''} --table <this file>`\n\n")
+            f.write(f"{len(rows)} layers, {total_flops / 1e9:.1f} dense-equivalent GFLOP.  Whole pass in one HIP "
+                    f"graph: {whole_us:.1f} us ({total_flops / (whole_us * 1e-6) / 1e12:.1f} TFLOP/s); sum of "
+                    f"per-layer times: {per_layer_sum:.1f} us.\n\n")
+            f.write("| layer | kind | tokens | K | C_out | path | us | TFLOP/s | note |\n|---|---|---|---|---|---|---|---|---|\n")
+            for r in rows:
+                f.write(f"| {r[0]} | {r[1]} | {r[2]} | {r[3]} | {r[4]} | {r[5]} | {r[6]:.2f} | {r[7]:.1f} | {r[8]} |\n")
+    for layer, _, _ in objs:
+        layer.close()
+    tflops = total_flops / (whole_us * 1e-6) / 1e12
+    return {
+        "metric": "dense-equivalent TFLOP/s of the AQ layer forward",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": 7,
+        "warmup": 1,
+        "ms_per_step": round(whole_us / 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded; LDM-4-shaped U-Net layers, random codebooks/codes/activations)",
+        "config": {"workload": f"unet_sweep_b8_{a.variant}{'_full' if a.full else ''}", "layers": len(rows),
+                   "launch": "hip graph of the whole pass"},
+        "hbm_gbs_algorithmic": round(total_bytes / (whole_us * 1e-6) / 1e9, 3),
+        "algorithmic_bytes": total_bytes,
+        "dense_flops": total_flops,
+        "per_layer_sum_us": round(per_layer_sum, 3),
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_MFMA_F16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / PEAK_MFMA_F16_TFLOPS, 4), "traffic": None},
+    }
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -126,6 +222,9 @@ def main(argv=None):
     ap.add_argument("--no-graph", action="store_true", help="launch every step from Python instead of a HIP graph")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run one plain device copy of this many bytes (counter calibration)")
+    ap.add_argument("--variant", default="W2", choices=["W2", "W4"], help="sweep: 2 or 4 bits per weight")
+    ap.add_argument("--full", action="store_true", help="sweep: every linear of the transformer blocks")
+    ap.add_argument("--table", default="", help="sweep: write the per-layer table (markdown) here")
     a = ap.parse_args(argv)
 
     if a.gpus != 1:
@@ -141,6 +240,9 @@ def main(argv=None):
 
     P.load_library()
     torch.cuda.set_device(0)
+    if a.config == "sweep":
+        print(json.dumps(sweep_bench(a, torch, P, W)), flush=True)
+        return 0
     spec = W.config_spec(a.config)
     inp = W.config_inputs(a.config)
     layer = P.AQLayer(spec, inp)

@@ -166,7 +166,7 @@ bool lut_plan_create(const aq_layer_desc& d, int g, int M, int G, LutPlan* p) {
     p->nchunk = (G + jc - 1) / jc;
     p->nt_max = nt;
     p->mfma_table = d.codebook_dtype == AQ_F16 && (d.x_dtype == AQ_F16 || d.x_dtype == AQ_I8) && g == 8;
-    int64_t tb = std::min<int64_t>(d.max_tokens, 256);
+    int64_t tb = std::min<int64_t>(d.max_tokens, 32);   // the table path serves few tokens per launch
     p->tok_block = (int)((tb + 3) / 4 * 4);
     // 32-bit code offsets in the kernel
     return (int64_t)p->nchunk * d.out_features * jc * M < (int64_t(1) << 31);
