@@ -25,6 +25,7 @@ static hipError_t conv_dec(const Geom& geo, const FusedPlan& p, const FusedLaunc
     if (p.dec == FUSED_DEC_PK16 && p.mc == 2) return conv_tiles<KIND, CM, FUSED_DEC_PK16, 2>(geo, p, fl);
     if (p.dec == FUSED_DEC_PK16 && p.mc == 4) return conv_tiles<KIND, CM, FUSED_DEC_PK16, 4>(geo, p, fl);
     if (p.dec == FUSED_DEC_T16G) return conv_tiles<KIND, CM, FUSED_DEC_T16G, 1>(geo, p, fl);
+    if (p.dec == FUSED_DEC_REC) return conv_tiles<KIND, CM, FUSED_DEC_REC, 1>(geo, p, fl);
     return hipErrorInvalidConfiguration;
 }
 

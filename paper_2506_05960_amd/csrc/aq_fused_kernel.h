@@ -177,6 +177,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     constexpr int NS = KIND == 1 ? 9 : CM;         // MFMA steps per chunk (= groups per lane)
     constexpr int AM = BM / 32, AN = BN / 32;
     using EntT = typename std::conditional<DEC == FUSED_DEC_T16G, uint16_t, uint8_t>::type;   // one code
+    constexpr bool CB_LDS = DEC != FUSED_DEC_T16G && DEC != FUSED_DEC_REC;   // codebook copied to LDS
     static_assert(KIND != 1 || CM == 1, "3x3 chunks are 16 channels");
 
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -207,10 +208,10 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // LDS layout [m][256 rows][row bytes]; the source is [m][2^B rows][row bytes].
     uint8_t* cb_lds = lds;
     constexpr int ROWB = DEC == FUSED_DEC_F32L ? 32 : 16;
-    constexpr int CB_PER_T = DEC == FUSED_DEC_T16G ? 0 : (MC * 256 * ROWB) / (16 * 256);
+    constexpr int CB_PER_T = CB_LDS ? (MC * 256 * ROWB) / (16 * 256) : 0;
     u32x4 cbr[CB_PER_T > 0 ? CB_PER_T : 1];
     const int rows_b = 1 << geo.B;
-    if constexpr (DEC != FUSED_DEC_T16G) {
+    if constexpr (CB_LDS) {
         const u32x4* src = static_cast<const u32x4*>(cb);
 #pragma unroll
         for (int i = 0; i < CB_PER_T; ++i) {
@@ -356,10 +357,13 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     };
 
     // ---- code records of one chunk: global -> registers ----
-    constexpr int REC_DW = (NS * MC * (int)sizeof(EntT) + 3) / 4;   // record dwords
+    constexpr int REC_DW = DEC == FUSED_DEC_REC ? 1 : (NS * MC * (int)sizeof(EntT) + 3) / 4;   // record dwords
     const __amdgpu_buffer_rsrc_t cr = buffer_rsrc(crec, (uint64_t)plan.nchunk * chunk_rec_stride);
+    // pre-decoded mode: operand record (chunk, step, channel, lane half), 16 bytes each
+    const __amdgpu_buffer_rsrc_t wr = buffer_rsrc(crec, (uint64_t)plan.nchunk * NS * geo.C_out * 32u);
     uint32_t crg[AN][REC_DW];
     auto codes_load = [&](int chunk) {
+        if constexpr (DEC == FUSED_DEC_REC) return;
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
             const uint32_t off = c_ok[b] ? c_off[b] + (uint32_t)chunk * chunk_rec_stride : kOutOfRange;
@@ -440,9 +444,16 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     };
     constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L && NS * MC <= 18;
     // weights of one 32-channel block of a chunk, decoded into MFMA operands
-    auto decode_block = [&](const uint32_t* codes_dw, u32x4 (&d)[NS]) {
+    auto decode_block = [&](const uint32_t* codes_dw, int dchunk, int db, u32x4 (&d)[NS]) {
         const EntT* ev = reinterpret_cast<const EntT*>(codes_dw);
-        if constexpr (LOOKAHEAD) {
+        if constexpr (DEC == FUSED_DEC_REC) {
+            const bool ok = c_ok[db] && dchunk < plan.nchunk;
+            const uint32_t base = (uint32_t)(((dchunk * NS) * geo.C_out + N0 + 32 * db + l32) * 2 + q) * 16u;
+#pragma unroll
+            for (int g = 0; g < NS; ++g)
+                d[g] = __builtin_amdgcn_raw_buffer_load_b128(
+                    wr, ok ? base + (uint32_t)(g * geo.C_out * 32) : kOutOfRange, 0, 0);
+        } else if constexpr (LOOKAHEAD) {
             GroupRaw<DEC, MC> raw[NS];
 #pragma unroll
             for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
@@ -470,7 +481,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         stage_load(chunk);
         codes_load(chunk);
     }
-    if constexpr (DEC != FUSED_DEC_T16G) {
+    if constexpr (CB_LDS) {
 #pragma unroll
         for (int i = 0; i < CB_PER_T; ++i) reinterpret_cast<u32x4*>(cb_lds)[tid + 256 * i] = cbr[i];
     }
@@ -479,7 +490,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         stage_store(pbuf0);
         wave_sync();
         load_af(pbuf0, af);
-        if constexpr (LOOKAHEAD) decode_block(crg[0], dec);
+        if constexpr (LOOKAHEAD) decode_block(crg[0], chunk, 0, dec);
     }
     int it = 0;
     for (; chunk < plan.nchunk; chunk += kWaves, ++it) {
@@ -501,19 +512,19 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             bool have_next = false;
             if constexpr (LOOKAHEAD) {
                 if (b + 1 < AN) {
-                    decode_block(crn[b + 1], dnext);
+                    decode_block(crn[b + 1], chunk, b + 1, dnext);
                     have_next = true;
                 } else if (more) {
-                    decode_block(crg[0], dnext);   // block 0 of the next chunk
+                    decode_block(crg[0], chunk + kWaves, 0, dnext);   // block 0 of the next chunk
                     have_next = true;
                 }
             } else {
-                decode_block(crn[b], dec);
+                decode_block(crn[b], chunk, b, dec);
             }
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 u32x4 bf;
-                if constexpr (KIND == 1) {
+                if constexpr (KIND == 1 && DEC != FUSED_DEC_REC) {
                     // position s: channel e of the lane's 8 is decoded value 9e + s
 #pragma unroll
                     for (int d = 0; d < 4; ++d) {

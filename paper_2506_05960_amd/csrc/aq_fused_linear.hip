@@ -20,6 +20,7 @@ static hipError_t lin_dec(const Geom& geo, const FusedPlan& p, const FusedLaunch
     if (p.dec == FUSED_DEC_PK16 && p.mc == 2) return lin_tiles<XT, FUSED_DEC_PK16, 2>(geo, p, fl);
     if (p.dec == FUSED_DEC_PK16 && p.mc == 4) return lin_tiles<XT, FUSED_DEC_PK16, 4>(geo, p, fl);
     if (p.dec == FUSED_DEC_T16G) return lin_tiles<XT, FUSED_DEC_T16G, 1>(geo, p, fl);
+    if (p.dec == FUSED_DEC_REC) return lin_tiles<XT, FUSED_DEC_REC, 1>(geo, p, fl);
     return hipErrorInvalidConfiguration;
 }
 

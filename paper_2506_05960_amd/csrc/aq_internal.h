@@ -44,7 +44,8 @@ enum FusedDec {
     FUSED_DEC_PK16 = 0,   // fp16 codebooks in LDS, codewords accumulated with packed fp16 adds
     FUSED_DEC_F32L = 1,   // fp32 codebooks in LDS, fp32 sum in ascending m
     FUSED_DEC_T16L = 2,   // M == 1, codebook pre-rounded to fp16, in LDS
-    FUSED_DEC_T16G = 3    // M == 1, codebook pre-rounded to fp16, read from global memory (B > 8)
+    FUSED_DEC_T16G = 3,   // M == 1, codebook pre-rounded to fp16, read from global memory (B > 8)
+    FUSED_DEC_REC = 4     // operands decoded beforehand into per-step records (one 16-byte load each)
 };
 
 struct FusedPlan {
@@ -77,6 +78,12 @@ struct FusedLaunch {
 };
 
 hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+
+// Operand records of the pre-decoded mode: record (chunk, step, channel, lane
+// half) = the 8 fp16 weights of that matrix-core B operand, unscaled.
+size_t operand_record_bytes(const Geom& geo, const FusedPlan& plan);
+hipError_t launch_operand_records(const Geom& geo, const FusedPlan& plan, const DeviceWeights& w, void* rec,
+                                  hipStream_t stream);
 hipError_t launch_fused_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 hipError_t launch_fused_conv1(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 hipError_t launch_fused_linear(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);

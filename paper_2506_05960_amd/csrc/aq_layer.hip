@@ -28,6 +28,7 @@ struct aq_layer {
     LutPlan plan;
     aq::FusedPlan fplan;
     uint8_t* d_crec;          // fused-path code records (null when the fused path does not apply)
+    void* d_wrec;             // fused-path operand records, decoded per forward in the pre-decoded mode
     bool lut_ok, dec_ok, fused_ok;
     aq_path path;
     int64_t lut_max_tokens;
@@ -124,7 +125,8 @@ aq_path choose(const aq_layer* L, int64_t tokens) {
 
 void free_layer(aq_layer* L) {
     if (!L) return;
-    void* ptrs[] = {L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, L->d_ws, L->d_crec};
+    void* ptrs[] = {L->d_cb,        L->d_cb32,   L->d_cbtile, L->d_codes, L->d_codes_lut,
+                    L->d_scales,    L->d_ws,     L->d_crec,   L->d_wrec};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete L;
@@ -282,8 +284,12 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
         if (q.lds_bytes > kLdsBytes) continue;
         const int64_t nwg = ((geo.tokens + t.bm - 1) / t.bm) * (int64_t)((geo.C_out + t.bn - 1) / t.bn);
         const int64_t rounds = (nwg + 255) / 256;
-        // rounds of whole-chip work, weighted by a per-tile overhead term
-        const double cost = (double)rounds * t.bm * t.bn * (1.0 + 48.0 / t.bm + 48.0 / t.bn) * t.upl / (t.upl + 2.0);
+        // rounds of whole-chip work, weighted by a per-tile overhead term; linear
+        // layers also weigh the staging units per lane (fitted to measured tiles)
+        double cost = (double)rounds * t.bm * t.bn * (1.0 + 48.0 / t.bm + 48.0 / t.bn);
+        if (p->kind == 0) cost *= t.upl / (t.upl + 2.0);
+        // pre-decoded operands of a linear layer: the 64 x 64 tile measured best
+        if (p->kind == 0 && p->dec == aq::FUSED_DEC_REC && !(t.bm == 64 && t.bn == 64)) cost *= 1.25;
         if (!found || cost < best) {
             best = cost;
             bestp = q;
@@ -292,6 +298,24 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
     }
     if (found) *p = bestp;
     return found;
+}
+
+// Pre-decoded mode (operands decoded once per forward into records the main
+// loop reads with plain 16-byte loads) instead of decoding inside the main
+// loop: chosen for codebooks too large for LDS (their codeword reads from L2
+// repeat for every token tile) once there are enough token tiles to repay the
+// extra pass.  AQ_FUSED_REC=1 / 0 forces it on / off.
+bool use_predecoded(const aq_layer* L, const Geom& geo) {
+    if (const char* s = std::getenv("AQ_FUSED_REC")) return std::atoi(s) != 0;
+    const int64_t token_tiles = (geo.tokens + 63) / 64;
+    const aq::FusedPlan& p = L->fplan;
+    if (p.dec == aq::FUSED_DEC_T16G) return token_tiles >= 8;
+    // measured on the U-Net layer shapes: the in-loop decode is repeated for every
+    // token tile, so the single decode pass wins once tokens x M is large enough
+    const int64_t tm = geo.tokens * p.mc;
+    if (p.kind == 1) return tm >= 32768 || (tm >= 8192 && geo.K >= 5000);
+    if (p.kind == 0) return p.mc >= 4 && geo.C_out >= 1152 && geo.tokens >= 2048;
+    return p.mc >= 4 && geo.tokens >= 32768;
 }
 
 }  // namespace
@@ -395,6 +419,8 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
     if (L->fused_ok) {
         std::vector<uint8_t> rec = fused_records(L->fplan, codes, C_out, G, M, B);
         AQ_TRY(dev_upload(&L->d_crec, rec.data(), rec.size(), "fused code records"));
+        const Geom g1 = make_geom(L, 1);
+        AQ_TRY(dev_upload(&L->d_wrec, nullptr, aq::operand_record_bytes(g1, L->fplan), "operand records"));
     }
 
     e = aq::launch_codebook_prep(L->d_cb, desc->codebook_dtype, (int64_t)cb_elems, L->d_cb32, L->d_cbtile,
@@ -436,12 +462,24 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
         // the fused kernel uses 32-bit element and byte offsets
         const bool fits31 = geo.tokens * (int64_t)std::max(geo.K, geo.C_out) * 4 < (int64_t(1) << 31) &&
                             (!geo.conv || n * (int64_t)geo.cin * geo.H * geo.W * 2 < (int64_t(1) << 31));
+        if (L->fused_ok && use_predecoded(L, geo)) {
+            // pre-decoded mode: operands decoded once per forward, then read with plain loads
+            fp.dec = aq::FUSED_DEC_REC;
+            fp.mc = 1;
+            fp.cb_bytes = 0;
+        }
         if (L->fused_ok && fits31 && !std::getenv("AQ_NO_FUSED") && fused_plan_tile(geo, &fp)) {
             const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
                                 : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
                                                                : L->d_cbtile;
-            const aq::FusedLaunch fl{cbsrc, L->d_crec, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
-            e = aq::launch_fused_forward(geo, fp, fl);
+            const uint8_t* recs = L->d_crec;
+            e = hipSuccess;
+            if (fp.dec == aq::FUSED_DEC_REC) {
+                e = aq::launch_operand_records(geo, fp, w, L->d_wrec, st);
+                recs = static_cast<const uint8_t*>(L->d_wrec);
+            }
+            const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
+            if (e == hipSuccess) e = aq::launch_fused_forward(geo, fp, fl);
         } else {
             e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
         }

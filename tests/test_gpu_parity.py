@@ -259,6 +259,21 @@ def test_fused_matches_oracle_and_generic(spec, monkeypatch):
     assert e1 <= 2e-3 and e2 <= 2e-3
 
 
+@pytest.mark.parametrize("spec", FUSED, ids=lambda s: s.name)
+def test_predecoded_operands_match_in_loop_decode(spec, monkeypatch):
+    """Pre-decoded operand records give bit-identical outputs to decoding inside the main loop."""
+    inp = generate(spec, 31)
+    monkeypatch.setenv("AQ_FUSED_REC", "1")
+    y_rec = _run(spec, inp, "decode")
+    monkeypatch.setenv("AQ_FUSED_REC", "0")
+    y_loop = _run(spec, inp, "decode")
+    monkeypatch.delenv("AQ_FUSED_REC")
+    err = O.rel_err_inf(y_rec, O.forward(spec, inp))
+    _say(f"predecoded {spec.name} err={err:.3e} identical={np.array_equal(y_rec, y_loop)}")
+    assert np.array_equal(y_rec, y_loop)
+    assert err <= 2e-3
+
+
 @pytest.mark.parametrize("tile", ["64x96", "64x64", "128x64", "32x128", "32x64"])
 def test_fused_tiles(tile, monkeypatch):
     """Every instantiated tile of the fused kernel on a conv and a linear layer."""
@@ -277,9 +292,11 @@ def test_fused_tiles(tile, monkeypatch):
 # exact checks through the fused path
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("M,B", [(3, 8), (2, 12), (1, 16), (2, 8), (4, 8), (4, 6)])
-def test_one_hot_rows_read_back_decoded_tile(M, B):
+@pytest.mark.parametrize("M,B,rec", [(3, 8, "0"), (2, 12, "0"), (1, 16, "0"), (2, 8, "0"), (4, 8, "0"), (4, 6, "0"),
+                                     (1, 16, "1"), (2, 8, "1"), (4, 8, "1")])
+def test_one_hot_rows_read_back_decoded_tile(M, B, rec, monkeypatch):
     """X = identity (fp16) through the matrix-core path returns fl32(W_tile * s) exactly."""
+    monkeypatch.setenv("AQ_FUSED_REC", rec)
     spec = LayerSpec(name="onehot", C_out=160, K=256, g=8, M=M, B=B, n=256, y_dtype="f32")
     inp = generate(spec, 99)
     inp["x"] = np.eye(256, dtype=np.float16)
