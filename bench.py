@@ -211,6 +211,65 @@ def sweep_bench(a, torch, P, W):
     }
 
 
+def lut_regime_bench(a, torch, P, W):
+    """Table path vs matrix-core path for few tokens on U-Net linear shapes (fp16, B = 8).
+
+    Each (K, C_out, M) layer is timed at every token count with both paths
+    forced, weights warm in the caches (the same layer runs back to back in a
+    HIP graph).  Algorithmic bytes: codes + codebooks + scales + X + Y.
+    """
+    ns = (1, 2, 4, 8, 16, 32)
+    shapes = sorted(set((s.K, s.C_out, s.M) for s in W.lut_regime_specs()))
+    rows = []
+    for K, C, M in shapes:
+        base = W.LayerSpec(name=f"lut_{K}to{C}_M{M}", C_out=C, K=K, g=8, M=M, B=8, n=max(ns))
+        inp = W.generate(base, W.SEED_BASE + 200 + len(rows))
+        layer = P.AQLayer(base, inp, max_tokens=max(ns))
+        xfull = torch.from_numpy(inp["x"]).cuda()
+        for n in ns:
+            spec = base.with_n(n)
+            x = xfull[:n].contiguous()
+            y = torch.empty((n, C), dtype=torch.float16, device="cuda")
+            t = {}
+            for path in ("lut", "decode"):
+                layer.set_path(path)
+                t[path] = _graph_time_us(torch, lambda: layer.forward(x, None, out=y), reps=20)
+            layer.set_path("auto")
+            rows.append((K, C, M, n, t["lut"], t["decode"], algorithmic_bytes(spec), layer.choose_path(n)))
+        layer.close()
+    if a.table:
+        with open(a.table, "w") as f:
+            f.write("# Table (LUT) path vs matrix-core path at few tokens, fp16, g=8, B=8\n\n")
+            f.write("Command: `python bench.py --config lutregime --table <this file>`\n\n")
+            f.write("Weights warm in the caches (same layer replayed in a HIP graph); GB/s are algorithmic bytes "
+                    "(codes, codebooks, scales, X, Y) over the table-path time.\n\n")
+            f.write("| K | C_out | M | tokens | table us | table GB/s | matrix-core us | faster | dispatch |\n"
+                    "|---|---|---|---|---|---|---|---|---|\n")
+            for K, C, M, n, tl, td, ab, ch in rows:
+                f.write(f"| {K} | {C} | {M} | {n} | {tl:.2f} | {ab / tl / 1e3:.0f} | {td:.2f} | "
+                        f"{'table' if tl < td else 'matrix-core'} | {ch} |\n")
+    best = max(rows, key=lambda r: r[6] / r[4])
+    gbs = best[6] / best[4] / 1e3
+    return {
+        "metric": "dense-equivalent TFLOP/s and HBM GB/s of AQ layer forward (table path)",
+        "value": round(gbs, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": 20,
+        "warmup": 1,
+        "ms_per_step": round(best[4] / 1e3, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded; U-Net linear shapes at few tokens)",
+        "config": {"workload": f"lut_{best[0]}to{best[1]}_M{best[2]}_n{best[3]}", "path": "lut",
+                   "launch": "hip graph of 20 steps", "cases": len(rows)},
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 3), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None},
+    }
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -242,6 +301,9 @@ def main(argv=None):
     torch.cuda.set_device(0)
     if a.config == "sweep":
         print(json.dumps(sweep_bench(a, torch, P, W)), flush=True)
+        return 0
+    if a.config == "lutregime":
+        print(json.dumps(lut_regime_bench(a, torch, P, W)), flush=True)
         return 0
     spec = W.config_spec(a.config)
     inp = W.config_inputs(a.config)
