@@ -78,6 +78,8 @@ struct FusedLaunch {
 };
 
 hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+// Dense matrix-core product over pre-decoded operand records (fl.crec), tile plan.bm x plan.bn.
+hipError_t launch_rec_gemm(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 
 // Operand records of the pre-decoded mode: record (chunk, step, channel, lane
 // half) = the 8 fp16 weights of that matrix-core B operand, unscaled.

@@ -300,6 +300,62 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
     return found;
 }
 
+// Tile of the dense product over pre-decoded records: the workgroup stages
+// each chunk's activations (all BM tokens) and weight records (BN channels)
+// in two LDS stages.  Returns false when no tile fits.
+bool gemm_plan_tile(const Geom& geo, aq::FusedPlan* p) {
+    static const TileCand cands[] = {{128, 128, 0}, {128, 64, 0}, {64, 128, 0}};
+    int want_bm = 0, want_bn = 0;
+    if (const char* s = std::getenv("AQ_GEMM_TILE")) std::sscanf(s, "%dx%d", &want_bm, &want_bn);
+    const int ns = p->kind == 1 ? 9 : p->cm;
+    double best = 0;
+    aq::FusedPlan bestp{};
+    bool found = false;
+    for (const TileCand& t : cands) {
+        if (want_bm && (t.bm != want_bm || t.bn != want_bn)) continue;
+        aq::FusedPlan q = *p;
+        q.bm = t.bm;
+        q.bn = t.bn;
+        int max_units;
+        if (p->kind != 0) {
+            if (!(t.bm % geo.OW == 0 || geo.OW % t.bm == 0)) continue;
+            const int tr = t.bm >= geo.OW ? t.bm / geo.OW : 1;
+            const int kh = p->kind == 1 ? 3 : 1;
+            q.pr = tr * kh;
+            q.pw = geo.W + 2 * geo.pad;
+            // A fragment reads: 16 consecutive lanes are consecutive tokens; when an
+            // output row is shorter than 16 they span rows, so widen the staged row
+            // until consecutive rows start OW 16-byte slots apart modulo the 64 banks
+            if (geo.OW < 16 && geo.stride == 1)
+                while ((kh * q.pw - geo.OW) % 16 != 0) ++q.pw;
+            q.ps = q.pr * q.pw * 16;
+            q.units = 2 * p->cm * q.pr * (geo.W / 2);
+            q.total_rows = (int)(geo.tokens / geo.OW);
+            max_units = 256 * 3;
+        } else {
+            q.pr = q.pw = 0;
+            q.ps = t.bm * 16 + 16;
+            q.units = t.bm * 2 * p->cm;
+            q.total_rows = 0;
+            max_units = 256 * 4;
+        }
+        if (q.units > max_units) continue;
+        q.pbuf_bytes = 2 * p->cm * q.ps + 32;
+        q.lds_bytes = (size_t)2 * (q.pbuf_bytes + (size_t)ns * t.bn * 32);
+        if (q.lds_bytes > kLdsBytes) continue;
+        const int64_t nwg = ((geo.tokens + t.bm - 1) / t.bm) * (int64_t)((geo.C_out + t.bn - 1) / t.bn);
+        const int64_t rounds = (nwg + 255) / 256;
+        const double cost = (double)rounds * t.bm * t.bn * (1.0 + 64.0 / t.bm + 64.0 / t.bn);
+        if (!found || cost < best) {
+            best = cost;
+            bestp = q;
+            found = true;
+        }
+    }
+    if (found) *p = bestp;
+    return found;
+}
+
 // Pre-decoded mode (operands decoded once per forward into records the main
 // loop reads with plain 16-byte loads) instead of decoding inside the main
 // loop: chosen for codebooks too large for LDS (their codeword reads from L2
@@ -468,7 +524,18 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
             fp.mc = 1;
             fp.cb_bytes = 0;
         }
-        if (L->fused_ok && fits31 && !std::getenv("AQ_NO_FUSED") && fused_plan_tile(geo, &fp)) {
+        aq::FusedPlan gp = fp;
+        // dense product over the records: a comparator route (AQ_GEMM=1); measured
+        // slower than the fused kernel's pre-decoded mode on every layer shape here
+        const char* ge = std::getenv("AQ_GEMM");
+        const bool gemm = L->fused_ok && fits31 && fp.dec == aq::FUSED_DEC_REC && ge && std::atoi(ge) != 0 &&
+                          gemm_plan_tile(geo, &gp);
+        if (gemm) {
+            e = aq::launch_operand_records(geo, gp, w, L->d_wrec, st);
+            const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(L->d_wrec), L->d_scales, X, xs, Y,
+                                     d.y_dtype, d.x_dtype, st};
+            if (e == hipSuccess) e = aq::launch_rec_gemm(geo, gp, fl);
+        } else if (L->fused_ok && fits31 && !std::getenv("AQ_NO_FUSED") && fused_plan_tile(geo, &fp)) {
             const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
                                 : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
                                                                : L->d_cbtile;

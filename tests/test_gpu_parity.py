@@ -265,12 +265,41 @@ def test_predecoded_operands_match_in_loop_decode(spec, monkeypatch):
     inp = generate(spec, 31)
     monkeypatch.setenv("AQ_FUSED_REC", "1")
     y_rec = _run(spec, inp, "decode")
+    monkeypatch.setenv("AQ_GEMM", "1")
+    y_gemm = _run(spec, inp, "decode")            # dense product over the same records
+    monkeypatch.delenv("AQ_GEMM")
     monkeypatch.setenv("AQ_FUSED_REC", "0")
     y_loop = _run(spec, inp, "decode")
     monkeypatch.delenv("AQ_FUSED_REC")
-    err = O.rel_err_inf(y_rec, O.forward(spec, inp))
-    _say(f"predecoded {spec.name} err={err:.3e} identical={np.array_equal(y_rec, y_loop)}")
+    y_ref = O.forward(spec, inp)
+    err, err_g = O.rel_err_inf(y_rec, y_ref), O.rel_err_inf(y_gemm, y_ref)
+    _say(f"predecoded {spec.name} err={err:.3e} gemm err={err_g:.3e} identical={np.array_equal(y_rec, y_loop)}")
     assert np.array_equal(y_rec, y_loop)
+    assert err <= 2e-3 and err_g <= 2e-3
+
+
+GEMM_CASES = [
+    LayerSpec(name="g_conv3", C_out=200, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 24, 16)),
+    LayerSpec(name="g_conv3_img8", C_out=150, K=48 * 9, g=8, M=1, B=16, n=5, conv=ConvGeom(48, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="g_conv3_s2", C_out=70, K=16 * 9, g=8, M=4, B=8, n=2, conv=ConvGeom(16, 3, 3, 2, 1, 32, 32)),
+    LayerSpec(name="g_conv1", C_out=130, K=128, g=8, M=2, B=8, n=2, conv=ConvGeom(128, 1, 1, 1, 0, 16, 24)),
+    LayerSpec(name="g_lin", C_out=300, K=200, g=8, M=4, B=8, n=333),
+    LayerSpec(name="g_lin_i8", C_out=170, K=136, g=8, M=4, B=8, n=129, x_dtype="i8"),
+    LayerSpec(name="g_lin_f32y", C_out=64, K=64, g=8, M=2, B=8, n=1000, y_dtype="f32"),
+]
+
+
+@pytest.mark.parametrize("tile", ["128x128", "128x64", "64x128"])
+@pytest.mark.parametrize("spec", GEMM_CASES, ids=lambda s: s.name)
+def test_dense_product_over_records(spec, tile, monkeypatch):
+    """Every tile of the dense product over pre-decoded records, against the oracle."""
+    monkeypatch.setenv("AQ_FUSED_REC", "1")
+    monkeypatch.setenv("AQ_GEMM", "1")
+    monkeypatch.setenv("AQ_GEMM_TILE", tile)
+    inp = generate(spec, 8)
+    y = _run(spec, inp, "decode")
+    err = O.rel_err_inf(y, O.forward(spec, inp))
+    _say(f"gemm {spec.name} {tile} err={err:.3e}")
     assert err <= 2e-3
 
 
