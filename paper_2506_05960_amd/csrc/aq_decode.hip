@@ -74,60 +74,66 @@ static hipError_t decode_dispatch_cb(const Geom& geo, const DeviceWeights& w, in
 // ---- operand records for the fused kernel's pre-decoded mode ----
 //
 // One thread per (chunk c, channel n, lane half q).  It decodes the groups
-// that lane of the fused kernel would decode -- a 3x3 chunk's groups
-// 18c + 9q + s, s < 9 (16 channels, channel outermost), or a 64-wide chunk's
-// groups 8c + 2s + q, s < 4 -- with the same arithmetic (codewords summed in
-// ascending m: in fp16 for an fp16 codebook, else in fp32 rounded once), and
-// writes the B operand of each step s.  For a 3x3 chunk the operand of
-// kernel position s is value 9e + s of the lane's 72 decoded values
-// (e = channel 0..7); otherwise it is group s itself.  Groups past the end of
-// K are zero.
-template <int CBT, typename CodeT>
+// that lane of the fused kernel covers -- a 3x3 chunk's 72 weights of 8 input
+// channels (K indices [(16c + 8q) * 9, + 72), channel outermost), or a
+// 64-wide chunk's groups 8c + 2s + q, s < 4 -- with the decode arithmetic
+// (codewords summed in ascending m: in fp16 for an fp16 codebook, else in fp32
+// rounded once), and writes the B operand of each step s.  For a 3x3 chunk the
+// operand of kernel position s is weight 9e + s of the 72 (e = channel 0..7);
+// otherwise it is group s itself.  Groups past the end of K are zero.
+template <int CBT, typename CodeT, int G>
 __device__ __forceinline__ void decode_group_f16(const void* cb, const CodeT* code, int M, int64_t rows,
-                                                 uint16_t (&v)[8]) {
+                                                 uint16_t (&v)[G]) {
     if constexpr (CBT == AQ_F16) {
         const uint16_t* c16 = static_cast<const uint16_t*>(cb);
-        _Float16 h[8];
+        _Float16 h[G];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) h[t] = __builtin_bit_cast(_Float16, c16[(int64_t)code[0] * 8 + t]);
+        for (int t = 0; t < G; ++t) h[t] = __builtin_bit_cast(_Float16, c16[(int64_t)code[0] * G + t]);
         for (int m = 1; m < M; ++m)
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-                h[t] = h[t] + __builtin_bit_cast(_Float16, c16[((int64_t)m * rows + code[m]) * 8 + t]);
+            for (int t = 0; t < G; ++t)
+                h[t] = h[t] + __builtin_bit_cast(_Float16, c16[((int64_t)m * rows + code[m]) * G + t]);
 #pragma unroll
-        for (int t = 0; t < 8; ++t) v[t] = __builtin_bit_cast(uint16_t, h[t]);
+        for (int t = 0; t < G; ++t) v[t] = __builtin_bit_cast(uint16_t, h[t]);
     } else {
-        float a[8];
+        float a[G];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) a[t] = load_as_f32<CBT>(cb, (int64_t)code[0] * 8 + t);
+        for (int t = 0; t < G; ++t) a[t] = load_as_f32<CBT>(cb, (int64_t)code[0] * G + t);
         for (int m = 1; m < M; ++m)
 #pragma unroll
-            for (int t = 0; t < 8; ++t) a[t] = __fadd_rn(a[t], load_as_f32<CBT>(cb, ((int64_t)m * rows + code[m]) * 8 + t));
+            for (int t = 0; t < G; ++t) a[t] = __fadd_rn(a[t], load_as_f32<CBT>(cb, ((int64_t)m * rows + code[m]) * G + t));
 #pragma unroll
-        for (int t = 0; t < 8; ++t) v[t] = f32_to_f16(opaque_f32(a[t]));
+        for (int t = 0; t < G; ++t) v[t] = f32_to_f16(opaque_f32(a[t]));
     }
 }
 
-template <int CBT, typename CodeT, bool K3>
+// K3: a 3x3 chunk (16 input channels); G: group size 8, or 9 (one group per
+// input channel's filter, the kernel-aware format of Sec. 3.1.2).  The lane's
+// 72 weights are K indices [(16c + 8q) * 9, + 72): nine groups of 8 or eight
+// groups of 9.
+template <int CBT, typename CodeT, bool K3, int G>
 __global__ void __launch_bounds__(256)
 operand_records_kernel(const void* __restrict__ cb, const CodeT* __restrict__ codes, u32x4* __restrict__ rec,
-                       int nchunk, int C_out, int G, int M, int B) {
+                       int nchunk, int C_out, int Gn, int M, int B) {
     constexpr int ns = K3 ? 9 : 4;
+    constexpr int NG = K3 ? 72 / G : 4;            // groups a thread decodes
+    static_assert(K3 || G == 8, "64-wide chunks use groups of 8");
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // (chunk, channel, half)
     if (idx >= (int64_t)nchunk * C_out * 2) return;
     const int c = (int)(idx / (2 * C_out));
     const int rem = (int)(idx - (int64_t)c * 2 * C_out);
     const int n = rem >> 1, q = rem & 1;
     const int64_t rows = (int64_t)1 << B;
-    uint16_t v[ns][8];
+    const int j0 = K3 ? (16 * c + 8 * q) * 9 / G : 0;
+    uint16_t v[NG][G];
 #pragma unroll
-    for (int s = 0; s < ns; ++s) {
-        const int j = K3 ? 18 * c + 9 * q + s : c * 2 * ns + 2 * s + q;
-        if (j < G) {
-            decode_group_f16<CBT, CodeT>(cb, codes + ((int64_t)n * G + j) * M, M, rows, v[s]);
+    for (int s = 0; s < NG; ++s) {
+        const int j = K3 ? j0 + s : c * 2 * ns + 2 * s + q;
+        if (j < Gn) {
+            decode_group_f16<CBT, CodeT, G>(cb, codes + ((int64_t)n * Gn + j) * M, M, rows, v[s]);
         } else {
 #pragma unroll
-            for (int t = 0; t < 8; ++t) v[s][t] = 0;
+            for (int t = 0; t < G; ++t) v[s][t] = 0;
         }
     }
 #pragma unroll
@@ -137,9 +143,10 @@ operand_records_kernel(const void* __restrict__ cb, const CodeT* __restrict__ co
         for (int d = 0; d < 4; ++d) {
             uint32_t lo, hi;
             if constexpr (K3) {
+                // position s of channel e (of the lane's 8) is weight 9e + s of the run
                 const int v0 = 9 * (2 * d) + s, v1 = 9 * (2 * d + 1) + s;
-                lo = v[v0 >> 3][v0 & 7];
-                hi = v[v1 >> 3][v1 & 7];
+                lo = v[v0 / G][v0 % G];
+                hi = v[v1 / G][v1 % G];
             } else {
                 lo = v[s][2 * d];
                 hi = v[s][2 * d + 1];
@@ -163,13 +170,18 @@ static hipError_t records_dispatch(const Geom& geo, const FusedPlan& plan, const
     const CodeT* codes = static_cast<const CodeT*>(w.codes);
     u32x4* r = static_cast<u32x4*>(rec);
     if (plan.kind != 1 && plan.cm != 4) return hipErrorInvalidConfiguration;
+    if (geo.g != 8 && !(geo.g == 9 && plan.kind == 1)) return hipErrorInvalidConfiguration;
 #define AQ_REC(CBT)                                                                                             \
-    if (plan.kind == 1)                                                                                        \
-        operand_records_kernel<CBT, CodeT, true><<<grid, block, 0, st>>>(w.codebooks, codes, r, plan.nchunk,   \
-                                                                          geo.C_out, geo.G, geo.M, geo.B);     \
+    if (plan.kind == 1 && geo.g == 9)                                                                          \
+        operand_records_kernel<CBT, CodeT, true, 9><<<grid, block, 0, st>>>(w.codebooks, codes, r, plan.nchunk, \
+                                                                             geo.C_out, geo.G, geo.M, geo.B);   \
+    else if (plan.kind == 1)                                                                                   \
+        operand_records_kernel<CBT, CodeT, true, 8><<<grid, block, 0, st>>>(w.codebooks, codes, r, plan.nchunk, \
+                                                                             geo.C_out, geo.G, geo.M, geo.B);   \
     else                                                                                                       \
-        operand_records_kernel<CBT, CodeT, false><<<grid, block, 0, st>>>(w.codebooks, codes, r, plan.nchunk,  \
-                                                                           geo.C_out, geo.G, geo.M, geo.B);
+        operand_records_kernel<CBT, CodeT, false, 8><<<grid, block, 0, st>>>(w.codebooks, codes, r,            \
+                                                                              plan.nchunk, geo.C_out, geo.G,   \
+                                                                              geo.M, geo.B);
     switch (w.cb_dtype) {
     case AQ_F32: AQ_REC(AQ_F32) break;
     case AQ_F16: AQ_REC(AQ_F16) break;

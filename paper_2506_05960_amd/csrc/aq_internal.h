@@ -56,6 +56,7 @@ struct FusedPlan {
     int dec;              // FusedDec
     int mc;               // M
     int cb_bytes;         // LDS codebook bytes (0 when read from global memory)
+    int rec_only;         // no in-loop decode for this format: always the pre-decoded mode
     // chosen per forward
     int bm, bn, upl;      // tile and staging units per lane
     int units;            // staging units per chunk

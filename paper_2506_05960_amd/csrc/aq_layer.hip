@@ -176,8 +176,9 @@ bool lut_plan_create(const aq_layer_desc& d, int g, int M, int G, LutPlan* p) {
 
 bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPlan* p) {
     std::memset(p, 0, sizeof(*p));
-    if (d.tile_dtype != AQ_F16 || g != 8) return false;
+    if (d.tile_dtype != AQ_F16 || (g != 8 && g != 9)) return false;
     const bool conv = is_conv(d);
+    if (g == 9 && !(conv && d.conv_kh == 3 && d.conv_kw == 3)) return false;   // g = 9: one 3x3 filter per group
     if (conv) {
         if (d.x_dtype != AQ_F16 || d.in_w % 2 != 0) return false;
         if (d.conv_kh == 3 && d.conv_kw == 3 && d.conv_cin % 16 == 0) {
@@ -197,14 +198,18 @@ bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPla
         p->cm = 4;
         p->nchunk = (d.in_features + 63) / 64;
     }
-    if ((M == 2 || M == 4) && B <= 8 && d.codebook_dtype == AQ_F16) {
+    if (g == 8 && (M == 2 || M == 4) && B <= 8 && d.codebook_dtype == AQ_F16) {
         p->dec = aq::FUSED_DEC_PK16;
         p->cb_bytes = M * 256 * 16;             // LDS keeps 256 rows per codebook
-    } else if (M == 1 && B > 8) {
+    } else if (g == 8 && M == 1 && B > 8 && d.codebook_dtype == AQ_F16) {
         p->dec = aq::FUSED_DEC_T16G;
         p->cb_bytes = 0;
     } else {
-        return false;
+        // any other codebook count, size or dtype, and g = 9: operands decoded
+        // once per forward by the records kernel
+        p->dec = aq::FUSED_DEC_REC;
+        p->cb_bytes = 0;
+        p->rec_only = 1;
     }
     p->mc = M;
     const int ns = p->kind == 1 ? 9 : p->cm;
@@ -362,6 +367,7 @@ bool gemm_plan_tile(const Geom& geo, aq::FusedPlan* p) {
 // repeat for every token tile) once there are enough token tiles to repay the
 // extra pass.  AQ_FUSED_REC=1 / 0 forces it on / off.
 bool use_predecoded(const aq_layer* L, const Geom& geo) {
+    if (L->fplan.rec_only) return true;
     if (const char* s = std::getenv("AQ_FUSED_REC")) return std::atoi(s) != 0;
     const int64_t token_tiles = (geo.tokens + 63) / 64;
     const aq::FusedPlan& p = L->fplan;
@@ -406,9 +412,12 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
             if (c[i] >= nk) return fail(AQ_ERR_INVALID_ARGUMENT, "code value >= 2^B at index " + std::to_string(i));
     }
     const bool lut_ok = B <= 8;
-    const bool dec_ok = desc->tile_dtype == AQ_F32 || g == 8;
+    aq::FusedPlan fplan;
+    const bool fused_ok = fused_plan_create(*desc, g, M, B, &fplan);
+    const bool dec_ok = desc->tile_dtype == AQ_F32 || g == 8 || fused_ok;
     if (!lut_ok && !dec_ok)
-        return fail(AQ_ERR_UNSUPPORTED, "no kernel for this format: LUT needs B <= 8, fp16/bf16 decode needs g == 8");
+        return fail(AQ_ERR_UNSUPPORTED, "no kernel for this format: LUT needs B <= 8; the fp16/bf16 decode needs "
+                                        "g == 8, or g == 9 on an fp16 3x3 convolution with C_in % 16 == 0");
 
     int ndev = 0;
     hipError_t e = hipGetDeviceCount(&ndev);
@@ -471,10 +480,13 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
         AQ_TRY(dev_upload(&L->d_ws, nullptr, (size_t)p.nchunk * p.tok_block * C_out * sizeof(float), "workspace"));
     }
 
-    L->fused_ok = fused_plan_create(*desc, g, M, B, &L->fplan);
+    L->fused_ok = fused_ok;
+    L->fplan = fplan;
     if (L->fused_ok) {
-        std::vector<uint8_t> rec = fused_records(L->fplan, codes, C_out, G, M, B);
-        AQ_TRY(dev_upload(&L->d_crec, rec.data(), rec.size(), "fused code records"));
+        if (!fplan.rec_only) {
+            std::vector<uint8_t> rec = fused_records(L->fplan, codes, C_out, G, M, B);
+            AQ_TRY(dev_upload(&L->d_crec, rec.data(), rec.size(), "fused code records"));
+        }
         const Geom g1 = make_geom(L, 1);
         AQ_TRY(dev_upload(&L->d_wrec, nullptr, aq::operand_record_bytes(g1, L->fplan), "operand records"));
     }
@@ -547,8 +559,11 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
             }
             const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
             if (e == hipSuccess) e = aq::launch_fused_forward(geo, fp, fl);
-        } else {
+        } else if (geo.g == 8) {
             e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
+        } else {
+            return fail(AQ_ERR_UNSUPPORTED, "g = 9 layers run on the fused kernel only (it was disabled or its "
+                                            "tiles do not fit this shape)");
         }
     }
     if (e != hipSuccess) return hip_fail(e, "forward launch");
@@ -571,7 +586,7 @@ aq_status aq_layer_set_path(aq_layer* L, aq_path path) {
         return fail(AQ_ERR_INVALID_ARGUMENT, "bad path");
     if (path == AQ_PATH_LUT && !L->lut_ok) return fail(AQ_ERR_UNSUPPORTED, "LUT path needs B <= 8");
     if (path == AQ_PATH_DECODE && !L->dec_ok)
-        return fail(AQ_ERR_UNSUPPORTED, "fp16/bf16 decode path needs g == 8");
+        return fail(AQ_ERR_UNSUPPORTED, "fp16/bf16 decode path needs g == 8 (or g == 9 on a 3x3 convolution)");
     L->path = path;
     return AQ_OK;
 }

@@ -77,6 +77,7 @@ DECODE_CASES = [
     LayerSpec(name="bf16tile", C_out=40, K=64, g=8, M=3, B=7, n=4, codebook_dtype="bf16", tile_dtype="bf16"),
     LayerSpec(name="g9", C_out=17, K=27, g=9, M=2, B=5, n=4, tile_dtype="f32", codebook_dtype="f32"),
     LayerSpec(name="b12", C_out=33, K=48, g=8, M=2, B=12, n=4),
+    LayerSpec(name="kaq_g9", C_out=24, K=32 * 9, g=9, M=2, B=8, n=1, conv=ConvGeom(32, 3, 3, 1, 1, 6, 6)),
 ]
 
 
@@ -300,6 +301,64 @@ def test_dense_product_over_records(spec, tile, monkeypatch):
     y = _run(spec, inp, "decode")
     err = O.rel_err_inf(y, O.forward(spec, inp))
     _say(f"gemm {spec.name} {tile} err={err:.3e}")
+    assert err <= 2e-3
+
+
+# ---------------------------------------------------------------------------
+# kernel-aware 3x3 format (g = 9, one group per input channel's filter) and
+# the formats without an in-loop decode, all through the pre-decoded operands
+# (output widths that tile the token dimension: the fused kernel's constraint)
+# ---------------------------------------------------------------------------
+
+KAQ = [
+    LayerSpec(name="kaq_m2", C_out=96, K=32 * 9, g=9, M=2, B=8, n=2, conv=ConvGeom(32, 3, 3, 1, 1, 16, 16)),
+    LayerSpec(name="kaq_m1_b12", C_out=70, K=48 * 9, g=9, M=1, B=12, n=3, conv=ConvGeom(48, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="kaq_m4_s2", C_out=130, K=16 * 9, g=9, M=4, B=8, n=2, conv=ConvGeom(16, 3, 3, 2, 1, 20, 16)),
+    LayerSpec(name="kaq_f32cb", C_out=64, K=64 * 9, g=9, M=2, B=6, n=1, codebook_dtype="f32",
+              conv=ConvGeom(64, 3, 3, 1, 1, 12, 8)),
+    LayerSpec(name="kaq_bf16cb", C_out=40, K=16 * 9, g=9, M=3, B=7, n=4, codebook_dtype="bf16",
+              conv=ConvGeom(16, 3, 3, 1, 1, 9, 16)),
+    LayerSpec(name="rec_m3_lin", C_out=100, K=136, g=8, M=3, B=8, n=200),
+    LayerSpec(name="rec_m8_conv", C_out=72, K=32 * 9, g=8, M=8, B=5, n=2, conv=ConvGeom(32, 3, 3, 1, 1, 10, 16)),
+    LayerSpec(name="rec_f32cb_conv1", C_out=40, K=64, g=8, M=2, B=8, n=2, codebook_dtype="f32",
+              conv=ConvGeom(64, 1, 1, 1, 0, 8, 8)),
+]
+
+
+@pytest.mark.parametrize("spec", KAQ, ids=lambda s: s.name)
+def test_predecoded_formats(spec):
+    inp = generate(spec, 909)
+    _say(f"kaq/rec {spec.name}")
+    y = _run(spec, inp, "decode")
+    err = O.rel_err_inf(y, O.forward(spec, inp))
+    _say(f"  rel_err_inf={err:.3e}")
+    assert err <= 2e-3
+
+
+def test_kaq_codebook_doubling_is_exact():
+    """g = 9: codebook values on a 2^-10 grid make every decode exact, so Y(2C) == 2 Y(C) bitwise."""
+    spec = LayerSpec(name="kaq_alpha", C_out=48, K=32 * 9, g=9, M=2, B=8, n=2, y_dtype="f32",
+                     conv=ConvGeom(32, 3, 3, 1, 1, 8, 8))
+    inp = generate(spec, 5)
+    rng = np.random.default_rng(6)
+    inp["codebooks"] = (rng.integers(-512, 512, size=inp["codebooks"].shape) / 1024.0).astype(np.float16)
+    y1 = _run(spec, inp, "decode")
+    inp2 = dict(inp)
+    inp2["codebooks"] = (inp["codebooks"].astype(np.float32) * 2).astype(np.float16)
+    y2 = _run(spec, inp2, "decode")
+    assert np.array_equal(y2, 2.0 * y1)
+
+
+def test_kaq_large_k_few_tokens_takes_the_table_path():
+    import paper_2506_05960_amd as P
+    spec = LayerSpec(name="kaq_lut", C_out=32, K=512 * 9, g=9, M=2, B=8, n=1, conv=ConvGeom(512, 3, 3, 1, 1, 1, 2))
+    inp = generate(spec, 3)
+    layer = P.AQLayer(spec, inp)
+    assert layer.choose_path(spec.tokens) == "lut"
+    layer.close()
+    y = _run(spec, inp, "auto")
+    err = O.rel_err_inf(y, O.forward(spec, inp))
+    _say(f"kaq lut err={err:.3e}")
     assert err <= 2e-3
 
 
