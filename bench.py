@@ -150,13 +150,14 @@ def sweep_bench(a, torch, P, W):
     this measurement).
     """
     layers = W.sweep_layers(full=a.full)
-    M = {"W2": 2, "W4": 4}[a.variant]
+    M = {"W2": 2, "W4": 4, "W2K": 2, "W4K": 4}[a.variant]
+    kaq = a.variant.endswith("K")       # 3x3 convolutions in the kernel-aware format (g = 9)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(W.SEED_BASE + 4)
     rows, calls, total_flops, total_bytes = [], [], 0, 0
     objs = []
     for i, lay in enumerate(layers):
-        spec = W.sweep_spec(lay, M, batch=8)
+        spec = W.sweep_spec(lay, M, batch=8, g=9 if kaq and lay.kind == "conv3x3" else 8)
         wts = W.generate(spec.with_n(1), W.SEED_BASE + 100 + i)       # weights are drawn before activations
         layer = P.AQLayer(spec, wts, max_tokens=spec.tokens)
         xshape = (spec.n, spec.K) if spec.conv is None else (spec.n, spec.conv.cin, spec.conv.H, spec.conv.W)
@@ -175,7 +176,8 @@ def sweep_bench(a, torch, P, W):
     per_layer_sum = sum(r[6] for r in rows)
     if a.table:
         with open(a.table, "w") as f:
-            f.write(f"# U-Net layer sweep, batch 8, {a.variant} (g=8, M={M}, B=8), fp16\n\n")
+            fmt = "g=9 for 3x3 convolutions, g=8 elsewhere" if kaq else "g=8"
+            f.write(f"# U-Net layer sweep, batch 8, {a.variant} ({fmt}, M={M}, B=8), fp16\n\n")
             f.write(f"Command: `python bench.py --config sweep --variant {a.variant}"
                     f"{' --full' if a.full else ''} --table <this file>`\n\n")
             f.write(f"{len(rows)} layers, {total_flops / 1e9:.1f} dense-equivalent GFLOP.  Whole pass in one HIP "
@@ -281,7 +283,8 @@ def main(argv=None):
     ap.add_argument("--no-graph", action="store_true", help="launch every step from Python instead of a HIP graph")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run one plain device copy of this many bytes (counter calibration)")
-    ap.add_argument("--variant", default="W2", choices=["W2", "W4"], help="sweep: 2 or 4 bits per weight")
+    ap.add_argument("--variant", default="W2", choices=["W2", "W4", "W2K", "W4K"],
+                    help="sweep: M = 2 or 4 codebooks of 256 (K: 3x3 convolutions with g = 9, one group per filter)")
     ap.add_argument("--full", action="store_true", help="sweep: every linear of the transformer blocks")
     ap.add_argument("--table", default="", help="sweep: write the per-layer table (markdown) here")
     a = ap.parse_args(argv)
