@@ -57,6 +57,7 @@ struct FusedPlan {
     int mc;               // M
     int cb_bytes;         // LDS codebook bytes (0 when read from global memory)
     int rec_only;         // no in-loop decode for this format: always the pre-decoded mode
+    int nmajor;           // workgroup order: channel tile slowest (else token tile slowest)
     // chosen per forward
     int bm, bn, upl;      // tile and staging units per lane
     int units;            // staging units per chunk

@@ -259,7 +259,15 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
     double best = 0;
     aq::FusedPlan bestp{};
     bool found = false;
-    for (int i = 0; i < ncand; ++i) {
+    // Output rows shorter than 16 tokens put two rows in one 16-lane group of an
+    // A-fragment read; a staged row widened until consecutive rows start OW
+    // 16-byte slots apart (mod 64 banks) makes those reads conflict free.  Each
+    // tile is tried widened and, at a cost penalty, as is.
+    const bool narrow = p->kind != 0 && geo.OW < 16 && geo.stride == 1;
+    for (int ci = 0; ci < 2 * ncand; ++ci) {
+        const int i = ci % ncand;
+        const bool widen = ci < ncand;
+        if (widen && !narrow) continue;
         const TileCand& t = cands[i];
         if (want_bm && (t.bm != want_bm || t.bn != want_bn)) continue;
         aq::FusedPlan q = *p;
@@ -272,6 +280,8 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
             const int kh = p->kind == 1 ? 3 : 1;
             q.pr = tr * kh;
             q.pw = geo.W + 2 * geo.pad;
+            if (widen)
+                while ((kh * q.pw - geo.OW) % 16 != 0) ++q.pw;
             q.ps = q.pr * q.pw * 16;                    // one plane of 8 channels
             q.units = 2 * p->cm * q.pr * (geo.W / 2);   // (plane, row, pixel pair)
             q.total_rows = (int)(geo.tokens / geo.OW);
@@ -295,6 +305,7 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
         if (p->kind == 0) cost *= t.upl / (t.upl + 2.0);
         // pre-decoded operands of a linear layer: the 64 x 64 tile measured best
         if (p->kind == 0 && p->dec == aq::FUSED_DEC_REC && !(t.bm == 64 && t.bn == 64)) cost *= 1.25;
+        if (narrow && !widen) cost *= 1.15;             // bank conflicts on the A-fragment reads (measured)
         if (!found || cost < best) {
             best = cost;
             bestp = q;
@@ -542,6 +553,12 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
         const char* ge = std::getenv("AQ_GEMM");
         const bool gemm = L->fused_ok && fits31 && fp.dec == aq::FUSED_DEC_REC && ge && std::atoi(ge) != 0 &&
                           gemm_plan_tile(geo, &gp);
+        auto order = [](aq::FusedPlan& q) {
+            q.nmajor = q.dec == aq::FUSED_DEC_REC;
+            if (const char* s = std::getenv("AQ_TILE_ORDER")) q.nmajor = s[0] == 'n';
+        };
+        order(fp);
+        order(gp);
         if (gemm) {
             e = aq::launch_operand_records(geo, gp, w, L->d_wrec, st);
             const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(L->d_wrec), L->d_scales, X, xs, Y,

@@ -46,9 +46,17 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
         const int xcd = h & 7, j = h >> 3;
         const int per = nwg >> 3, rem = nwg & 7;
         const int L = xcd * per + min(xcd, rem) + j;
-        const int ntn = (geo.C_out + BN - 1) / BN;
-        tile_m = L / ntn;
-        tile_n = L - tile_m * ntn;
+        if (plan.nmajor) {
+            // channel tile slowest: an XCD's range covers few channel tiles, so the
+            // weight operands it streams stay in its L2
+            const int ntm = (int)((geo.tokens + BM - 1) / BM);
+            tile_n = L / ntm;
+            tile_m = L - tile_n * ntm;
+        } else {
+            const int ntn = (geo.C_out + BN - 1) / BN;
+            tile_m = L / ntn;
+            tile_n = L - tile_m * ntn;
+        }
     }
     const int T0 = tile_m * BM;
     const int N0 = tile_n * BN;
