@@ -357,7 +357,9 @@ bool gemm_plan_tile(const Geom& geo, aq::FusedPlan* p) {
         }
         if (q.units > max_units) continue;
         q.pbuf_bytes = 2 * p->cm * q.ps + 32;
-        q.lds_bytes = (size_t)2 * (q.pbuf_bytes + (size_t)ns * t.bn * 32);
+        const size_t rows = p->kind != 0 ? t.bn : t.bm, cols = p->kind != 0 ? t.bm : t.bn;
+        const size_t red = (rows / 4) * (cols + 1) * 16;                   // the epilogue's tile
+        q.lds_bytes = std::max<size_t>((size_t)2 * (q.pbuf_bytes + (size_t)ns * t.bn * 32), red);
         if (q.lds_bytes > kLdsBytes) continue;
         const int64_t nwg = ((geo.tokens + t.bm - 1) / t.bm) * (int64_t)((geo.C_out + t.bn - 1) / t.bn);
         const int64_t rounds = (nwg + 255) / 256;

@@ -14,7 +14,8 @@
 //    16 consecutive records) are staged in LDS by the whole workgroup, double
 //    buffered with one barrier per chunk, and every wave reads its A and B
 //    fragments from there.
-//  * No partial tiles to combine: each wave scales and stores its own quarter.
+//  * No partial tiles to combine; the tile passes through LDS once so that
+//    the stores are 16-byte row segments.
 #include "aq_fused_kernel.h"
 
 namespace aq {
@@ -141,12 +142,33 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
     const __amdgpu_buffer_rsrc_t wr = buffer_rsrc(recs, (uint64_t)plan.nchunk * NS * geo.C_out * 32u);
     struct Regs {
         uint32_t stage[UPL][SREG];
-        u32x4 wreg[BPT];
     };
-    Regs ra;                                         // the next chunk, in flight
+    Regs ra;                                         // the next chunk's activations, in flight
+    // weight records go straight from global memory into the stage's LDS area
+    // (direct-to-LDS loads: lane l of a wave fills slot base + l); every wave
+    // issues whole 64-record runs, so the stage's run count is wave-uniform
+    auto issue_weights = [&](int chunk, uint8_t* stg) {
+        uint8_t* wdst = stg + abytes;
+#pragma unroll
+        for (int i = 0; i < BPT; ++i) {
+            const int run0 = 256 * i + 64 * wave;    // first slot of this wave's run
+            if (run0 < BREC) {
+                // LDS slot e = (s * 2 + h) * BN + n holds record (chunk, s, N0 + n, h); channels
+                // past C_out read a valid record whose products are never stored
+                const int e = run0 + lane;
+                const int sh = e / BN;
+                const int n = e - sh * BN;
+                const int st = sh >> 1, h = sh & 1;
+                const int nc = min(N0 + n, geo.C_out - 1);
+                const uint8_t* src = recs + ((size_t)((chunk * NS + st) * geo.C_out + nc) * 2 + h) * 16;
+                __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                                 (__attribute__((address_space(3))) void*)(wdst + (size_t)run0 * 16),
+                                                 16, 0, 0);
+            }
+        }
+    };
     auto load_chunk = [&](int chunk, Regs& rg) {
         auto& stage = rg.stage;
-        auto& wreg = rg.wreg;
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
             if constexpr (CONV) {
@@ -168,23 +190,9 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
                 }
             }
         }
-        // weight records of this chunk: step s, channel N0 + n, half h -> record e = (s * BN + n) * 2 + h
-#pragma unroll
-        for (int i = 0; i < BPT; ++i) {
-            // LDS slot e = (s * 2 + h) * BN + n holds record (chunk, s, N0 + n, h)
-            const int e = tid + 256 * i;
-            const int sh = e / BN;
-            const int n = e - sh * BN;
-            const int st = sh >> 1, h = sh & 1;
-            const bool ok = e < BREC && N0 + n < geo.C_out;
-            const uint32_t off =
-                ok ? (((uint32_t)((chunk * NS + st) * geo.C_out + N0 + n)) * 2u + (uint32_t)h) * 16u : kOutOfRange;
-            wreg[i] = __builtin_amdgcn_raw_buffer_load_b128(wr, off, 0, 0);
-        }
     };
     auto store_chunk = [&](uint8_t* stg, const Regs& rg) {
         const auto& stage = rg.stage;
-        const auto& wreg = rg.wreg;
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
             uint8_t* dst = stg + l_off[j];
@@ -203,12 +211,6 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
                 else v = u32x4{stage[j][0], stage[j][1], stage[j][2], stage[j][3]};
                 *reinterpret_cast<u32x4*>(dst) = v;
             }
-        }
-        u32x4* wdst = reinterpret_cast<u32x4*>(stg + abytes);
-#pragma unroll
-        for (int i = 0; i < BPT; ++i) {
-            const int e = tid + 256 * i;
-            if (BREC % 256 == 0 || e < BREC) wdst[e] = wreg[i];
         }
     };
 
@@ -254,54 +256,132 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
     // chunk c is computed from stage c % 2 while chunk c + 1 is fetched into registers
     const int nch = plan.nchunk;
     if (nch > 0) {
+        issue_weights(0, st0);
         load_chunk(0, ra);
         store_chunk(st0, ra);
     }
+    __builtin_amdgcn_s_waitcnt(0);                   // the direct-to-LDS loads have landed
     __syncthreads();
     for (int chunk = 0; chunk < nch; ++chunk) {
         uint8_t* cur = (chunk & 1) ? st1 : st0;
         uint8_t* nxt = (chunk & 1) ? st0 : st1;
         const bool more = chunk + 1 < nch;
-        if (more) load_chunk(chunk + 1, ra);
+        if (more) {
+            load_chunk(chunk + 1, ra);
+            issue_weights(chunk + 1, nxt);
+        }
         compute(cur);
         if (more) store_chunk(nxt, ra);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
 
-    // ---- epilogue: each wave scales and stores its quarter ----
-    const int ybytes = y_dtype == AQ_F32 ? 4 : 2;
-    const __amdgpu_buffer_rsrc_t yr = buffer_rsrc(Y, (uint64_t)geo.tokens * geo.C_out * ybytes);
-    const int plane = CONV ? geo.OH * geo.OW : 0;
+    // ---- epilogue: the tile meets in LDS (rows interleaved by 4 so that each
+    // lane writes float4s, plus one padding float4 per row quad), then every
+    // thread scales, converts and writes 4 rows x 8 columns as 16-byte segments.
+    // Rows are output channels (convolution) or tokens (linear).
+    constexpr int ROWS = CONV ? BN : BM, COLS = CONV ? BM : BN;
+    constexpr int COLSP = COLS + 1;
+    floatx4* red = reinterpret_cast<floatx4*>(lds);   // the stages are free after the last barrier
 #pragma unroll
     for (int a = 0; a < AM; ++a)
 #pragma unroll
         for (int b = 0; b < AN; ++b)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i) {
+                const int row0 = (CONV ? WN * wn + 32 * b : WM * wm + 32 * a) + 8 * i + 4 * q;
+                const int col = (CONV ? WM * wm + 32 * a : WN * wn + 32 * b) + l32;
+                red[(row0 / 4) * COLSP + col] =
+                    floatx4{acc[a][b][4 * i], acc[a][b][4 * i + 1], acc[a][b][4 * i + 2], acc[a][b][4 * i + 3]};
+            }
+    __syncthreads();
+    const int ybytes = y_dtype == AQ_F32 ? 4 : 2;
+    const __amdgpu_buffer_rsrc_t yr = buffer_rsrc(Y, (uint64_t)geo.tokens * geo.C_out * ybytes);
+    const int plane = CONV ? geo.OH * geo.OW : 0;
+    constexpr int TASKS = (ROWS / 4) * (COLS / 8);
+    for (int task = tid; task < TASKS; task += 256) {
+        const int c8 = (task / (ROWS / 4)) * 8;
+        const int rq = task - (task / (ROWS / 4)) * (ROWS / 4);
+        floatx4 v[8];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int rowi = 8 * i + 4 * q + e;   // MFMA row within the 32 x 32 block
-                    int tok, co;
-                    if constexpr (CONV) {
-                        co = N0 + WN * wn + 32 * b + rowi;
-                        tok = T0 + WM * wm + 32 * a + l32;
-                    } else {
-                        tok = T0 + WM * wm + 32 * a + rowi;
-                        co = N0 + WN * wn + 32 * b + l32;
-                    }
-                    if (tok >= tokens || co >= geo.C_out) continue;
-                    float v = acc[a][b][4 * i + e] * scales[co];
-                    if (!CONV && x_scales) v *= x_scales[tok];
+        for (int c = 0; c < 8; ++c) v[c] = red[rq * COLSP + c8 + c];
+        int col0, ncols, rows_left;
+        bool aligned;
+        if constexpr (CONV) {
+            col0 = T0 + c8;
+            ncols = min(8, tokens - col0);
+            rows_left = geo.C_out - (N0 + 4 * rq);
+            aligned = plane % 8 == 0;
+        } else {
+            col0 = N0 + c8;
+            ncols = min(8, geo.C_out - col0);
+            rows_left = tokens - (T0 + 4 * rq);
+            aligned = geo.C_out % 8 == 0;
+        }
+        if (ncols <= 0 || rows_left <= 0) continue;
+        // row scales (channel for a convolution, token for a linear layer) and column scales
+        float rs[4], cs[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if constexpr (CONV) {
+                const int co = min(N0 + 4 * rq + e, geo.C_out - 1);
+                rs[e] = scales[co];
+            } else {
+                const int tok = min(T0 + 4 * rq + e, tokens - 1);
+                rs[e] = x_scales ? x_scales[tok] : 1.0f;
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+            if constexpr (CONV) cs[c] = 1.0f;
+            else cs[c] = scales[min(col0 + c, geo.C_out - 1)];
+        }
+        if (ncols == 8 && aligned) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (e >= rows_left) break;
+                int yi0;
+                if constexpr (CONV) {
+                    const int co = N0 + 4 * rq + e;
+                    const int bimg = col0 / plane;
+                    yi0 = (bimg * geo.C_out + co) * plane + (col0 - bimg * plane);
+                } else {
+                    yi0 = (T0 + 4 * rq + e) * geo.C_out + col0;
+                }
+                float o[8];
+#pragma unroll
+                for (int c = 0; c < 8; ++c) o[c] = v[c][e] * cs[c] * rs[e];
+                if (y_dtype == AQ_F32) {
+                    __builtin_amdgcn_raw_buffer_store_b128(
+                        u32x4{__float_as_uint(o[0]), __float_as_uint(o[1]), __float_as_uint(o[2]), __float_as_uint(o[3])},
+                        yr, yi0 * 4, 0, 0);
+                    __builtin_amdgcn_raw_buffer_store_b128(
+                        u32x4{__float_as_uint(o[4]), __float_as_uint(o[5]), __float_as_uint(o[6]), __float_as_uint(o[7])},
+                        yr, yi0 * 4 + 16, 0, 0);
+                } else {
+                    u32x4 h;
+#pragma unroll
+                    for (int d = 0; d < 4; ++d)
+                        h[d] = (uint32_t)f32_to_f16(o[2 * d]) | ((uint32_t)f32_to_f16(o[2 * d + 1]) << 16);
+                    __builtin_amdgcn_raw_buffer_store_b128(h, yr, yi0 * 2, 0, 0);
+                }
+            }
+        } else {
+            for (int e = 0; e < 4 && e < rows_left; ++e)
+                for (int c = 0; c < ncols; ++c) {
                     int yi;
                     if constexpr (CONV) {
-                        const int bimg = tok / plane;
-                        yi = (bimg * geo.C_out + co) * plane + (tok - bimg * plane);
+                        const int tk = col0 + c, bb = tk / plane;
+                        yi = (bb * geo.C_out + N0 + 4 * rq + e) * plane + (tk - bb * plane);
                     } else {
-                        yi = tok * geo.C_out + co;
+                        yi = (T0 + 4 * rq + e) * geo.C_out + col0 + c;
                     }
-                    if (y_dtype == AQ_F32) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), yr, yi * 4, 0, 0);
-                    else __builtin_amdgcn_raw_buffer_store_b16(f32_to_f16(v), yr, yi * 2, 0, 0);
+                    const float o = v[c][e] * cs[c] * rs[e];
+                    if (y_dtype == AQ_F32) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o), yr, yi * 4, 0, 0);
+                    else __builtin_amdgcn_raw_buffer_store_b16(f32_to_f16(o), yr, yi * 2, 0, 0);
                 }
+        }
+    }
 }
 
 template <int KIND, int XT, int BM, int BN>
