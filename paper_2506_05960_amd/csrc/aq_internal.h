@@ -80,8 +80,13 @@ struct FusedLaunch {
 };
 
 hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
-// Dense matrix-core product over pre-decoded operand records (fl.crec), tile plan.bm x plan.bn.
-hipError_t launch_rec_gemm(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+// Dense matrix-core product over pre-decoded operand records (fl.crec), tile plan.bm x plan.bn;
+// for a convolution plan.pr / plan.ps / plan.pw are the staging's image slots, rows per
+// slot and padded row width.  `xpack` receives the repacked activations (convolution, int8
+// input), `zero` points at 16 zero bytes.
+hipError_t launch_rec_gemm(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl, void* xpack,
+                           const void* zero);
+size_t rec_gemm_lds_bytes(int kind, int bm, int bn);
 
 // Operand records of the pre-decoded mode: record (chunk, step, channel, lane
 // half) = the 8 fp16 weights of that matrix-core B operand, unscaled.

@@ -29,6 +29,8 @@ struct aq_layer {
     aq::FusedPlan fplan;
     uint8_t* d_crec;          // fused-path code records (null when the fused path does not apply)
     void* d_wrec;             // fused-path operand records, decoded per forward in the pre-decoded mode
+    void* d_xpack;            // dense product: activations repacked per forward
+    void* d_zero;             // 256 zero bytes
     bool lut_ok, dec_ok, fused_ok;
     aq_path path;
     int64_t lut_max_tokens;
@@ -125,8 +127,8 @@ aq_path choose(const aq_layer* L, int64_t tokens) {
 
 void free_layer(aq_layer* L) {
     if (!L) return;
-    void* ptrs[] = {L->d_cb,        L->d_cb32,   L->d_cbtile, L->d_codes, L->d_codes_lut,
-                    L->d_scales,    L->d_ws,     L->d_crec,   L->d_wrec};
+    void* ptrs[] = {L->d_cb,     L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales,
+                    L->d_ws,     L->d_crec, L->d_wrec,   L->d_xpack, L->d_zero};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete L;
@@ -323,7 +325,6 @@ bool gemm_plan_tile(const Geom& geo, aq::FusedPlan* p) {
     static const TileCand cands[] = {{128, 128, 0}, {128, 64, 0}, {64, 128, 0}};
     int want_bm = 0, want_bn = 0;
     if (const char* s = std::getenv("AQ_GEMM_TILE")) std::sscanf(s, "%dx%d", &want_bm, &want_bn);
-    const int ns = p->kind == 1 ? 9 : p->cm;
     double best = 0;
     aq::FusedPlan bestp{};
     bool found = false;
@@ -332,34 +333,34 @@ bool gemm_plan_tile(const Geom& geo, aq::FusedPlan* p) {
         aq::FusedPlan q = *p;
         q.bm = t.bm;
         q.bn = t.bn;
-        int max_units;
         if (p->kind != 0) {
             if (!(t.bm % geo.OW == 0 || geo.OW % t.bm == 0)) continue;
-            const int tr = t.bm >= geo.OW ? t.bm / geo.OW : 1;
             const int kh = p->kind == 1 ? 3 : 1;
-            q.pr = tr * kh;
-            q.pw = geo.W + 2 * geo.pad;
-            // A fragment reads: 16 consecutive lanes are consecutive tokens; when an
-            // output row is shorter than 16 they span rows, so widen the staged row
-            // until consecutive rows start OW 16-byte slots apart modulo the 64 banks
-            if (geo.OW < 16 && geo.stride == 1)
-                while ((kh * q.pw - geo.OW) % 16 != 0) ++q.pw;
-            q.ps = q.pr * q.pw * 16;
-            q.units = 2 * p->cm * q.pr * (geo.W / 2);
-            q.total_rows = (int)(geo.tokens / geo.OW);
-            max_units = 256 * 3;
-        } else {
-            q.pr = q.pw = 0;
-            q.ps = t.bm * 16 + 16;
-            q.units = t.bm * 2 * p->cm;
-            q.total_rows = 0;
-            max_units = 256 * 4;
+            const int tr = t.bm >= geo.OW ? t.bm / geo.OW : 1;
+            const int64_t rows_total = geo.tokens / geo.OW;
+            const int64_t ntm = (geo.tokens + t.bm - 1) / t.bm;
+            int ni = 1;                                      // most images one tile's rows span
+            for (int64_t m = 0; m < std::min<int64_t>(ntm, 4 * geo.OH + 4); ++m) {
+                const int64_t g0 = m * t.bm / geo.OW;
+                const int64_t gl = std::min<int64_t>((m * t.bm + t.bm - 1) / geo.OW, rows_total - 1);
+                ni = std::max<int>(ni, (int)(gl / geo.OH - g0 / geo.OH + 1));
+            }
+            const int rpi = (std::min(tr, geo.OH) - 1) * geo.stride + kh;
+            const int planes = p->kind == 1 ? 2 : 8;
+            // staged rows `stride` apart per output row: widen so that two rows in one
+            // 16-lane fragment read fall on different banks when an output row is short
+            int pw = geo.W + 2 * geo.pad;
+            if (geo.OW < 16) {
+                int w = pw;
+                while ((geo.stride * w - geo.OW) % 16 != 0 && w < pw + 16) ++w;
+                if ((geo.stride * w - geo.OW) % 16 == 0 && (int64_t)planes * ni * rpi * w <= 1024) pw = w;
+            }
+            if ((int64_t)planes * ni * rpi * pw > 1024) continue;
+            q.pr = ni;
+            q.ps = rpi;
+            q.pw = pw;
         }
-        if (q.units > max_units) continue;
-        q.pbuf_bytes = 2 * p->cm * q.ps + 32;
-        const size_t rows = p->kind != 0 ? t.bn : t.bm, cols = p->kind != 0 ? t.bm : t.bn;
-        const size_t red = (rows / 4) * (cols + 1) * 16;                   // the epilogue's tile
-        q.lds_bytes = std::max<size_t>((size_t)2 * (q.pbuf_bytes + (size_t)ns * t.bn * 32), red);
+        q.lds_bytes = aq::rec_gemm_lds_bytes(p->kind, t.bm, t.bn);
         if (q.lds_bytes > kLdsBytes) continue;
         const int64_t nwg = ((geo.tokens + t.bm - 1) / t.bm) * (int64_t)((geo.C_out + t.bn - 1) / t.bn);
         const int64_t rounds = (nwg + 255) / 256;
@@ -502,6 +503,21 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
         }
         const Geom g1 = make_geom(L, 1);
         AQ_TRY(dev_upload(&L->d_wrec, nullptr, aq::operand_record_bytes(g1, L->fplan), "operand records"));
+        // the dense product's repacked activations (convolution, int8 input) and a zero block
+        size_t xpack = 0;
+        if (is_conv(*desc)) {
+            const int64_t nimg_max = (desc->max_tokens + (int64_t)g1.OH * g1.OW - 1) / ((int64_t)g1.OH * g1.OW);
+            xpack = (size_t)nimg_max * desc->conv_cin * desc->in_h * desc->in_w * 2;
+        } else if (desc->x_dtype == AQ_I8) {
+            xpack = (size_t)desc->max_tokens * K * 2;
+        }
+        if (xpack) AQ_TRY(dev_upload(&L->d_xpack, nullptr, xpack, "packed activations"));
+        AQ_TRY(dev_upload(&L->d_zero, nullptr, 256, "zero block"));
+        e = hipMemset(L->d_zero, 0, 256);
+        if (e != hipSuccess) {
+            free_layer(L);
+            return hip_fail(e, "zero block");
+        }
     }
 
     e = aq::launch_codebook_prep(L->d_cb, desc->codebook_dtype, (int64_t)cb_elems, L->d_cb32, L->d_cbtile,
@@ -565,7 +581,7 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
             e = aq::launch_operand_records(geo, gp, w, L->d_wrec, st);
             const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(L->d_wrec), L->d_scales, X, xs, Y,
                                      d.y_dtype, d.x_dtype, st};
-            if (e == hipSuccess) e = aq::launch_rec_gemm(geo, gp, fl);
+            if (e == hipSuccess) e = aq::launch_rec_gemm(geo, gp, fl, L->d_xpack, L->d_zero);
         } else if (L->fused_ok && fits31 && !std::getenv("AQ_NO_FUSED") && fused_plan_tile(geo, &fp)) {
             const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
                                 : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)

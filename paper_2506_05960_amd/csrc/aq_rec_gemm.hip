@@ -7,32 +7,72 @@
 //  * A workgroup of 4 waves owns a BM (tokens) x BN (output channels) tile;
 //    the waves sit 2 x 2 on it, each accumulating a (BM/2) x (BN/2) quarter.
 //  * K is walked in the fused kernel's chunks (16 input channels x 9 kernel
-//    positions for a 3x3 convolution, 64 consecutive k otherwise).  Each chunk's
-//    activations (the input rows the tile touches, 8-channel planes of 16 B
-//    per pixel, zero padding columns) and weight records (BN channels x steps
-//    x 32 B, stored step- and lane-half-major so that 16 consecutive lanes read
-//    16 consecutive records) are staged in LDS by the whole workgroup, double
-//    buffered with one barrier per chunk, and every wave reads its A and B
-//    fragments from there.
+//    positions for a 3x3 convolution, 64 consecutive k otherwise).  Each
+//    chunk's activations and weight records reach LDS through direct-to-LDS
+//    loads (lane l of a wave fills slot base + l): no registers, no staging
+//    arithmetic.  Three LDS stages keep two chunks in flight; every thread
+//    issues the same number of loads per chunk (slots with nothing to load
+//    read a zero block), so one vmcnt wait retires exactly one chunk.
+//  * Activations come in channel-interleaved fp16: a convolution's input is
+//    repacked per forward to [n][C/8][H][W][8] (`act_pack_conv_kernel`), an
+//    int8 token matrix is widened to fp16, an fp16 one is read in place.  A
+//    convolution stages every input row its tile touches once per image
+//    (kernel rows become LDS offsets), zero outside the image.
 //  * No partial tiles to combine; the tile passes through LDS once so that
 //    the stores are 16-byte row segments.
 #include "aq_fused_kernel.h"
 
 namespace aq {
 
+struct GemmArgs {
+    const uint8_t* recs;       // operand records [chunk][step][C_out][2] x 16 B
+    const uint8_t* xa;         // activations: packed conv input / fp16 tokens [T][K]
+    const uint8_t* zero;       // 16 zero bytes
+    const float* scales;
+    const float* x_scales;
+    void* Y;
+    int y_dtype;
+    int ni, rpi, pw;           // convolution staging: image slots, rows per slot, padded row width
+    uint32_t cstride;          // bytes between consecutive chunks of activations
+};
+
+constexpr int kGemmStages = 3;
+
+__device__ __forceinline__ void lds_dma16(const uint8_t* src, uint8_t* dst_wave_base) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)dst_wave_base, 16, 0, 0);
+}
+
+// s_waitcnt with vmcnt <= n (n < 64), expcnt and lgkmcnt unrestricted (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier without the release fence of __syncthreads(): that fence
+// waits for every outstanding vector-memory operation, which would also drain
+// the direct-to-LDS prefetches of later chunks. LDS reads issued before the
+// barrier are drained here; the DMA writes are awaited by wait_vmcnt.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 template <int KIND, int XT, int BM, int BN>
 __global__ void __launch_bounds__(256, 1)
-rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, const float* __restrict__ scales,
-                const void* __restrict__ X, const float* __restrict__ x_scales, void* __restrict__ Y, int y_dtype) {
+rec_gemm_kernel(Geom geo, FusedPlan plan, GemmArgs ga) {
     constexpr bool CONV = KIND != 0;
     constexpr int KH = KIND == 1 ? 3 : 1;
-    constexpr int CM = KIND == 1 ? 1 : 4;
-    constexpr int NS = KIND == 1 ? 9 : CM;          // MFMA steps per chunk
-    constexpr int WM = BM / 2, WN = BN / 2;         // a wave's quarter
+    constexpr int NS = KIND == 1 ? 9 : 4;            // MFMA steps per chunk
+    constexpr int WM = BM / 2, WN = BN / 2;          // a wave's quarter
     constexpr int AM = WM / 32, AN = WN / 32;
-    constexpr int UPL = CONV ? 3 : 4;               // staging units per thread (the planner keeps units <= 256 UPL)
-    constexpr int BREC = NS * BN * 2;               // 16-byte weight records per chunk
-    constexpr int BPT = (BREC + 255) / 256;         // weight records per thread
+    constexpr int ACT_T = CONV ? 4 : 5;              // activation slots per thread per chunk
+    constexpr int BREC = NS * BN * 2;                // 16-byte weight records per chunk
+    constexpr int WREC_T = (BREC + 255) / 256;       // weight slots per thread per chunk
+    constexpr int ASLOTS = ACT_T * 256;
+    constexpr int STAGE = (ASLOTS + WREC_T * 256) * 16;
+    constexpr int LOADS = ACT_T + WREC_T;            // direct-to-LDS loads per thread per chunk
+    constexpr int LPS = BM + 1;                      // linear: slots per plane (one spare)
 
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     const int tid = threadIdx.x;
@@ -63,154 +103,91 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
     const int N0 = tile_n * BN;
     const int tokens = (int)geo.tokens;
 
-    // LDS: two stages, each [activation planes | weight records]
-    const int abytes = plan.pbuf_bytes;              // activation planes (+ spare slot)
-    const int stage_bytes = abytes + BREC * 16;
-    uint8_t* st0 = lds;
-    uint8_t* st1 = lds + stage_bytes;
-
-    // ---- activation staging addresses (whole workgroup) ----
-    const int HW = CONV ? geo.H * geo.W : 0;
-    uint32_t a_base[AM];
-    uint32_t g_off[UPL], l_off[UPL];
-    bool g_ok[UPL];
-    int k_first[UPL];
+    // ---- activation slots: this thread's slots z = tid + 256 j of a stage ----
+    // convolution: z = ((o * ni + i) * rpi + rr) * pw + pc  (plane o of 8 channels, image
+    // slot i, staged row rr, padded column pc); linear: z = o * (BM + 1) + tt (plane o of
+    // 8 consecutive k, token tt; tt == BM is a spare slot)
+    uint32_t aoff[ACT_T];        // byte offset of chunk 0's source
+    bool aok[ACT_T];
+    int ako[ACT_T];              // linear: first k of the slot within its chunk (bounds the last chunk)
+    int gr0 = 0, b0 = 0;
     if constexpr (CONV) {
-        const float inv_ow = 1.0f / (float)geo.OW, inv_oh = 1.0f / (float)geo.OH;
-        const float inv_pr = 1.0f / (float)plan.pr;
-        const int gr0 = fdiv(T0, geo.OW, inv_ow);
+        gr0 = T0 / geo.OW;
+        b0 = gr0 / geo.OH;
+    }
 #pragma unroll
-        for (int a = 0; a < AM; ++a) {
-            const int T = T0 + WM * wm + 32 * a + l32;
-            const int gT = fdiv(T, geo.OW, inv_ow);
-            const int r = gT - gr0;
-            const int ow = T - gT * geo.OW;
-            a_base[a] = (uint32_t)(q * plan.ps + ((r * KH) * plan.pw + ow * geo.stride) * 16);
-        }
-        const int wp = geo.W >> 1;
-        const float inv_wp = 1.0f / (float)wp;
-#pragma unroll
-        for (int j = 0; j < UPL; ++j) {
-            const int u = tid + 256 * j;
-            const int t = fdiv(u, wp, inv_wp);
-            const int pp = u - t * wp;
-            const int o = fdiv(t, plan.pr, inv_pr);
-            const int pr = t - o * plan.pr;
-            const int r = pr / KH, kh = pr - r * KH;
-            const int gr = gr0 + r;
-            const int b = fdiv(gr, geo.OH, inv_oh), oh = gr - b * geo.OH;
-            const int ih = oh * geo.stride - geo.pad + kh;
-            const bool l_ok = u < plan.units;
-            g_ok[j] = l_ok && gr < plan.total_rows && ih >= 0 && ih < geo.H;
-            g_off[j] = g_ok[j] ? (uint32_t)(__umul24(__umul24(b, geo.cin) + 8 * o, geo.H) + ih) * (uint32_t)geo.W + 2u * pp : 0u;
-            l_off[j] = l_ok ? (uint32_t)(o * plan.ps + (pr * plan.pw + 2 * pp + geo.pad) * 16) : (uint32_t)(abytes - 32);
-            k_first[j] = 0;
-        }
-        // zero the padding columns of both stages once
-        const int padc = plan.pw - geo.W;
-        const int nrow = 2 * 2 * CM * plan.pr;
-        for (int i = tid; i < nrow * padc; i += 256) {
-            const int row = i / padc, pcx = i - row * padc;
-            const int bsel = row & 1, rest = row >> 1;
-            const int o = fdiv(rest, plan.pr, inv_pr), pr = rest - o * plan.pr;
-            const int pcol = pcx < geo.pad ? pcx : geo.W + pcx;
-            uint8_t* dst = (bsel ? st1 : st0) + o * plan.ps + (pr * plan.pw + pcol) * 16;
-            *reinterpret_cast<u32x4*>(dst) = u32x4{0u, 0u, 0u, 0u};
-        }
-    } else {
-#pragma unroll
-        for (int a = 0; a < AM; ++a) a_base[a] = (uint32_t)(q * plan.ps + (WM * wm + 32 * a + l32) * 16);
-#pragma unroll
-        for (int j = 0; j < UPL; ++j) {
-            const int u = tid + 256 * j;
-            const int o = u % (2 * CM);
-            const int tt = u / (2 * CM);
+    for (int j = 0; j < ACT_T; ++j) {
+        const int z = tid + 256 * j;
+        aok[j] = false;
+        aoff[j] = 0;
+        ako[j] = 0;
+        if constexpr (CONV) {
+            const int pc = z % ga.pw;
+            const int t1 = z / ga.pw;
+            const int rr = t1 % ga.rpi;
+            const int t2 = t1 / ga.rpi;
+            const int i = t2 % ga.ni;
+            const int o = t2 / ga.ni;
+            const int b = b0 + i;
+            const int oh_first = i == 0 ? gr0 - b0 * geo.OH : 0;
+            const int ih = oh_first * geo.stride - geo.pad + rr;
+            const int iw = pc - geo.pad;
+            const int nimg = (int)(geo.tokens / ((int64_t)geo.OH * geo.OW));
+            aok[j] = o < (KIND == 1 ? 2 : 8) && b < nimg && ih >= 0 && ih < geo.H && iw >= 0 && iw < geo.W;
+            if (aok[j])
+                aoff[j] = ((((uint32_t)b * (uint32_t)(geo.cin / 8) + (uint32_t)o) * (uint32_t)geo.H + (uint32_t)ih) *
+                               (uint32_t)geo.W + (uint32_t)iw) * 16u;
+        } else {
+            const int o = z / LPS;
+            const int tt = z - o * LPS;
             const int T = T0 + tt;
-            const bool l_ok = u < plan.units;
-            g_ok[j] = l_ok && T < tokens;
-            k_first[j] = 8 * o;
-            g_off[j] = g_ok[j] ? (uint32_t)(T * geo.K + 8 * o) : 0u;
-            l_off[j] = l_ok ? (uint32_t)(o * plan.ps + tt * 16) : (uint32_t)(abytes - 32);
+            aok[j] = o < 8 && tt < BM && T < tokens;
+            ako[j] = 8 * o;
+            if (aok[j]) aoff[j] = ((uint32_t)T * (uint32_t)geo.K + 8u * (uint32_t)o) * 2u;
+        }
+    }
+    // A-fragment base of each of the wave's token blocks (plane q of the step)
+    uint32_t a_base[AM];
+#pragma unroll
+    for (int a = 0; a < AM; ++a) {
+        const int T = T0 + WM * wm + 32 * a + l32;
+        if constexpr (CONV) {
+            const int gr = T / geo.OW;
+            const int ow = T - gr * geo.OW;
+            const int b = gr / geo.OH;
+            const int oh = gr - b * geo.OH;
+            const int i = min(b - b0, ga.ni - 1);        // tokens past the end: any slot, never stored
+            const int oh_first = i == 0 ? gr0 - b0 * geo.OH : 0;
+            const int rr = min(max(oh - oh_first, 0) * geo.stride, ga.rpi - KH);
+            a_base[a] = (uint32_t)((((q * ga.ni + i) * ga.rpi + rr) * ga.pw + ow * geo.stride) * 16);
+        } else {
+            a_base[a] = (uint32_t)((q * LPS + WM * wm + 32 * a + l32) * 16);
         }
     }
 
-    constexpr int SREG = CONV ? 8 : 4;
-    constexpr int XB = XT == AQ_I8 ? 1 : 2;
-    const uint64_t xbytes = CONV ? (uint64_t)plan.total_rows / geo.OH * geo.cin * HW * 2
-                                 : (uint64_t)geo.tokens * geo.K * XB;
-    const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(X, xbytes);
-    const __amdgpu_buffer_rsrc_t wr = buffer_rsrc(recs, (uint64_t)plan.nchunk * NS * geo.C_out * 32u);
-    struct Regs {
-        uint32_t stage[UPL][SREG];
-    };
-    Regs ra;                                         // the next chunk's activations, in flight
-    // weight records go straight from global memory into the stage's LDS area
-    // (direct-to-LDS loads: lane l of a wave fills slot base + l); every wave
-    // issues whole 64-record runs, so the stage's run count is wave-uniform
-    auto issue_weights = [&](int chunk, uint8_t* stg) {
-        uint8_t* wdst = stg + abytes;
+    // ---- one chunk's direct-to-LDS loads ----
+    auto issue = [&](int chunk, uint8_t* stg) {
+        const uint32_t cshift = (uint32_t)chunk * ga.cstride;
 #pragma unroll
-        for (int i = 0; i < BPT; ++i) {
-            const int run0 = 256 * i + 64 * wave;    // first slot of this wave's run
-            if (run0 < BREC) {
-                // LDS slot e = (s * 2 + h) * BN + n holds record (chunk, s, N0 + n, h); channels
-                // past C_out read a valid record whose products are never stored
-                const int e = run0 + lane;
-                const int sh = e / BN;
-                const int n = e - sh * BN;
-                const int st = sh >> 1, h = sh & 1;
-                const int nc = min(N0 + n, geo.C_out - 1);
-                const uint8_t* src = recs + ((size_t)((chunk * NS + st) * geo.C_out + nc) * 2 + h) * 16;
-                __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                                 (__attribute__((address_space(3))) void*)(wdst + (size_t)run0 * 16),
-                                                 16, 0, 0);
-            }
+        for (int j = 0; j < ACT_T; ++j) {
+            bool ok = aok[j];
+            if constexpr (!CONV) ok = ok && 64 * chunk + ako[j] < geo.K;   // K need not be a multiple of 64
+            const uint8_t* src = ok ? ga.xa + aoff[j] + cshift : ga.zero;
+            lds_dma16(src, stg + (size_t)(256 * j + 64 * wave) * 16);
         }
-    };
-    auto load_chunk = [&](int chunk, Regs& rg) {
-        auto& stage = rg.stage;
+        uint8_t* wdst = stg + ASLOTS * 16;
 #pragma unroll
-        for (int j = 0; j < UPL; ++j) {
-            if constexpr (CONV) {
-                const uint32_t base = g_ok[j] ? (g_off[j] + (uint32_t)(chunk * 16 * CM) * HW) * 2u : kOutOfRange;
-#pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    stage[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, 0);
-            } else {
-                const int k = chunk * 16 * CM + k_first[j];
-                const bool ok = g_ok[j] && k < geo.K;
-                const uint32_t off = ok ? (g_off[j] + (uint32_t)(chunk * 16 * CM)) * XB : kOutOfRange;
-                if constexpr (XT == AQ_I8) {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 0);
-                    stage[j][0] = v[0];
-                    stage[j][1] = v[1];
-                } else {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
-                    stage[j][0] = v[0]; stage[j][1] = v[1]; stage[j][2] = v[2]; stage[j][3] = v[3];
-                }
-            }
-        }
-    };
-    auto store_chunk = [&](uint8_t* stg, const Regs& rg) {
-        const auto& stage = rg.stage;
-#pragma unroll
-        for (int j = 0; j < UPL; ++j) {
-            uint8_t* dst = stg + l_off[j];
-            if constexpr (CONV) {
-                u32x4 p0, p1;
-#pragma unroll
-                for (int d = 0; d < 4; ++d) {
-                    p0[d] = pick2(stage[j][2 * d], 0, stage[j][2 * d + 1], 0);
-                    p1[d] = pick2(stage[j][2 * d], 1, stage[j][2 * d + 1], 1);
-                }
-                reinterpret_cast<u32x4*>(dst)[0] = p0;
-                reinterpret_cast<u32x4*>(dst)[1] = p1;
-            } else {
-                u32x4 v;
-                if constexpr (XT == AQ_I8) v = i8x8_to_f16((uint64_t)stage[j][0] | ((uint64_t)stage[j][1] << 32));
-                else v = u32x4{stage[j][0], stage[j][1], stage[j][2], stage[j][3]};
-                *reinterpret_cast<u32x4*>(dst) = v;
-            }
+        for (int i = 0; i < WREC_T; ++i) {
+            // LDS slot e = (s * 2 + h) * BN + n holds record (chunk, s, N0 + n, h); channels
+            // past C_out read a valid record whose products are never stored
+            const int e = 256 * i + tid;
+            const int sh = e / BN;
+            const int n = e - sh * BN;
+            const int st = sh >> 1, h = sh & 1;
+            const int nc = min(N0 + n, geo.C_out - 1);
+            const uint8_t* src = e < BREC ? ga.recs + ((size_t)((chunk * NS + st) * geo.C_out + nc) * 2 + h) * 16
+                                          : ga.zero;
+            lds_dma16(src, wdst + (size_t)(256 * i + 64 * wave) * 16);
         }
     };
 
@@ -226,10 +203,11 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
     // records of its channel blocks; step s + 1's are read before step s's
     // MFMAs are issued, so LDS latency hides behind the matrix cores
     auto frag_load = [&](const uint8_t* cur, int s, u32x4 (&af)[AM], u32x4 (&bf)[AN]) {
-        const u32x4* wl = reinterpret_cast<const u32x4*>(cur + abytes);
+        const u32x4* wl = reinterpret_cast<const u32x4*>(cur + ASLOTS * 16);
         uint32_t soff;
-        if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
-        else soff = (uint32_t)(2 * s * plan.ps);
+        if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * ga.pw + (s % 3)) * 16);
+        else if constexpr (CONV) soff = (uint32_t)(2 * s * ga.ni * ga.rpi * ga.pw * 16);
+        else soff = (uint32_t)(2 * s * LPS * 16);
 #pragma unroll
         for (int a = 0; a < AM; ++a) af[a] = *reinterpret_cast<const u32x4*>(cur + a_base[a] + soff);
 #pragma unroll
@@ -253,29 +231,26 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
         }
     };
 
-    // chunk c is computed from stage c % 2 while chunk c + 1 is fetched into registers
+    // ---- main loop: chunk c computes from stage c % 3 while chunks c + 1 and c + 2 land ----
     const int nch = plan.nchunk;
-    if (nch > 0) {
-        issue_weights(0, st0);
-        load_chunk(0, ra);
-        store_chunk(st0, ra);
-    }
-    __builtin_amdgcn_s_waitcnt(0);                   // the direct-to-LDS loads have landed
-    __syncthreads();
+    auto stg = [&](int c) { return lds + (size_t)(c % kGemmStages) * STAGE; };
+    if (nch > 0) issue(0, stg(0));
+    if (nch > 1) issue(1, stg(1));
+    if (nch > 1) wait_vmcnt<LOADS>();                // chunk 0 landed (chunk 1 may be in flight)
+    else wait_vmcnt<0>();
+    lds_barrier();
     for (int chunk = 0; chunk < nch; ++chunk) {
-        uint8_t* cur = (chunk & 1) ? st1 : st0;
-        uint8_t* nxt = (chunk & 1) ? st0 : st1;
-        const bool more = chunk + 1 < nch;
-        if (more) {
-            load_chunk(chunk + 1, ra);
-            issue_weights(chunk + 1, nxt);
-        }
-        compute(cur);
-        if (more) store_chunk(nxt, ra);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+        if (chunk + 2 < nch) issue(chunk + 2, stg(chunk + 2));
+        compute(stg(chunk));
+        if (chunk + 2 < nch) wait_vmcnt<LOADS>();    // chunk + 1 landed
+        else wait_vmcnt<0>();
+        lds_barrier();
     }
 
+    const float* scales = ga.scales;
+    const float* x_scales = ga.x_scales;
+    void* Y = ga.Y;
+    const int y_dtype = ga.y_dtype;
     // ---- epilogue: the tile meets in LDS (rows interleaved by 4 so that each
     // lane writes float4s, plus one padding float4 per row quad), then every
     // thread scales, converts and writes 4 rows x 8 columns as 16-byte segments.
@@ -385,7 +360,7 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ recs, cons
 }
 
 template <int KIND, int XT, int BM, int BN>
-static hipError_t rec_gemm_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
+static hipError_t rec_gemm_cfg(const Geom& geo, const FusedPlan& plan, const GemmArgs& ga, hipStream_t st) {
     auto kern = rec_gemm_kernel<KIND, XT, BM, BN>;
     static size_t attr_bytes = 0;
     if (plan.lds_bytes > attr_bytes) {
@@ -395,13 +370,80 @@ static hipError_t rec_gemm_cfg(const Geom& geo, const FusedPlan& plan, const Fus
         attr_bytes = plan.lds_bytes;
     }
     const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN)));
-    kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y, fl.y_dtype);
+    kern<<<grid, 256, plan.lds_bytes, st>>>(geo, plan, ga);
     return hipGetLastError();
 }
 
-hipError_t launch_rec_gemm(const Geom& geo, const FusedPlan& p, const FusedLaunch& fl) {
+// LDS bytes of a tile: three stages (activation and weight slots) or the epilogue's tile
+size_t rec_gemm_lds_bytes(int kind, int bm, int bn) {
+    const int act_t = kind != 0 ? 4 : 5;
+    const int ns = kind == 1 ? 9 : 4;
+    const int wrec_t = (ns * bn * 2 + 255) / 256;
+    const size_t stage = (size_t)(act_t * 256 + wrec_t * 256) * 16;
+    const size_t rows = kind != 0 ? bn : bm, cols = kind != 0 ? bm : bn;
+    const size_t red = (rows / 4) * (cols + 1) * 16;
+    return std::max<size_t>(kGemmStages * stage, red);
+}
+
+// Repack an NCHW fp16 input to [n][C/8][H][W][8] (one thread per pixel and 8 channels).
+__global__ void __launch_bounds__(256)
+act_pack_conv_kernel(const uint16_t* __restrict__ x, u32x4* __restrict__ out, int nimg, int C, int H, int W) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t hw = (int64_t)H * W;
+    const int64_t total = (int64_t)nimg * (C / 8) * hw;
+    if (idx >= total) return;
+    const int64_t p = idx % hw;
+    const int64_t nc8 = idx / hw;                    // n * C/8 + cblk
+    const int64_t src0 = nc8 * 8 * hw + p;           // channel 8 cblk of image n
+    u32x4 v;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+        v[d] = (uint32_t)x[src0 + (2 * d) * hw] | ((uint32_t)x[src0 + (2 * d + 1) * hw] << 16);
+    out[idx] = v;
+}
+
+// Widen an int8 token matrix to fp16 (exact), 8 values per thread.
+__global__ void __launch_bounds__(256)
+act_widen_i8_kernel(const uint64_t* __restrict__ x, u32x4* __restrict__ out, int64_t n8) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= n8) return;
+    out[idx] = i8x8_to_f16(x[idx]);
+}
+
+hipError_t launch_rec_gemm(const Geom& geo, const FusedPlan& p, const FusedLaunch& fl, void* xpack,
+                           const void* zero) {
+    GemmArgs ga;
+    ga.recs = fl.crec;
+    ga.zero = static_cast<const uint8_t*>(zero);
+    ga.scales = fl.scales;
+    ga.x_scales = fl.x_scales;
+    ga.Y = fl.Y;
+    ga.y_dtype = fl.y_dtype;
+    ga.ni = p.pr;              // the planner keeps the staging geometry in pr / ps / pw
+    ga.rpi = p.ps;
+    ga.pw = p.pw;
+    hipStream_t st = fl.stream;
+    if (p.kind != 0) {
+        const int nimg = (int)(geo.tokens / ((int64_t)geo.OH * geo.OW));
+        const int64_t total = (int64_t)nimg * (geo.cin / 8) * geo.H * geo.W;
+        act_pack_conv_kernel<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
+            static_cast<const uint16_t*>(fl.X), static_cast<u32x4*>(xpack), nimg, geo.cin, geo.H, geo.W);
+        ga.xa = static_cast<const uint8_t*>(xpack);
+        ga.cstride = (uint32_t)((p.kind == 1 ? 2 : 8) * geo.H * geo.W * 16);   // the chunk's 8-channel planes
+    } else if (fl.x_dtype == AQ_I8) {
+        const int64_t n8 = geo.tokens * geo.K / 8;
+        act_widen_i8_kernel<<<(unsigned)((n8 + 255) / 256), 256, 0, st>>>(static_cast<const uint64_t*>(fl.X),
+                                                                           static_cast<u32x4*>(xpack), n8);
+        ga.xa = static_cast<const uint8_t*>(xpack);
+        ga.cstride = 64 * 2;
+    } else {
+        ga.xa = static_cast<const uint8_t*>(fl.X);
+        ga.cstride = 64 * 2;
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
 #define AQ_G(K, XT, TBM, TBN) \
-    if (p.bm == TBM && p.bn == TBN) return rec_gemm_cfg<K, XT, TBM, TBN>(geo, p, fl);
+    if (p.bm == TBM && p.bn == TBN) return rec_gemm_cfg<K, XT, TBM, TBN>(geo, p, ga, st);
     if (p.kind == 1) {
         AQ_G(1, AQ_F16, 128, 128)
         AQ_G(1, AQ_F16, 128, 64)
@@ -410,10 +452,6 @@ hipError_t launch_rec_gemm(const Geom& geo, const FusedPlan& p, const FusedLaunc
         AQ_G(2, AQ_F16, 128, 128)
         AQ_G(2, AQ_F16, 128, 64)
         AQ_G(2, AQ_F16, 64, 128)
-    } else if (fl.x_dtype == AQ_I8) {
-        AQ_G(0, AQ_I8, 128, 128)
-        AQ_G(0, AQ_I8, 128, 64)
-        AQ_G(0, AQ_I8, 64, 128)
     } else {
         AQ_G(0, AQ_F16, 128, 128)
         AQ_G(0, AQ_F16, 128, 64)
