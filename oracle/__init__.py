@@ -1,4 +1,4 @@
-"""CPU oracle for the additively-quantized (AQ) layer forward.
+"""CPU oracle for the additively-quantized (AQ) layer forward and codebook gradient.
 
 TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
 benchmark's CPU-baseline leg may import this package.  The GPU library never
@@ -21,4 +21,8 @@ from .aq_oracle import (  # noqa: F401
     dense_conv_flops,
     lut_conv_flops,
     lut_breakpoint_cout,
+    weight_grad_linear,
+    weight_grad_conv,
+    codebook_grad_from_weight_grad,
+    codebook_grad,
 )

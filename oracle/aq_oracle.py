@@ -1,4 +1,5 @@
-"""Plain fp64 CPU oracle of the AQ linear / im2col-convolution forward.
+"""Plain fp64 CPU oracle of the AQ linear / im2col-convolution forward and of
+its codebook gradient.
 
 TEST INFRASTRUCTURE ONLY: imported by tests, by the smoke check and by the
 benchmark's CPU-baseline leg, never by the GPU library.
@@ -25,6 +26,10 @@ Every stored value (fp32, fp16, bf16, int8) converts to fp64 exactly, and the
 arithmetic is fp64 with numpy's BLAS matmul as the one library primitive.
 The LUT route of the appendix (eq. (12)) is an exact algebraic rearrangement
 of the same sum, so this plain definition is also the oracle for it.
+
+The codebook gradient (O7 below; the continuous step of PV-Tuning, Sec. 3.2)
+is the chain rule through the same definitions: dW = dY^T X, then a
+scatter-add of s[i] * dW over the codes.
 """
 from __future__ import annotations
 
@@ -291,3 +296,74 @@ def lut_breakpoint_cout(M: int, k: int, h1w1: int) -> float:
     function implements the count.
     """
     return M * (1 << k) * (2 * h1w1 - 1) / (2 * h1w1 - M)
+
+
+# ---------------------------------------------------------------------------
+# O7: codebook gradient (the continuous step of PV-Tuning, Sec. 3.2)
+# ---------------------------------------------------------------------------
+#
+# Knowledge distillation (Sec. 3.2) tunes the codebooks of every quantized
+# layer by gradient descent while the codes stay fixed between discrete
+# updates; the limitations paragraph of Sec. 5 names this optimizer's cost.
+# With the loss gradient dY at a layer's output, the chain rule through
+# Y = X W^T gives dW = dY^T X, and through eq. (4) (with the per-row scale)
+# every weight W[i, j*g + t] depends on codebook entry C[m, k, t] exactly
+# when b[i, j, m] = k, with derivative s[i].  Hence
+#     dC[m, k, t] = sum over (i, j) with b[i, j, m] = k of s[i] * dW[i, j*g + t].
+
+def weight_grad_linear(X: np.ndarray, dY: np.ndarray) -> np.ndarray:
+    """dW [C_out, K] = dY^T X for a linear layer (X [N, K], dY [N, C_out]), fp64."""
+    return np.asarray(dY, dtype=np.float64).T @ np.asarray(X, dtype=np.float64)
+
+
+def weight_grad_conv(x: np.ndarray, dy: np.ndarray, kh: int, kw: int, stride: int, pad: int) -> np.ndarray:
+    """dW [C_out, C*kh*kw] of an im2col convolution (Sec. 3.1.1), fp64.
+
+    ``x`` is the NCHW input and ``dy`` the NCHW output gradient; tokens are
+    (image, output row, output column) exactly as in the forward.
+    """
+    cols = im2col(x, kh, kw, stride, pad)                        # [N, K]
+    dy = np.asarray(dy, dtype=np.float64)
+    n, C_out, OH, OW = dy.shape
+    dY = dy.transpose(0, 2, 3, 1).reshape(n * OH * OW, C_out)     # token-major
+    if dY.shape[0] != cols.shape[0]:
+        raise ValueError("output gradient does not match the convolution geometry")
+    return dY.T @ cols
+
+
+def codebook_grad_from_weight_grad(dW: np.ndarray, codes: np.ndarray, scales: np.ndarray,
+                                   g: int, n_entries: int) -> np.ndarray:
+    """dC [M, n_entries, g] from dW [C_out, K] by the chain rule through eq. (4).
+
+    Each (row i, group j, codebook m) adds s[i] * dW[i, j*g : (j+1)*g] to row
+    b[i, j, m] of codebook m's gradient; ``np.add.at`` is the unbuffered
+    scatter-add, so repeated codes accumulate.
+    """
+    dW = np.asarray(dW, dtype=np.float64)
+    C_out, G, M = codes.shape
+    if dW.shape != (C_out, G * g):
+        raise ValueError("weight gradient shape does not match the codes")
+    contrib = np.asarray(scales, dtype=np.float64)[:, None, None] * dW.reshape(C_out, G, g)
+    dC = np.zeros((M, n_entries, g), dtype=np.float64)
+    idx = codes.astype(np.int64)
+    for m in range(M):
+        np.add.at(dC[m], idx[:, :, m].reshape(-1), contrib.reshape(C_out * G, g))
+    return dC
+
+
+def codebook_grad(spec, inputs, dy: np.ndarray, x_dtype: str = None, dy_dtype: str = "f64") -> np.ndarray:
+    """Gradient of the loss with respect to every codebook entry, [M, 2**B, g] fp64.
+
+    ``inputs`` holds codes, scales and the layer input ``x`` (stored in
+    ``x_dtype``, default the layer's); ``dy`` is the output gradient in the
+    layer's output layout ([N, C_out] or NCHW), stored in ``dy_dtype``.
+    """
+    xd = spec.x_dtype if x_dtype is None else x_dtype
+    X = activations_f64(inputs["x"], xd, inputs.get("x_scales"))
+    dY = np.asarray(dy, dtype=np.float64) if dy_dtype == "f64" else to_f64(dy, dy_dtype)
+    if spec.conv is None:
+        dW = weight_grad_linear(X, dY)
+    else:
+        c = spec.conv
+        dW = weight_grad_conv(X, dY, c.kh, c.kw, c.stride, c.pad)
+    return codebook_grad_from_weight_grad(dW, inputs["codes"], inputs["scales"], spec.g, 1 << spec.B)
