@@ -112,6 +112,31 @@ aq_status aq_layer_forward(aq_layer* layer, const void* X, const float* x_scales
  */
 aq_status aq_layer_decode(aq_layer* layer, void* W, void* stream);
 
+/*
+ * Codebook gradient, the continuous step of PV-Tuning (Sec. 3.2): codebooks
+ * are tuned by gradient descent while the codes stay fixed.  With dY the loss
+ * gradient at the layer output, the chain rule through Y = X * W^T and
+ * eq. (4) with the per-channel scale gives
+ *     dC[m][k][t] = sum over (i, j) with b[i][j][m] == k of s[i] * (dY^T X)[i][j*g + t],
+ * where X is the im2col matrix for a convolution (Sec. 3.1.1).
+ *   X      device; the forward's input layout (linear [n][K], conv NCHW);
+ *          dtype `dtype`; 16-byte aligned
+ *   dY     device; the forward's output layout (linear [n][C_out], conv NCHW
+ *          [n][C_out][OH][OW]); dtype `dtype`; 16-byte aligned
+ *   dtype  aq_dtype F16 or BF16, for both X and dY (others: AQ_ERR_UNSUPPORTED)
+ *   dC     device [M][2^B][g] fp32, caller-owned, overwritten
+ *   n      tokens (linear) or images (conv); tokens <= max_tokens
+ * Supported: linear layers with C_out and K multiples of 8; 1x1 and 3x3
+ * convolutions with stride 1, same padding and in_w a multiple of 8.  Other
+ * layers return AQ_ERR_UNSUPPORTED.  The first call on a layer builds an
+ * index of the codes and allocates a workspace of up to 16 * C_out * K * 4
+ * bytes (synchronous); later calls are asynchronous on `stream` and allocate
+ * nothing.  Summation orders are fixed: repeated calls give identical bits.
+ * Calls on one layer share its workspace: serialise them on one stream.
+ */
+aq_status aq_layer_codebook_grad(aq_layer* layer, const void* X, const void* dY, int32_t dtype, float* dC,
+                                 int64_t n, void* stream);
+
 /* Force a path for later forwards (AUTO restores the dispatcher).  Forcing an
  * unavailable path returns AQ_ERR_UNSUPPORTED and leaves the setting as is. */
 aq_status aq_layer_set_path(aq_layer* layer, aq_path path);

@@ -25,4 +25,5 @@ from .aq_oracle import (  # noqa: F401
     weight_grad_conv,
     codebook_grad_from_weight_grad,
     codebook_grad,
+    codebook_grad_entries,
 )

@@ -367,3 +367,49 @@ def codebook_grad(spec, inputs, dy: np.ndarray, x_dtype: str = None, dy_dtype: s
         c = spec.conv
         dW = weight_grad_conv(X, dY, c.kh, c.kw, c.stride, c.pad)
     return codebook_grad_from_weight_grad(dW, inputs["codes"], inputs["scales"], spec.g, 1 << spec.B)
+
+
+def codebook_grad_entries(spec, inputs, dy: np.ndarray, entries: Sequence[Sequence[int]],
+                          x_dtype: str = None, dy_dtype: str = "f64") -> np.ndarray:
+    """Rows dC[m, k, :] for the listed (m, k) pairs only, [len(entries), g] fp64.
+
+    Same definition as ``codebook_grad``, evaluated one entry at a time: the
+    (row, group) pairs with b[i, j, m] = k are found by a scan of the codes,
+    and only their columns of dW = dY^T X are formed (tokens as im2col rows
+    for a convolution), so layers too large for the full oracle stay cheap.
+    """
+    xd = spec.x_dtype if x_dtype is None else x_dtype
+    X = activations_f64(inputs["x"], xd, inputs.get("x_scales"))
+    dY = np.asarray(dy, dtype=np.float64) if dy_dtype == "f64" else to_f64(dy, dy_dtype)
+    codes = inputs["codes"]
+    s = np.asarray(inputs["scales"], dtype=np.float64)
+    g = spec.g
+    if spec.conv is not None:
+        c = spec.conv
+        n, C_out, OH, OW = dY.shape
+        dY = dY.transpose(0, 2, 3, 1).reshape(n * OH * OW, C_out)
+        _, C, H, Wd = X.shape
+        xp = np.zeros((n, C, H + 2 * c.pad, Wd + 2 * c.pad), dtype=np.float64)
+        xp[:, :, c.pad:c.pad + H, c.pad:c.pad + Wd] = X
+    out = np.zeros((len(entries), g), dtype=np.float64)
+    for e, (m, k) in enumerate(entries):
+        rows, groups = np.nonzero(codes[:, :, m].astype(np.int64) == k)
+        for i, j in zip(rows, groups):
+            if spec.conv is None:
+                cols = X[:, j * g:(j + 1) * g]
+            else:
+                cols = _im2col_columns(xp, c.kh, c.kw, c.stride, OH, OW, range(j * g, (j + 1) * g))
+            out[e] += s[i] * (dY[:, i] @ cols)
+    return out
+
+
+def _im2col_columns(xp: np.ndarray, kh: int, kw: int, stride: int, OH: int, OW: int, ks) -> np.ndarray:
+    """Columns ``ks`` of im2col (Sec. 3.1.1 ordering) of the zero-padded input
+    ``xp``, [n*OH*OW, len(ks)], without forming the rest."""
+    cols = []
+    for k in ks:
+        ch, rs = divmod(k, kh * kw)
+        r, q = divmod(rs, kw)
+        patch = xp[:, ch, r:r + stride * (OH - 1) + 1:stride, q:q + stride * (OW - 1) + 1:stride]
+        cols.append(patch.reshape(-1))
+    return np.stack(cols, axis=1)

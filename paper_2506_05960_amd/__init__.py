@@ -1,4 +1,4 @@
-"""MI355X-native additively-quantized (AQ) layer forward.
+"""MI355X-native additively-quantized (AQ) layer: forward and codebook gradient.
 
 The product is ``libaq.so`` (HIP kernels for gfx950 behind the C ABI in
 ``include/aq.h``); this package holds its sources (``csrc/``), the build
@@ -14,6 +14,7 @@ from .aq import (  # noqa: F401
     aq_layer_create,
     aq_layer_forward,
     aq_layer_decode,
+    aq_layer_codebook_grad,
     aq_layer_set_path,
     aq_layer_choose_path,
     aq_layer_destroy,

@@ -24,8 +24,8 @@ PATH_NAMES = {v: k for k, v in PATH_CODES.items()}
 STATUS_NAMES = {0: "AQ_OK", 1: "AQ_ERR_INVALID_ARGUMENT", 2: "AQ_ERR_UNSUPPORTED", 3: "AQ_ERR_OUT_OF_MEMORY",
                 4: "AQ_ERR_DEVICE"}
 
-EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_set_path",
-            "aq_layer_choose_path", "aq_layer_destroy", "aq_last_error", "aq_version")
+EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
+            "aq_layer_set_path", "aq_layer_choose_path", "aq_layer_destroy", "aq_last_error", "aq_version")
 
 
 class AQError(RuntimeError):
@@ -69,11 +69,12 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_create.argtypes = [ctypes.POINTER(aq_layer_desc), vp, vp, vp, i32, i32, i32, ctypes.POINTER(vp)]
     lib.aq_layer_forward.argtypes = [vp, vp, vp, vp, i64, vp]
     lib.aq_layer_decode.argtypes = [vp, vp, vp]
+    lib.aq_layer_codebook_grad.argtypes = [vp, vp, vp, i32, vp, i64, vp]
     lib.aq_layer_set_path.argtypes = [vp, i32]
     lib.aq_layer_choose_path.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_int)]
     lib.aq_layer_destroy.argtypes = [vp]
-    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_set_path",
-              "aq_layer_choose_path", "aq_layer_destroy"):
+    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
+              "aq_layer_set_path", "aq_layer_choose_path", "aq_layer_destroy"):
         getattr(lib, f).restype = ctypes.c_int
     lib.aq_last_error.restype = ctypes.c_char_p
     lib.aq_last_error.argtypes = []
@@ -123,6 +124,10 @@ def aq_layer_forward(handle: int, X: int, x_scales: int, Y: int, n: int, stream:
 
 def aq_layer_decode(handle: int, W: int, stream: int) -> None:
     _check(load_library().aq_layer_decode(handle, W, stream))
+
+
+def aq_layer_codebook_grad(handle: int, X: int, dY: int, dtype: str, dC: int, n: int, stream: int) -> None:
+    _check(load_library().aq_layer_codebook_grad(handle, X, dY, DTYPE_CODES[dtype], dC, n, stream))
 
 
 def aq_layer_set_path(handle: int, path: str) -> None:
@@ -195,6 +200,19 @@ class AQLayer:
             out = torch.empty((s.C_out, s.K), dtype=dt, device="cuda")
         st = stream if stream is not None else torch.cuda.current_stream().cuda_stream
         aq_layer_decode(self.handle, out.data_ptr(), st)
+        return out
+
+    def codebook_grad(self, x, dy, out=None, stream=None):
+        """dC [M, 2**B, g] fp32 for input ``x`` and output gradient ``dy`` (both fp16 or bf16 device tensors)."""
+        import torch
+        s = self.spec
+        if x.dtype != dy.dtype or x.dtype not in (torch.float16, torch.bfloat16):
+            raise ValueError("x and dy must share one dtype, float16 or bfloat16")
+        if out is None:
+            out = torch.empty((s.M, 1 << s.B, s.g), dtype=torch.float32, device=x.device)
+        st = stream if stream is not None else torch.cuda.current_stream(x.device).cuda_stream
+        dt = "f16" if x.dtype == torch.float16 else "bf16"
+        aq_layer_codebook_grad(self.handle, x.data_ptr(), dy.data_ptr(), dt, out.data_ptr(), x.shape[0], st)
         return out
 
     def set_path(self, path: str) -> None:

@@ -6,6 +6,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "aq.h"
 
 namespace aq {
@@ -119,5 +121,21 @@ int lut_tokens_per_entry(const LutPlan& plan, int ntok);
 
 hipError_t launch_f32_forward(const Geom& geo, const DeviceWeights& w, const void* X, int x_dtype,
                               const float* x_scales, void* Y, int y_dtype, hipStream_t stream);
+
+// ---- codebook gradient ----
+
+struct GradPlan {
+    int bm, bn;                   // weight-gradient tile: output channels x inputs
+    int tiles_m, tiles_n;
+    int s_max;                    // most token splits (partial buffers in the workspace)
+};
+
+GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens);
+// X, dY: fp16 or bf16 (dtype); P: [s_max][C_out][K] fp32 workspace; offs / ent: the code index
+hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, const void* X, const void* dY,
+                                const float* scales, float* P, const int32_t* offs, const int32_t* ent, float* dC,
+                                int splits_override, hipStream_t st);
+void build_code_index(const void* codes, int B, int C_out, int G, int M, std::vector<int32_t>& offs,
+                      std::vector<int32_t>& ent);
 
 }  // namespace aq

@@ -31,6 +31,12 @@ struct aq_layer {
     void* d_wrec;             // fused-path operand records, decoded per forward in the pre-decoded mode
     void* d_xpack;            // dense product: activations repacked per forward
     void* d_zero;             // 256 zero bytes
+    // codebook gradient, prepared by the first gradient call
+    bool grad_ready;
+    aq::GradPlan gplan;
+    int32_t* d_gidx_offs;     // [M][2^B + 1] list offsets per codebook entry
+    int32_t* d_gidx_ent;      // [M][C_out * G] (row, group) pairs i * G + j, sorted by code
+    float* d_gpart;           // [s_max][C_out][K] fp32 partial weight gradients
     bool lut_ok, dec_ok, fused_ok;
     aq_path path;
     int64_t lut_max_tokens;
@@ -128,7 +134,8 @@ aq_path choose(const aq_layer* L, int64_t tokens) {
 void free_layer(aq_layer* L) {
     if (!L) return;
     void* ptrs[] = {L->d_cb,     L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales,
-                    L->d_ws,     L->d_crec, L->d_wrec,   L->d_xpack, L->d_zero};
+                    L->d_ws,     L->d_crec, L->d_wrec,   L->d_xpack, L->d_zero, L->d_gidx_offs,
+                    L->d_gidx_ent, L->d_gpart};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete L;
@@ -602,6 +609,64 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
         }
     }
     if (e != hipSuccess) return hip_fail(e, "forward launch");
+    return AQ_OK;
+}
+
+// Codebook gradient: validation, one-time preparation (code index and
+// partial-gradient workspace), then the two launches.
+aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int32_t dtype, float* dC, int64_t n,
+                                 void* stream) {
+    if (!L || !X || !dY || !dC) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    if (n < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "n must be >= 1");
+    if (dtype < AQ_F32 || dtype > AQ_I8) return fail(AQ_ERR_INVALID_ARGUMENT, "bad dtype");
+    if (dtype != AQ_F16 && dtype != AQ_BF16)
+        return fail(AQ_ERR_UNSUPPORTED, "the codebook gradient takes fp16 or bf16 X and dY");
+    const aq_layer_desc& d = L->desc;
+    const Geom geo = make_geom(L, n);
+    if (geo.tokens > d.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens");
+    if ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(dY)) & 15)
+        return fail(AQ_ERR_INVALID_ARGUMENT, "X and dY must be 16-byte aligned");
+    if (reinterpret_cast<uintptr_t>(dC) & 3) return fail(AQ_ERR_INVALID_ARGUMENT, "dC must be 4-byte aligned");
+    if (geo.conv) {
+        const bool k3 = geo.kh == 3 && geo.kw == 3 && geo.pad == 1, k1 = geo.kh == 1 && geo.kw == 1 && geo.pad == 0;
+        if (!(k3 || k1) || geo.stride != 1 || geo.W % 8 != 0)
+            return fail(AQ_ERR_UNSUPPORTED, "the codebook gradient supports 1x1 and 3x3 convolutions with stride 1, "
+                                            "same padding and an input width that is a multiple of 8");
+    } else if (geo.C_out % 8 != 0 || geo.K % 8 != 0) {
+        return fail(AQ_ERR_UNSUPPORTED, "the codebook gradient of a linear layer needs C_out and K multiples of 8");
+    }
+    if ((int64_t)geo.C_out * geo.G >= (int64_t(1) << 31))
+        return fail(AQ_ERR_UNSUPPORTED, "too many code groups for the 32-bit code index");
+    if (!L->grad_ready) {
+        // one-time preparation: synchronous and allocating
+        const size_t ncodes = (size_t)geo.C_out * geo.G * geo.M;
+        std::vector<uint8_t> host(ncodes * (geo.B <= 8 ? 1 : 2));
+        hipError_t e = hipMemcpy(host.data(), L->d_codes, host.size(), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(e, "codes readback");
+        std::vector<int32_t> offs, ent;
+        aq::build_code_index(host.data(), geo.B, geo.C_out, geo.G, geo.M, offs, ent);
+        L->gplan = aq::grad_plan_create(geo, d.max_tokens);
+        aq_status s = dev_upload(&L->d_gidx_offs, offs.data(), offs.size() * sizeof(int32_t), "code index");
+        if (s == AQ_OK) s = dev_upload(&L->d_gidx_ent, ent.data(), ent.size() * sizeof(int32_t), "code index");
+        if (s == AQ_OK)
+            s = dev_upload(&L->d_gpart, nullptr, (size_t)L->gplan.s_max * geo.C_out * geo.K * sizeof(float),
+                           "gradient workspace");
+        if (s != AQ_OK) {
+            for (void** p : {(void**)&L->d_gidx_offs, (void**)&L->d_gidx_ent, (void**)&L->d_gpart})
+                if (*p) {
+                    (void)hipFree(*p);
+                    *p = nullptr;
+                }
+            return s;
+        }
+        L->grad_ready = true;
+    }
+    int splits = 0;
+    if (const char* sv = std::getenv("AQ_GRAD_SPLITS")) splits = std::atoi(sv);
+    const hipError_t e =
+        aq::launch_codebook_grad(geo, L->gplan, dtype, X, dY, L->d_scales, L->d_gpart, L->d_gidx_offs, L->d_gidx_ent,
+                                 dC, splits, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "codebook gradient launch");
     return AQ_OK;
 }
 

@@ -156,6 +156,8 @@ def test_null_handles_are_rejected():
     lib = _lib()
     assert lib.aq_layer_forward(None, 16, None, 16, 1, None) == A.AQ_ERR_INVALID_ARGUMENT
     assert lib.aq_layer_decode(None, 16, None) == A.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layer_codebook_grad(None, 16, 16, A.AQ_F16, 16, 1, None) == A.AQ_ERR_INVALID_ARGUMENT
+    assert "null" in lib.aq_last_error().decode()
     assert lib.aq_layer_set_path(None, A.AQ_PATH_LUT) == A.AQ_ERR_INVALID_ARGUMENT
     out = ctypes.c_int()
     assert lib.aq_layer_choose_path(None, 4, ctypes.byref(out)) == A.AQ_ERR_INVALID_ARGUMENT

@@ -164,3 +164,30 @@ def test_stored_dtypes_widen_exactly():
     dyr = O.bf16_bits_to_f32(dyb).astype(np.float64)
     d = O.codebook_grad(spec, {"codes": codes, "scales": s, "x": xr}, dyr, x_dtype="f32")
     assert np.array_equal(c, d)
+
+
+@pytest.mark.parametrize("conv", [None, (3, 1, 1), (1, 1, 0), (3, 2, 1)])
+def test_entry_sampled_gradient_matches_full(conv):
+    """The per-entry evaluation used at full layer sizes agrees with the whole-tensor oracle."""
+    rng = np.random.default_rng(60 + (0 if conv is None else conv[0] + conv[1]))
+    g, M, B, C_out = 8, 2, 3, 5
+    if conv is None:
+        G, N = 4, 9
+        x = rng.normal(size=(N, G * g))
+        dy = rng.normal(size=(N, C_out))
+        spec = _spec(g, M, B)
+    else:
+        kh, stride, pad = conv
+        C, H, Wd = 8, 5, 6
+        G = C * kh * kh // g
+        x = rng.normal(size=(2, C, H, Wd))
+        OH = (H + 2 * pad - kh) // stride + 1
+        OW = (Wd + 2 * pad - kh) // stride + 1
+        dy = rng.normal(size=(2, C_out, OH, OW))
+        spec = _spec(g, M, B, _conv(kh, kh, stride, pad))
+    _, codes, s = _layer(rng, C_out, G, g, M, B)
+    inputs = {"codes": codes, "scales": s, "x": x}
+    full = O.codebook_grad(spec, inputs, dy)
+    entries = [(m, k) for m in range(M) for k in range(1 << B)]
+    part = O.codebook_grad_entries(spec, inputs, dy, entries)
+    np.testing.assert_allclose(part, full.reshape(-1, g), rtol=1e-12, atol=1e-12)

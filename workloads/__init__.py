@@ -1,4 +1,4 @@
-"""Seeded synthetic inputs for the additively-quantized (AQ) layer forward.
+"""Seeded synthetic inputs for the additively-quantized (AQ) layer forward and codebook gradient.
 
 This package only draws random numbers and does shape bookkeeping; it holds
 none of the AQ arithmetic (no decode, no matmul).  Both the CPU oracle tests
@@ -9,6 +9,7 @@ from .layers import (  # noqa: F401
     ConvGeom,
     LayerSpec,
     generate,
+    generate_grad_inputs,
     CONFIGS,
     config_spec,
     config_inputs,

@@ -160,6 +160,24 @@ def generate(spec: LayerSpec, seed: int) -> Dict[str, np.ndarray]:
     return {"codebooks": codebooks, "codes": codes, "scales": scales, "x": x, "x_scales": x_scales}
 
 
+def generate_grad_inputs(spec: LayerSpec, seed: int, dtype: str = "f16") -> Dict[str, np.ndarray]:
+    """Layer input ``x`` and output gradient ``dy`` for the codebook gradient.
+
+    Both are drawn from ``default_rng(seed)`` as N(0, x_std) and N(0, 1) in
+    ``dtype`` (fp16, or bf16 as uint16 bits), in the forward's layouts:
+    [n, K] and [n, C_out] for a linear layer, NCHW for a convolution.
+    """
+    rng = np.random.default_rng(seed)
+    if spec.conv is None:
+        xshape, yshape = (spec.n, spec.K), (spec.n, spec.C_out)
+    else:
+        c = spec.conv
+        xshape, yshape = (spec.n, c.cin, c.H, c.W), (spec.n, spec.C_out, c.OH, c.OW)
+    x = _cast(rng.normal(0.0, spec.x_std, size=xshape), dtype)
+    dy = _cast(rng.normal(0.0, 1.0, size=yshape), dtype)
+    return {"x": x, "dy": dy}
+
+
 # ---------------------------------------------------------------------------
 # The four single-layer workloads plus the LDM-4-shaped sweep.
 # ---------------------------------------------------------------------------
