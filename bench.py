@@ -272,6 +272,75 @@ def lut_regime_bench(a, torch, P, W):
     }
 
 
+def grad_bench(a, torch, P, W):
+    """One step = one codebook gradient (weight gradient on the matrix cores plus the code-indexed gather).
+
+    The workload is the named layer with fp16 X and dY (an int8 forward input is
+    replaced by fp16 values of the same shape).  FLOPs are those of dY^T X,
+    2 per multiply-accumulate, the same count as the forward.
+    """
+    import dataclasses
+
+    import numpy as np
+
+    spec = W.config_spec(a.config)
+    if spec.x_dtype != "f16":
+        spec = dataclasses.replace(spec, x_dtype="f16")
+    inp = W.generate(spec, W.SEED_BASE + 100)
+    gi = W.generate_grad_inputs(spec, W.SEED_BASE + 101, "f16")
+    layer = P.AQLayer(spec, inp)
+    x = torch.from_numpy(np.ascontiguousarray(gi["x"])).cuda()
+    dy = torch.from_numpy(np.ascontiguousarray(gi["dy"])).cuda()
+    dC = torch.empty((spec.M, 1 << spec.B, spec.g), dtype=torch.float32, device="cuda")
+    for _ in range(max(1, a.warmup)):
+        layer.codebook_grad(x, dy, out=dC)       # the first call prepares the code index
+    torch.cuda.synchronize()
+    per_graph = max(1, min(a.steps, 50))
+    reps = (a.steps + per_graph - 1) // per_graph
+    us = _graph_time_us(torch, lambda: layer.codebook_grad(x, dy, out=dC), per_graph, trials=reps)
+    ms = us * 1e-3
+    flops = spec.dense_flops
+    tflops = flops / (ms * 1e-3) / 1e12
+    out = {
+        "metric": "dense-equivalent TFLOP/s of the AQ codebook gradient",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": reps * per_graph,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms, 6),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded; LDM-4-shaped layer, random codes, fp16 activations and output gradients)",
+        "config": {"workload": spec.name + "_codebook_grad", "launch": f"hip graph of {per_graph} steps",
+                   "tokens": spec.tokens, "K": spec.K, "C_out": spec.C_out, "g": spec.g, "M": spec.M, "B": spec.B},
+        "dense_flops": flops,
+        # both launches of a step (weight gradient, then gather); the kernel
+        # trace splits them
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_MFMA_F16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / PEAK_MFMA_F16_TFLOPS, 4), "traffic": None, "kernel_us": round(us, 3)},
+    }
+    if not a.no_cpu_baseline:
+        import oracle as O
+        ginp = {"codes": inp["codes"], "scales": inp["scales"], "x": gi["x"]}
+        t0 = time.perf_counter()
+        O.codebook_grad(spec, ginp, gi["dy"], x_dtype="f16", dy_dtype="f16")
+        t = time.perf_counter() - t0
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+        except Exception:
+            threads = os.cpu_count() or 1
+        out["cpu_baseline"] = {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+                               "kind": "oracle",
+                               "sample": f"whole layer ({spec.name}): fp64 dY^T X (BLAS) + scatter-add, one run, "
+                                         f"{t:.3f} s"}
+    layer.close()
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -287,6 +356,8 @@ def main(argv=None):
                     help="sweep: M = 2 or 4 codebooks of 256 (K: 3x3 convolutions with g = 9, one group per filter)")
     ap.add_argument("--full", action="store_true", help="sweep: every linear of the transformer blocks")
     ap.add_argument("--table", default="", help="sweep: write the per-layer table (markdown) here")
+    ap.add_argument("--op", default="forward", choices=["forward", "grad"],
+                    help="grad: the codebook gradient of the named layer instead of its forward")
     a = ap.parse_args(argv)
 
     if a.gpus != 1:
@@ -307,6 +378,9 @@ def main(argv=None):
         return 0
     if a.config == "lutregime":
         print(json.dumps(lut_regime_bench(a, torch, P, W)), flush=True)
+        return 0
+    if a.op == "grad":
+        print(json.dumps(grad_bench(a, torch, P, W)), flush=True)
         return 0
     spec = W.config_spec(a.config)
     inp = W.config_inputs(a.config)

@@ -129,9 +129,11 @@ aq_status aq_layer_decode(aq_layer* layer, void* W, void* stream);
  * Supported: linear layers with C_out and K multiples of 8; 1x1 and 3x3
  * convolutions with stride 1, same padding and in_w a multiple of 8.  Other
  * layers return AQ_ERR_UNSUPPORTED.  The first call on a layer builds an
- * index of the codes and allocates a workspace of up to 16 * C_out * K * 4
- * bytes (synchronous); later calls are asynchronous on `stream` and allocate
- * nothing.  Summation orders are fixed: repeated calls give identical bits.
+ * index of the codes (4 * C_out * (K/g) * M bytes) and a workspace of fp32
+ * partial weight gradients, one C_out x K slice per token split, at most
+ * max(32 MiB, C_out * K * 4) bytes (synchronous).  Later calls are
+ * asynchronous on `stream` and allocate nothing.  Summation orders are
+ * fixed: repeated calls give identical bits.
  * Calls on one layer share its workspace: serialise them on one stream.
  */
 aq_status aq_layer_codebook_grad(aq_layer* layer, const void* X, const void* dY, int32_t dtype, float* dC,

@@ -16,6 +16,37 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Raw buffer resource over `bytes` bytes; loads at offsets >= bytes return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0,
+                                             (int)(uint32_t)(bytes < 0xFFFFFFFFull ? bytes : 0xFFFFFFFFull), 0x00020000);
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;   // byte offset past every buffer the kernels read
+
+// ---- direct-to-LDS loads ----
+
+// 16 bytes from global memory into LDS: lane l of the wave writes slot
+// dst_wave_base + 16 * l (the base must be wave-uniform).
+__device__ __forceinline__ void lds_dma16(const uint8_t* src, uint8_t* dst_wave_base) {
+    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
+                                     (__attribute__((address_space(3))) void*)dst_wave_base, 16, 0, 0);
+}
+
+// s_waitcnt with vmcnt <= n (n < 64), expcnt and lgkmcnt unrestricted (gfx9 encoding)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt field");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier without the release fence of __syncthreads(): that fence
+// waits for every outstanding vector-memory operation, which would also drain
+// the direct-to-LDS prefetches of later chunks.  LDS reads issued before the
+// barrier are drained here; the DMA writes are awaited by wait_vmcnt.
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // ---- scalar conversions (storage bits <-> fp32) ----
 
 __device__ __forceinline__ float f16_to_f32(uint16_t b) { return (float)__builtin_bit_cast(_Float16, b); }

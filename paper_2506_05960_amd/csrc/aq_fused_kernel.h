@@ -66,12 +66,6 @@ __device__ __forceinline__ uint32_t pick2(uint32_t xlo, int hlo, uint32_t xhi, i
     return __builtin_amdgcn_perm(xhi, xlo, sel);
 }
 
-// Raw buffer resource over `bytes` bytes; loads at offsets >= bytes return zero.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uint64_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0,
-                                             (int)(uint32_t)(bytes < 0xFFFFFFFFull ? bytes : 0xFFFFFFFFull), 0x00020000);
-}
-constexpr uint32_t kOutOfRange = 0x80000000u;   // byte offset past every buffer this kernel reads
 
 // Quotient of non-negative a < 2^24 by d >= 1 through an fp32 reciprocal,
 // corrected to the exact integer quotient.

@@ -16,6 +16,8 @@
 //      the kernel sums their s-scaled gradient groups over all splits in a
 //      fixed order.  No atomics: repeated calls give identical bits.
 #include <algorithm>
+#include <cstdio>
+#include <cstdlib>
 #include <vector>
 
 #include "aq_device.h"
@@ -62,27 +64,25 @@ __device__ __forceinline__ u32x4 block_column(const u32x4 (&r)[8], int e) {
 
 // Eight input values shifted by d in {-1, 0, +1} positions along the row:
 // out[e] = in[e + d], with `nb` the value that enters at the open end.
+// Branch-free: d differs between the lanes of a wave.
 __device__ __forceinline__ u32x4 shift_row(const u32x4& v, uint32_t nb, int d) {
-    if (d == 0) return v;
+    const u32x4 lo{__builtin_amdgcn_alignbyte(v[0], nb << 16, 2), __builtin_amdgcn_alignbyte(v[1], v[0], 2),
+                   __builtin_amdgcn_alignbyte(v[2], v[1], 2), __builtin_amdgcn_alignbyte(v[3], v[2], 2)};
+    const u32x4 hi{__builtin_amdgcn_alignbyte(v[1], v[0], 2), __builtin_amdgcn_alignbyte(v[2], v[1], 2),
+                   __builtin_amdgcn_alignbyte(v[3], v[2], 2), __builtin_amdgcn_alignbyte(nb, v[3], 2)};
     u32x4 o;
-    if (d < 0) {
-        o[0] = __builtin_amdgcn_alignbyte(v[0], nb << 16, 2);
-        o[1] = __builtin_amdgcn_alignbyte(v[1], v[0], 2);
-        o[2] = __builtin_amdgcn_alignbyte(v[2], v[1], 2);
-        o[3] = __builtin_amdgcn_alignbyte(v[3], v[2], 2);
-    } else {
-        o[0] = __builtin_amdgcn_alignbyte(v[1], v[0], 2);
-        o[1] = __builtin_amdgcn_alignbyte(v[2], v[1], 2);
-        o[2] = __builtin_amdgcn_alignbyte(v[3], v[2], 2);
-        o[3] = __builtin_amdgcn_alignbyte(nb, v[3], 2);
-    }
+#pragma unroll
+    for (int w = 0; w < 4; ++w) o[w] = d < 0 ? lo[w] : (d > 0 ? hi[w] : v[w]);
     return o;
 }
 
 // KIND: 0 linear (token-major X [N][K], dY [N][C_out]); 1 3x3 and 2 1x1
 // convolutions with stride 1 and same padding (NCHW X and dY, OW % 8 == 0).
+// Two workgroups per CU, except the 128 x 128 convolution tile, whose two
+// register sets of eight staged rows each need the whole register file.
 template <int KIND, int DT, int BM, int BN>
-__global__ void __launch_bounds__(256, 2) wgrad_kernel(Geom geo, GradArgs ga) {
+__global__ void __launch_bounds__(256, (KIND != 0 && BM == 128 && BN == 128) ? 1 : 2)
+    wgrad_kernel(Geom geo, GradArgs ga) {
     constexpr bool CONV = KIND != 0;
     constexpr int KHW = KIND == 1 ? 9 : 1, KW = KIND == 1 ? 3 : 1, PAD = KIND == 1 ? 1 : 0;
     constexpr int WM = BM / 2, WN = BN / 2, AM = WM / 32, AN = WN / 32;
@@ -108,63 +108,95 @@ __global__ void __launch_bounds__(256, 2) wgrad_kernel(Geom geo, GradArgs ga) {
     const int l32 = lane & 31, hi = lane >> 5;
     const int64_t N = geo.tokens;
 
-    // ---- staging: global -> registers (next chunk) -> LDS ----
-    u32x4 rv[CONV ? VPT : 8];
-    uint32_t nbv[CONV ? VPT : 1];
-    int dsh[CONV ? VPT : 1];
-    auto load_chunk = [&](int chunk) {
-        const int64_t n0 = (int64_t)chunk * kGradChunk;
+    // ---- staging: global -> registers -> LDS ----
+    // Register sets hold whole chunks; loads run two chunks ahead of the
+    // matrix cores.  Offsets are 32-bit (the host checks the sizes).
+    constexpr int NV = CONV ? VPT : 8;
+    constexpr int NB = CONV ? VPT : 1;
+    const int N32 = (int)N;
+    // convolution: every unit of this thread shares the token block tb = tid % 8;
+    // per-row parts of the addresses are fixed for the whole loop
+    int roff[NB], rmeta[NB];     // A: i*P; B: c*H*W | meta: bit0 live, bits 1..4 kernel row, bits 5..6 shift+1
+    if constexpr (CONV) {
+        const int P = geo.OH * geo.OW;
+#pragma unroll
+        for (int u = 0; u < VPT; ++u) {
+            const int row = (tid >> 3) + 32 * u;
+            if (u < BM / 32) {
+                const int i = i0 + row;
+                roff[u] = i * P;
+                rmeta[u] = (i < geo.C_out) ? 1 : 0;
+            } else {
+                const int k = k0 + row - BM;
+                const int c = k / KHW, rs = k - c * KHW;
+                const int r = rs / KW, q = rs - r * KW;
+                roff[u] = c * geo.H * geo.W;
+                rmeta[u] = (k < geo.K ? 1 : 0) | (r << 1) | ((q - PAD + 1) << 5);
+            }
+        }
+    }
+    // Loads are branch-free buffer loads: an invalid element's offset lies past
+    // the buffer, which returns zero.
+    const int64_t xbytes = CONV ? (N / (geo.OH * geo.OW)) * geo.cin * geo.H * geo.W * 2 : N * geo.K * 2;
+    const __amdgpu_buffer_rsrc_t rx = buffer_rsrc(ga.X, (uint64_t)xbytes);
+    const __amdgpu_buffer_rsrc_t ry = buffer_rsrc(ga.dY, (uint64_t)(N * geo.C_out * 2));
+    auto load_chunk = [&](int chunk, u32x4 (&rv)[NV], uint32_t (&nbv)[NB]) {
+        const int n0 = chunk * kGradChunk;
         if constexpr (!CONV) {
-            // one 8x8 block per thread: 8 tokens x 8 channels (dY) or 8 inputs (X)
-            const bool isA = tid < BM;
+            // one 8x8 block per thread: 8 tokens x 8 channels (dY) or 8 inputs (X);
+            // BM is a multiple of 64, so whole waves load dY
+            const bool isA = __builtin_amdgcn_readfirstlane(tid >> 6) * 64 < BM;
             const int bid = isA ? tid : tid - BM;
             const int nb8 = isA ? BM / 8 : BN / 8;
             const int cb = bid % nb8, tb = bid / nb8;
             const int len = isA ? geo.C_out : geo.K;
             const int col = (isA ? i0 : k0) + 8 * cb;
-            const uint16_t* src = isA ? ga.dY : ga.X;
-            const bool live = tid < ROWS && col < len;
+            const bool live = tid < ROWS && col < len && chunk < c_end;
+            uint32_t off[8];
 #pragma unroll
             for (int a = 0; a < 8; ++a) {
-                const int64_t n = n0 + 8 * tb + a;
-                rv[a] = (live && n < N) ? *reinterpret_cast<const u32x4*>(src + n * len + col) : u32x4{0, 0, 0, 0};
+                const int n = n0 + 8 * tb + a;
+                off[a] = (live && n < N32) ? (uint32_t)(n * len + col) * 2u : kOutOfRange;
+            }
+            if (isA) {
+#pragma unroll
+                for (int a = 0; a < 8; ++a) rv[a] = __builtin_amdgcn_raw_buffer_load_b128(ry, off[a], 0, 0);
+            } else {
+#pragma unroll
+                for (int a = 0; a < 8; ++a) rv[a] = __builtin_amdgcn_raw_buffer_load_b128(rx, off[a], 0, 0);
             }
         } else {
-            const int64_t P = (int64_t)geo.OH * geo.OW;
+            const int P = geo.OH * geo.OW;
+            const int n = n0 + 8 * (tid & 7);
+            const bool live_n = n < N32 && chunk < c_end;
+            // unconditional (a select around the division becomes a branch)
+            const int b = (int)((unsigned)n / (unsigned)P);
+            const int p = n - b * P;
+            const int oh = (int)((unsigned)p / (unsigned)geo.OW);
+            const int ow0 = p - oh * geo.OW;
+            const int ybase = b * geo.C_out * P + p;
+            const int xbase = b * geo.cin * geo.H * geo.W + ow0;
 #pragma unroll
             for (int u = 0; u < VPT; ++u) {
-                const int v = tid + 256 * u;
-                const int row = v >> 3, tb = v & 7;
-                const int64_t n = n0 + 8 * tb;
-                rv[u] = u32x4{0, 0, 0, 0};
-                nbv[u] = 0;
-                dsh[u] = 0;
-                if (n >= N) continue;
-                const int64_t b = n / P;
-                const int64_t p = n - b * P;
-                if (row < BM) {
-                    const int i = i0 + row;
-                    if (i < geo.C_out)
-                        rv[u] = *reinterpret_cast<const u32x4*>(ga.dY + (b * geo.C_out + i) * P + p);
-                } else {
-                    const int k = k0 + row - BM;
-                    if (k >= geo.K) continue;
-                    const int c = k / KHW, rs = k - c * KHW;
-                    const int r = rs / KW, q = rs - r * KW;
-                    const int oh = (int)(p / geo.OW), ow0 = (int)(p - (int64_t)oh * geo.OW);
-                    const int ih = oh + r - PAD;
-                    if (ih < 0 || ih >= geo.H) continue;
-                    const uint16_t* rowp = ga.X + ((b * geo.cin + c) * geo.H + ih) * (int64_t)geo.W;
-                    rv[u] = *reinterpret_cast<const u32x4*>(rowp + ow0);
-                    const int d = q - PAD;
-                    dsh[u] = d;
-                    if (d < 0 && ow0 > 0) nbv[u] = rowp[ow0 - 1];
-                    if (d > 0 && ow0 + 8 < geo.W) nbv[u] = rowp[ow0 + 8];
+                const bool live = live_n && (rmeta[u] & 1);
+                if (u < BM / 32) {           // rows of dY (the row index is 32u + tid / 8)
+                    const uint32_t off = live ? (uint32_t)(ybase + roff[u]) * 2u : kOutOfRange;
+                    rv[u] = __builtin_amdgcn_raw_buffer_load_b128(ry, off, 0, 0);
+                    nbv[u] = 0;
+                } else {                     // im2col rows of X: a shifted input row
+                    const int ih = oh + ((rmeta[u] >> 1) & 15) - PAD;
+                    const bool ok = live && ih >= 0 && ih < geo.H;
+                    const uint32_t off = ok ? (uint32_t)(xbase + roff[u] + ih * geo.W) * 2u : kOutOfRange;
+                    const int d = (rmeta[u] >> 5) - 1;
+                    const bool nb_ok = ok && ((d < 0 && ow0 > 0) || (d > 0 && ow0 + 8 < geo.W));
+                    const uint32_t noff = nb_ok ? (d < 0 ? off - 2u : off + 16u) : kOutOfRange;
+                    rv[u] = __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0);
+                    nbv[u] = __builtin_amdgcn_raw_buffer_load_b16(rx, noff, 0, 0);
                 }
             }
         }
     };
-    auto store_chunk = [&](uint16_t* st) {
+    auto store_chunk = [&](uint16_t* st, const u32x4 (&rv)[NV], const uint32_t (&nbv)[NB]) {
         if constexpr (!CONV) {
             if (tid < ROWS) {
                 const bool isA = tid < BM;
@@ -179,9 +211,9 @@ __global__ void __launch_bounds__(256, 2) wgrad_kernel(Geom geo, GradArgs ga) {
         } else {
 #pragma unroll
             for (int u = 0; u < VPT; ++u) {
-                const int v = tid + 256 * u;
-                const int row = v >> 3, tb = v & 7;
-                *reinterpret_cast<u32x4*>(st + row * kGradPitch + 8 * tb) = shift_row(rv[u], nbv[u], dsh[u]);
+                const int row = (tid >> 3) + 32 * u;
+                const int d = u < BM / 32 ? 0 : (rmeta[u] >> 5) - 1;
+                *reinterpret_cast<u32x4*>(st + row * kGradPitch + 8 * (tid & 7)) = shift_row(rv[u], nbv[u], d);
             }
         }
     };
@@ -212,16 +244,32 @@ __global__ void __launch_bounds__(256, 2) wgrad_kernel(Geom geo, GradArgs ga) {
         }
     };
 
+    // Chunk c computes from LDS stage c % 2.  At the top of its iteration one
+    // register set holds chunk c + 1 and the other receives chunk c + 2; chunk
+    // c + 1 goes to the free stage after the MFMAs.  The loop body is written
+    // twice so that the two register sets swap roles without copies.  Loads
+    // past the split's last chunk are issued anyway with out-of-range offsets:
+    // unconditional loads keep the compiler's wait counts exact (a load that
+    // is issued on one path only makes it wait for every load at the join).
     if (c_beg < c_end) {
-        load_chunk(c_beg);
-        store_chunk(lds);
+        u32x4 ra[NV], rb[NV];
+        uint32_t na[NB], nbr[NB];
+        load_chunk(c_beg, ra, na);
+        store_chunk(lds, ra, na);
+        load_chunk(c_beg + 1, ra, na);
         __syncthreads();
-        for (int c = c_beg; c < c_end; ++c) {
-            const int cur = (c - c_beg) & 1;
-            if (c + 1 < c_end) load_chunk(c + 1);
-            compute(lds + cur * STAGE);
-            if (c + 1 < c_end) store_chunk(lds + (cur ^ 1) * STAGE);
+        int c = c_beg;
+        while (true) {
+            load_chunk(c + 2, rb, nbr);
+            compute(lds + ((c - c_beg) & 1) * STAGE);
+            store_chunk(lds + ((c + 1 - c_beg) & 1) * STAGE, ra, na);   // past the end: zeros, never read
             __syncthreads();
+            if (++c >= c_end) break;
+            load_chunk(c + 2, ra, na);
+            compute(lds + ((c - c_beg) & 1) * STAGE);
+            store_chunk(lds + ((c + 1 - c_beg) & 1) * STAGE, rb, nbr);
+            __syncthreads();
+            if (++c >= c_end) break;
         }
     }
 
@@ -236,6 +284,179 @@ __global__ void __launch_bounds__(256, 2) wgrad_kernel(Geom geo, GradArgs ga) {
             for (int r = 0; r < 16; ++r) {
                 const int i = i0 + WM * wm + 32 * a + 8 * (r >> 2) + 4 * hi + (r & 3);
                 if (i < geo.C_out && k < geo.K) Pz[(int64_t)i * geo.K + k] = ga.scales[i] * acc[a][b][r];
+            }
+        }
+}
+
+// Eight values moved one position along the row: out[e] = in[e + 1] with nb
+// entering at the top (up), or out[e] = in[e - 1] with nb entering at the
+// bottom (down).
+__device__ __forceinline__ u32x4 shift_up(const u32x4& v, uint32_t nb) {
+    return u32x4{__builtin_amdgcn_alignbyte(v[1], v[0], 2), __builtin_amdgcn_alignbyte(v[2], v[1], 2),
+                 __builtin_amdgcn_alignbyte(v[3], v[2], 2), __builtin_amdgcn_alignbyte(nb, v[3], 2)};
+}
+__device__ __forceinline__ u32x4 shift_down(const u32x4& v, uint32_t nb) {
+    return u32x4{__builtin_amdgcn_alignbyte(v[0], nb << 16, 2), __builtin_amdgcn_alignbyte(v[1], v[0], 2),
+                 __builtin_amdgcn_alignbyte(v[2], v[1], 2), __builtin_amdgcn_alignbyte(v[3], v[2], 2)};
+}
+
+// Convolution weight gradient with both operands streamed into LDS by
+// direct-to-LDS loads.  Needs stride 1, same padding, OW dividing 64 and
+// OH * OW a multiple of 64, so that a 64-token chunk is whole output rows of
+// one image.  Column (c, r, q) of the im2col matrix is input row r of channel
+// c shifted by q - pad along each output row; the shift moves onto dY:
+//     sum_n dY[i][n] * x[c][oh + r - pad][ow + q - pad]
+//   = sum_m dYq[i][(oh, m)] * x[c][oh + r - pad][m],
+// with dYq[i][(oh, m)] = dY[i][(oh, m - q + pad)] and zero past the row ends.
+// LDS then holds unshifted spans -- 64 tokens of dY row i, and of input rows
+// (c, r) -- and the q variants of every dY fragment are built in registers
+// from the fragment and its two neighbouring values.  Rows are 128 bytes with
+// the 16-byte pieces XOR-swizzled by the row index (conflict-free fragment
+// reads); three stages keep two chunks of loads in flight.
+template <int KIND, int DT, int BM, int BNP>
+__global__ void __launch_bounds__(256, 2) wgrad_conv_dma_kernel(Geom geo, GradArgs ga, const uint8_t* zero) {
+    constexpr int KQ = KIND == 1 ? 3 : 1;        // kernel columns: variants of dY
+    constexpr int KR = KIND == 1 ? 3 : 1;        // kernel rows
+    constexpr int PAD = KIND == 1 ? 1 : 0;
+    constexpr int WM = BM / 2, WN = BNP / 2, AM = WM / 32, AN = WN / 32;
+    constexpr int ROWS = BM + BNP;
+    constexpr int STAGE = ROWS * 128;
+    constexpr int NST = 3;
+    constexpr int LOADS = ROWS / 32;             // 16-byte loads per thread per chunk
+    static_assert(ROWS % 32 == 0, "rows per stage");
+    __shared__ __attribute__((aligned(16))) uint8_t lds[NST * STAGE];
+
+    const int total = ga.S * ga.tiles_m * ga.tiles_n;
+    const int per_xcd = (total + 7) / 8;
+    const int w = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+    if (w >= total) return;
+    const int tn = w % ga.tiles_n;
+    const int tm = (w / ga.tiles_n) % ga.tiles_m;
+    const int z = w / (ga.tiles_n * ga.tiles_m);
+    const int i0 = tm * BM, p0 = tn * BNP;
+    const int c_beg = z * ga.cps, c_end = min(ga.nchunk, c_beg + ga.cps);
+    const int nch = max(0, c_end - c_beg);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int P = geo.OH * geo.OW;
+    const int npairs = geo.cin * KR;
+    const uint8_t* dyb = reinterpret_cast<const uint8_t*>(ga.dY);
+    const uint8_t* xb = reinterpret_cast<const uint8_t*>(ga.X);
+
+    // this lane's slot in every load: row (8 g + lane / 8), logical piece pc
+    const int lrow = lane >> 3;
+    const int lpc = (lane & 7) ^ lrow;
+    auto issue = [&](int chunk, uint8_t* st) {
+        const int n0 = chunk * 64;
+        const int b = n0 / P;
+        const int pb = n0 - b * P;
+        const int t = 8 * lpc;                   // token of the piece within the chunk
+        const int oh = pb / geo.OW + t / geo.OW, ow = t % geo.OW;
+#pragma unroll
+        for (int j = 0; j < LOADS; ++j) {
+            const int grp = wave + 4 * j;
+            const int row = 8 * grp + lrow;
+            const uint8_t* src = zero;
+            if (8 * grp < BM) {
+                const int i = i0 + row;
+                if (i < geo.C_out) src = dyb + ((int64_t)(b * geo.C_out + i) * P + pb + t) * 2;
+            } else {
+                const int pr = p0 + row - BM;
+                const int c = pr / KR, r = pr - c * KR;
+                const int ih = oh + r - PAD;
+                if (pr < npairs && ih >= 0 && ih < geo.H)
+                    src = xb + ((int64_t)(b * geo.cin + c) * geo.H * geo.W + ih * geo.W + ow) * 2;
+            }
+            lds_dma16(src, st + grp * 1024);
+        }
+    };
+
+    // neighbour masks: the piece starts (ends) an output row
+    bool lft_ok[4], rgt_ok[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const int pc = 2 * s + hi;
+        lft_ok[s] = (8 * pc) % geo.OW != 0;
+        rgt_ok[s] = (8 * pc + 8) % geo.OW != 0;
+    }
+
+    floatx16 acc[KQ][AM][AN];
+#pragma unroll
+    for (int q = 0; q < KQ; ++q)
+#pragma unroll
+        for (int a = 0; a < AM; ++a)
+#pragma unroll
+            for (int b = 0; b < AN; ++b)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[q][a][b][r] = 0.0f;
+
+    auto compute = [&](const uint8_t* st) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            const int pc = 2 * s + hi;
+            u32x4 av[KQ][AM], bf[AN];
+#pragma unroll
+            for (int a = 0; a < AM; ++a) {
+                const int row = WM * wm + 32 * a + l32;
+                const uint8_t* rp = st + row * 128;
+                const u32x4 v = *reinterpret_cast<const u32x4*>(rp + ((pc ^ (row & 7)) << 4));
+                if constexpr (KQ == 3) {
+                    const uint32_t left = lft_ok[s] ? *reinterpret_cast<const uint16_t*>(
+                                                          rp + ((((pc - 1) & 7) ^ (row & 7)) << 4) + 14)
+                                                    : 0u;
+                    const uint32_t right =
+                        rgt_ok[s] ? *reinterpret_cast<const uint16_t*>(rp + ((((pc + 1) & 7) ^ (row & 7)) << 4)) : 0u;
+                    av[0][a] = shift_up(v, right);     // q = 0: dY[m + 1]
+                    av[1][a] = v;                      // q = 1
+                    av[2][a] = shift_down(v, left);    // q = 2: dY[m - 1]
+                } else {
+                    av[0][a] = v;
+                }
+            }
+#pragma unroll
+            for (int b = 0; b < AN; ++b) {
+                const int row = BM + WN * wn + 32 * b + l32;
+                bf[b] = *reinterpret_cast<const u32x4*>(st + row * 128 + ((pc ^ (row & 7)) << 4));
+            }
+#pragma unroll
+            for (int q = 0; q < KQ; ++q)
+#pragma unroll
+                for (int a = 0; a < AM; ++a)
+#pragma unroll
+                    for (int b = 0; b < AN; ++b) acc[q][a][b] = mfma_grad<DT>(av[q][a], bf[b], acc[q][a][b]);
+        }
+    };
+
+    auto stg = [&](int c) { return lds + (c % NST) * STAGE; };
+    if (nch > 0) issue(c_beg, stg(0));
+    if (nch > 1) issue(c_beg + 1, stg(1));
+    if (nch > 1) wait_vmcnt<LOADS>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    for (int t = 0; t < nch; ++t) {
+        if (t + 2 < nch) issue(c_beg + t + 2, stg(t + 2));
+        compute(stg(t));
+        if (t + 2 < nch) wait_vmcnt<LOADS>();    // chunk t + 1 landed
+        else wait_vmcnt<0>();
+        lds_barrier();
+    }
+
+    float* Pz = ga.P + (int64_t)z * geo.C_out * geo.K;
+#pragma unroll
+    for (int a = 0; a < AM; ++a)
+#pragma unroll
+        for (int b = 0; b < AN; ++b) {
+            const int pr = p0 + WN * wn + 32 * b + l32;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int i = i0 + WM * wm + 32 * a + 8 * (r >> 2) + 4 * hi + (r & 3);
+                if (i < geo.C_out && pr < npairs) {
+                    const float sc = ga.scales[i];
+#pragma unroll
+                    for (int q = 0; q < KQ; ++q) Pz[(int64_t)i * geo.K + pr * KQ + q] = sc * acc[q][a][b][r];
+                }
             }
         }
 }
@@ -290,12 +511,48 @@ __global__ void __launch_bounds__(256) cbgrad_gather_kernel(const float* __restr
     }
 }
 
+// Sum of the S partial weight gradients into the first, in split order
+// (streaming; float4 per thread when every slice starts 16-byte aligned).
+__global__ void __launch_bounds__(256) split_sum_kernel(float* __restrict__ P, int64_t slice, int S) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (slice % 4 == 0) {
+        for (int64_t i = t0; i < slice / 4; i += stride) {
+            floatx4 a = reinterpret_cast<const floatx4*>(P)[i];
+            for (int s = 1; s < S; ++s) a += reinterpret_cast<const floatx4*>(P + s * slice)[i];
+            reinterpret_cast<floatx4*>(P)[i] = a;
+        }
+    } else {
+        for (int64_t i = t0; i < slice; i += stride) {
+            float a = P[i];
+            for (int s = 1; s < S; ++s) a += P[s * slice + i];
+            P[i] = a;
+        }
+    }
+}
+
 template <int KIND, int DT, int BM, int BN>
 hipError_t wgrad_launch(const Geom& geo, const GradArgs& ga, hipStream_t st) {
     const int total = ga.S * ga.tiles_m * ga.tiles_n;
     const unsigned grid = (unsigned)(8 * ((total + 7) / 8));
     wgrad_kernel<KIND, DT, BM, BN><<<grid, 256, 0, st>>>(geo, ga);
     return hipGetLastError();
+}
+
+template <int KIND, int DT, int BM, int BNP>
+hipError_t wgrad_dma_launch(const Geom& geo, const GradArgs& ga, const uint8_t* zero, hipStream_t st) {
+    const int total = ga.S * ga.tiles_m * ga.tiles_n;
+    const unsigned grid = (unsigned)(8 * ((total + 7) / 8));
+    wgrad_conv_dma_kernel<KIND, DT, BM, BNP><<<grid, 256, 0, st>>>(geo, ga, zero);
+    return hipGetLastError();
+}
+
+template <int KIND, int DT>
+hipError_t wgrad_dma_dispatch(const Geom& geo, const GradPlan& gp, const GradArgs& ga, const uint8_t* zero,
+                              hipStream_t st) {
+    if (gp.bm == 128 && gp.bn == 64) return wgrad_dma_launch<KIND, DT, 128, 64>(geo, ga, zero, st);
+    if (gp.bm == 64 && gp.bn == 64) return wgrad_dma_launch<KIND, DT, 64, 64>(geo, ga, zero, st);
+    return hipErrorInvalidConfiguration;
 }
 
 template <int KIND, int DT>
@@ -308,27 +565,62 @@ hipError_t wgrad_dispatch(const Geom& geo, const GradPlan& gp, const GradArgs& g
 
 }  // namespace
 
+// Convolutions whose 64-token chunks are whole output rows of one image take
+// the direct-to-LDS kernel.
+static bool grad_dma_ok(const Geom& geo) {
+    if (!geo.conv || geo.stride != 1 || geo.OW != geo.W || geo.OH != geo.H || geo.W % 8 != 0) return false;
+    if (64 % geo.OW != 0 || ((int64_t)geo.OH * geo.OW) % 64 != 0) return false;
+    if (const char* e = std::getenv("AQ_GRAD_DMA")) return std::atoi(e) != 0;
+    return true;
+}
+
 // Tile and split choice: the largest tile that still gives about one
-// workgroup per CU, then token splits up to about two workgroups per CU.
+// workgroup per CU, then token splits up to about four workgroups per CU
+// while the partial gradients stay within 32 MiB (each split adds a full
+// C_out x K fp32 partial to write and to sum).
 GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens) {
     GradPlan gp{};
-    const int shapes[3][2] = {{128, 128}, {64, 128}, {64, 64}};
-    int pick = 2;
-    for (int s = 0; s < 3; ++s) {
-        const int64_t tiles = (int64_t)((geo.C_out + shapes[s][0] - 1) / shapes[s][0]) *
-                              ((geo.K + shapes[s][1] - 1) / shapes[s][1]);
-        if (tiles >= 240) {
-            pick = s;
-            break;
+    gp.dma = grad_dma_ok(geo);
+    int want_bm = 0, want_bn = 0;
+    if (const char* e = std::getenv("AQ_GRAD_TILE")) std::sscanf(e, "%dx%d", &want_bm, &want_bn);
+    if (gp.dma) {
+        // rows of C_out x (input channel, kernel row) pairs
+        // 64 x 64 measured faster than 128 x 64 on every layer shape here (more
+        // workgroups per CU hide the load latency better)
+        const int npairs = geo.cin * (geo.kh == 3 ? 3 : 1);
+        gp.bm = want_bm == 128 ? 128 : 64;
+        gp.bn = 64;
+        gp.tiles_m = (geo.C_out + gp.bm - 1) / gp.bm;
+        gp.tiles_n = (npairs + gp.bn - 1) / gp.bn;
+    } else {
+        const int shapes[3][2] = {{128, 128}, {64, 128}, {64, 64}};
+        int pick = 2;
+        for (int s = 0; s < 3; ++s) {
+            if (want_bm) {
+                if (shapes[s][0] == want_bm && shapes[s][1] == want_bn) {
+                    pick = s;
+                    break;
+                }
+                continue;
+            }
+            const int64_t tiles = (int64_t)((geo.C_out + shapes[s][0] - 1) / shapes[s][0]) *
+                                  ((geo.K + shapes[s][1] - 1) / shapes[s][1]);
+            if (tiles >= 240) {
+                pick = s;
+                break;
+            }
         }
+        gp.bm = shapes[pick][0];
+        gp.bn = shapes[pick][1];
+        gp.tiles_m = (geo.C_out + gp.bm - 1) / gp.bm;
+        gp.tiles_n = (geo.K + gp.bn - 1) / gp.bn;
     }
-    gp.bm = shapes[pick][0];
-    gp.bn = shapes[pick][1];
-    gp.tiles_m = (geo.C_out + gp.bm - 1) / gp.bm;
-    gp.tiles_n = (geo.K + gp.bn - 1) / gp.bn;
     const int64_t tiles = (int64_t)gp.tiles_m * gp.tiles_n;
     const int64_t nchunk = std::max<int64_t>(1, (max_tokens + kGradChunk - 1) / kGradChunk);
-    gp.s_max = (int)std::min<int64_t>({16, nchunk, std::max<int64_t>(1, (480 + tiles - 1) / tiles)});
+    const int64_t slice = (int64_t)geo.C_out * geo.K * 4;
+    gp.s_max = (int)std::min<int64_t>({16, nchunk, std::max<int64_t>(1, (960 + tiles - 1) / tiles),
+                                       std::max<int64_t>(1, (int64_t(32) << 20) / slice)});
+    if (const char* e = std::getenv("AQ_GRAD_SPLITS")) gp.s_max = (int)std::min<int64_t>({16, nchunk, std::max(1, std::atoi(e))});
     return gp;
 }
 
@@ -339,7 +631,7 @@ int grad_kind(const Geom& geo) {
 
 hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, const void* X, const void* dY,
                                 const float* scales, float* P, const int32_t* offs, const int32_t* ent, float* dC,
-                                int splits_override, hipStream_t st) {
+                                const void* zero, int splits_override, hipStream_t st) {
     GradArgs ga;
     ga.X = static_cast<const uint16_t*>(X);
     ga.dY = static_cast<const uint16_t*>(dY);
@@ -354,7 +646,13 @@ hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, 
     ga.tiles_n = gp.tiles_n;
     const int kind = grad_kind(geo);
     hipError_t e;
-    if (dtype == AQ_BF16) {
+    const uint8_t* z16 = static_cast<const uint8_t*>(zero);
+    if (gp.dma) {
+        e = kind == 1 ? (dtype == AQ_BF16 ? wgrad_dma_dispatch<1, AQ_BF16>(geo, gp, ga, z16, st)
+                                          : wgrad_dma_dispatch<1, AQ_F16>(geo, gp, ga, z16, st))
+                      : (dtype == AQ_BF16 ? wgrad_dma_dispatch<2, AQ_BF16>(geo, gp, ga, z16, st)
+                                          : wgrad_dma_dispatch<2, AQ_F16>(geo, gp, ga, z16, st));
+    } else if (dtype == AQ_BF16) {
         e = kind == 0 ? wgrad_dispatch<0, AQ_BF16>(geo, gp, ga, st)
             : kind == 1 ? wgrad_dispatch<1, AQ_BF16>(geo, gp, ga, st)
                         : wgrad_dispatch<2, AQ_BF16>(geo, gp, ga, st);
@@ -364,17 +662,27 @@ hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, 
                         : wgrad_dispatch<2, AQ_F16>(geo, gp, ga, st);
     }
     if (e != hipSuccess) return e;
+    const int64_t slice = (int64_t)geo.C_out * geo.K;
+    int S_gather = ga.S;
+    if (ga.S > 1) {
+        // the gather visits every (row, group) once per codebook: sum the splits first
+        const int64_t n4 = std::max<int64_t>(1, slice / 4);
+        const unsigned grid = (unsigned)std::min<int64_t>((n4 + 255) / 256, 4096);
+        split_sum_kernel<<<grid, 256, 0, st>>>(P, slice, ga.S);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        S_gather = 1;
+    }
     const int nk = 1 << geo.B;
     const int64_t buckets = (int64_t)geo.M * nk;
     const int64_t nent = (int64_t)geo.C_out * geo.G;
-    const int64_t slice = (int64_t)geo.C_out * geo.K;
     // a wave per entry when lists are short (large codebooks), a workgroup otherwise
     if (nent / nk < 64) {
-        cbgrad_gather_kernel<64><<<(unsigned)((buckets + 3) / 4), 256, 0, st>>>(P, slice, ga.S, offs, ent, nent, nk,
-                                                                               geo.M, geo.g, dC);
+        cbgrad_gather_kernel<64><<<(unsigned)((buckets + 3) / 4), 256, 0, st>>>(P, slice, S_gather, offs, ent, nent,
+                                                                               nk, geo.M, geo.g, dC);
     } else {
-        cbgrad_gather_kernel<256><<<(unsigned)buckets, 256, 0, st>>>(P, slice, ga.S, offs, ent, nent, nk, geo.M, geo.g,
-                                                                     dC);
+        cbgrad_gather_kernel<256><<<(unsigned)buckets, 256, 0, st>>>(P, slice, S_gather, offs, ent, nent, nk, geo.M,
+                                                                     geo.g, dC);
     }
     return hipGetLastError();
 }

@@ -125,7 +125,8 @@ hipError_t launch_f32_forward(const Geom& geo, const DeviceWeights& w, const voi
 // ---- codebook gradient ----
 
 struct GradPlan {
-    int bm, bn;                   // weight-gradient tile: output channels x inputs
+    bool dma;                     // convolution kernel with direct-to-LDS staging
+    int bm, bn;                   // weight-gradient tile: output channels x inputs (x (channel, kernel row) pairs)
     int tiles_m, tiles_n;
     int s_max;                    // most token splits (partial buffers in the workspace)
 };
@@ -134,7 +135,7 @@ GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens);
 // X, dY: fp16 or bf16 (dtype); P: [s_max][C_out][K] fp32 workspace; offs / ent: the code index
 hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, const void* X, const void* dY,
                                 const float* scales, float* P, const int32_t* offs, const int32_t* ent, float* dC,
-                                int splits_override, hipStream_t st);
+                                const void* zero, int splits_override, hipStream_t st);
 void build_code_index(const void* codes, int B, int C_out, int G, int M, std::vector<int32_t>& offs,
                       std::vector<int32_t>& ent);
 

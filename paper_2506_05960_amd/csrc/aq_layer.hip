@@ -637,6 +637,11 @@ aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int
     }
     if ((int64_t)geo.C_out * geo.G >= (int64_t(1) << 31))
         return fail(AQ_ERR_UNSUPPORTED, "too many code groups for the 32-bit code index");
+    // the weight-gradient kernel addresses X and dY with 32-bit byte offsets
+    const int64_t lim = int64_t(1) << 31;
+    const int64_t xbytes = geo.conv ? n * geo.cin * (int64_t)geo.H * geo.W * 2 : geo.tokens * geo.K * 2;
+    if (xbytes >= lim || geo.tokens * geo.C_out * 2 >= lim)
+        return fail(AQ_ERR_UNSUPPORTED, "X or dY of 2 GiB or more: beyond the codebook-gradient kernel's offsets");
     if (!L->grad_ready) {
         // one-time preparation: synchronous and allocating
         const size_t ncodes = (size_t)geo.C_out * geo.G * geo.M;
@@ -651,6 +656,10 @@ aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int
         if (s == AQ_OK)
             s = dev_upload(&L->d_gpart, nullptr, (size_t)L->gplan.s_max * geo.C_out * geo.K * sizeof(float),
                            "gradient workspace");
+        if (s == AQ_OK && !L->d_zero) {
+            s = dev_upload(&L->d_zero, nullptr, 256, "zero block");
+            if (s == AQ_OK && (e = hipMemset(L->d_zero, 0, 256)) != hipSuccess) s = hip_fail(e, "zero block");
+        }
         if (s != AQ_OK) {
             for (void** p : {(void**)&L->d_gidx_offs, (void**)&L->d_gidx_ent, (void**)&L->d_gpart})
                 if (*p) {
@@ -665,7 +674,7 @@ aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int
     if (const char* sv = std::getenv("AQ_GRAD_SPLITS")) splits = std::atoi(sv);
     const hipError_t e =
         aq::launch_codebook_grad(geo, L->gplan, dtype, X, dY, L->d_scales, L->d_gpart, L->d_gidx_offs, L->d_gidx_ent,
-                                 dC, splits, static_cast<hipStream_t>(stream));
+                                 dC, L->d_zero, splits, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "codebook gradient launch");
     return AQ_OK;
 }

@@ -38,25 +38,6 @@ struct GemmArgs {
 
 constexpr int kGemmStages = 3;
 
-__device__ __forceinline__ void lds_dma16(const uint8_t* src, uint8_t* dst_wave_base) {
-    __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)src,
-                                     (__attribute__((address_space(3))) void*)dst_wave_base, 16, 0, 0);
-}
-
-// s_waitcnt with vmcnt <= n (n < 64), expcnt and lgkmcnt unrestricted (gfx9 encoding)
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt field");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// Workgroup barrier without the release fence of __syncthreads(): that fence
-// waits for every outstanding vector-memory operation, which would also drain
-// the direct-to-LDS prefetches of later chunks. LDS reads issued before the
-// barrier are drained here; the DMA writes are awaited by wait_vmcnt.
-__device__ __forceinline__ void lds_barrier() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
 
 template <int KIND, int XT, int BM, int BN>
 __global__ void __launch_bounds__(256, 1)

@@ -101,6 +101,10 @@ CASES = [
     (_conv("conv3_g9_kaq", 24, 64, 8, 8, 3, 9, 2, 8, 2), "f16"),
     (_conv("conv3_bf16", 16, 80, 8, 24, 3, 8, 1, 10, 1), "bf16"),
     (_conv("conv3_b16", 32, 64, 4, 8, 3, 8, 1, 16, 2), "f16"),
+    # 64-token chunks that are whole output rows (the direct-to-LDS kernel)
+    (_conv("conv3_w16", 24, 72, 8, 16, 3, 8, 2, 8, 2), "f16"),
+    (_conv("conv3_w32_bf16", 16, 136, 4, 32, 3, 8, 2, 7, 3), "bf16"),
+    (_conv("conv3_w64", 8, 40, 3, 64, 3, 8, 1, 9, 1), "f16"),
     # 1x1 convolutions
     (_conv("conv1", 64, 96, 8, 8, 1, 8, 2, 8, 3), "f16"),
     (_conv("conv1_g16", 128, 40, 4, 16, 1, 16, 4, 6, 2), "bf16"),
@@ -119,7 +123,10 @@ def test_codebook_grad_matches_oracle(spec, dt):
     assert err <= TOL, err
 
 
-@pytest.mark.parametrize("spec,dt", [CASES[1], CASES[9], CASES[13]], ids=["lin", "conv3", "conv1"])
+SPLIT_CASES = [c for c in CASES if c[0].name in ("lin_tiles", "conv3_tiles", "conv3_w16", "conv1")]
+
+
+@pytest.mark.parametrize("spec,dt", SPLIT_CASES, ids=[c[0].name for c in SPLIT_CASES])
 def test_token_splits_agree(spec, dt):
     """One split and the planner's split count give the same gradient within the bar."""
     _say(f"[grad splits] {spec.name}")
@@ -129,6 +136,36 @@ def test_token_splits_agree(spec, dt):
     b = _grad(spec, inp, gi, dt)
     ref = _ref(spec, inp, gi, dt)
     assert O.rel_err_inf(a, ref) <= TOL
+    assert O.rel_err_inf(b, ref) <= TOL
+
+
+def _grad_env(spec, inp, gi, dt, **env):
+    old = {k: os.environ.get(k) for k in env}
+    os.environ.update({k: str(v) for k, v in env.items()})
+    try:
+        return _grad(spec, inp, gi, dt)
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+
+
+DMA_CASES = [c for c in CASES if c[0].name in ("conv3_small", "conv3_g9_kaq", "conv3_w16", "conv1", "conv1_g16")]
+
+
+@pytest.mark.parametrize("spec,dt", DMA_CASES, ids=[c[0].name for c in DMA_CASES])
+def test_direct_to_lds_and_register_staged_kernels_agree(spec, dt):
+    """Convolutions eligible for the direct-to-LDS kernel, also run through the register-staged one."""
+    _say(f"[grad dma vs regs] {spec.name}")
+    inp = generate(spec, 46)
+    gi = generate_grad_inputs(spec, 47, dt)
+    ref = _ref(spec, inp, gi, dt)
+    for tile in ("64x64", "128x64"):
+        a = _grad_env(spec, inp, gi, dt, AQ_GRAD_TILE=tile)
+        assert O.rel_err_inf(a, ref) <= TOL, tile
+    b = _grad_env(spec, inp, gi, dt, AQ_GRAD_DMA=0)
     assert O.rel_err_inf(b, ref) <= TOL
 
 
