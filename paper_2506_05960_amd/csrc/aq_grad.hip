@@ -461,6 +461,143 @@ __global__ void __launch_bounds__(256, 2) wgrad_conv_dma_kernel(Geom geo, GradAr
         }
 }
 
+// Linear weight gradient with both operands streamed into LDS by
+// direct-to-LDS loads, untransposed: a chunk is 64 tokens x 64 channels of dY
+// and 64 tokens x 64 inputs of X, each row 128 bytes (one token), so the
+// reduction dimension (tokens) is the slow one in LDS.  The MFMA fragments
+// come out with the gfx950 transpose read ds_read_b64_tr_b16: within each
+// group of 16 lanes, lane l receives element l % 4 of the 8-byte rows
+// addressed by lanes 4f + l / 4 (f = 0..3).  So lane 16 g + 4 f + q addresses
+// the four channels 16 (g % 2) + 4 q .. + 3 at token 8 (g / 2) + f, and
+// lane l obtains channel l % 32 at tokens 8 (l / 32) + 0..3 -- half of its
+// fragment; a second read 4 tokens on gives the other half.  The 16-byte
+// pieces of a row are XOR-swizzled with 4 * ((token / 2) % 2), which spreads
+// the 32 lanes of a half-wave over all banks.
+__device__ __forceinline__ int lin_swz(int n) { return ((n >> 1) & 1) << 2; }
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Four transpose reads at LDS byte addresses, completed before returning.
+// Written as one asm block: through the builtin the compiler orders every
+// such read after all outstanding direct-to-LDS loads (it cannot tell the
+// addresses apart), which would drain the prefetched chunks.  The loads of
+// the chunk read here were awaited explicitly before the barrier.
+__device__ __forceinline__ void tr_read4(u32x2& a0, u32x2& a1, u32x2& b0, u32x2& b1, uint32_t pa0, uint32_t pa1,
+                                         uint32_t pb0, uint32_t pb1) {
+    asm volatile(
+        "ds_read_b64_tr_b16 %0, %4\n\t"
+        "ds_read_b64_tr_b16 %1, %5\n\t"
+        "ds_read_b64_tr_b16 %2, %6\n\t"
+        "ds_read_b64_tr_b16 %3, %7\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(a0), "=&v"(a1), "=&v"(b0), "=&v"(b1)
+        : "v"(pa0), "v"(pa1), "v"(pb0), "v"(pb1)
+        : "memory");
+}
+
+template <int DT>
+__global__ void __launch_bounds__(256, 2) wgrad_linear_dma_kernel(Geom geo, GradArgs ga, const uint8_t* zero) {
+    constexpr int BM = 64, BN = 64;
+    constexpr int STAGE = 64 * 128 * 2;          // A then B: 64 tokens x 128 bytes each
+    constexpr int NST = 3;
+    constexpr int LOADS = 4;                     // 16-byte loads per thread per chunk
+    __shared__ __attribute__((aligned(16))) uint8_t lds[NST * STAGE];
+
+    const int total = ga.S * ga.tiles_m * ga.tiles_n;
+    const int per_xcd = (total + 7) / 8;
+    const int w = (int)(blockIdx.x % 8) * per_xcd + (int)(blockIdx.x / 8);
+    if (w >= total) return;
+    const int tn = w % ga.tiles_n;
+    const int tm = (w / ga.tiles_n) % ga.tiles_m;
+    const int z = w / (ga.tiles_n * ga.tiles_m);
+    const int i0 = tm * BM, k0 = tn * BN;
+    const int c_beg = z * ga.cps, c_end = min(ga.nchunk, c_beg + ga.cps);
+    const int nch = max(0, c_end - c_beg);
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int64_t N = geo.tokens;
+    const uint8_t* dyb = reinterpret_cast<const uint8_t*>(ga.dY);
+    const uint8_t* xb = reinterpret_cast<const uint8_t*>(ga.X);
+
+    // load slot of this lane: row 8 * grp + lane / 8 of a region, slot piece lane % 8
+    const int lrow = lane >> 3;
+    auto issue = [&](int chunk, uint8_t* st) {
+        const int64_t n0 = (int64_t)chunk * 64;
+#pragma unroll
+        for (int j = 0; j < LOADS; ++j) {
+            const int grp = wave + 4 * j;        // 0..7: dY rows, 8..15: X rows
+            const int row = 8 * (grp & 7) + lrow;
+            const int pc = (lane & 7) ^ lin_swz(row);
+            const int64_t n = n0 + row;
+            const uint8_t* src = zero;
+            if (grp < 8) {
+                const int i = i0 + 8 * pc;
+                if (n < N && i < geo.C_out) src = dyb + (n * geo.C_out + i) * 2;
+            } else {
+                const int k = k0 + 8 * pc;
+                if (n < N && k < geo.K) src = xb + (n * geo.K + k) * 2;
+            }
+            lds_dma16(src, st + grp * 1024);
+        }
+    };
+
+    // transpose-read addresses (bytes within a stage) for every step and half:
+    // lane 16 g + 4 f + q reads channels (inputs) c .. c + 3, c = 16 (g % 2) + 4 q
+    // of the wave's 32-wide block, at token 16 s + 8 (g / 2) + 4 h + f
+    const int g16 = lane >> 4, j16 = lane & 15;
+    const int fo = j16 >> 2, qo = j16 & 3;
+    int offa[4][2], offb[4][2];
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int n = 16 * s + 8 * (g16 >> 1) + 4 * h + fo;
+            const int ca = 32 * wm + 16 * (g16 & 1) + 4 * qo;
+            const int cb = 32 * wn + 16 * (g16 & 1) + 4 * qo;
+            offa[s][h] = n * 128 + (((ca >> 3) ^ lin_swz(n)) << 4) + (ca & 7) * 2;
+            offb[s][h] = 64 * 128 + n * 128 + (((cb >> 3) ^ lin_swz(n)) << 4) + (cb & 7) * 2;
+        }
+
+    floatx16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.0f;
+
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)lds;
+    auto compute = [&](int stage) {
+        const uint32_t st = lds0 + stage * STAGE;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            u32x2 a0, a1, b0, b1;
+            tr_read4(a0, a1, b0, b1, st + offa[s][0], st + offa[s][1], st + offb[s][0], st + offb[s][1]);
+            acc = mfma_grad<DT>(u32x4{a0[0], a0[1], a1[0], a1[1]}, u32x4{b0[0], b0[1], b1[0], b1[1]}, acc);
+        }
+    };
+
+    auto stg = [&](int c) { return lds + (c % NST) * STAGE; };
+    if (nch > 0) issue(c_beg, stg(0));
+    if (nch > 1) issue(c_beg + 1, stg(1));
+    if (nch > 1) wait_vmcnt<LOADS>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    for (int t = 0; t < nch; ++t) {
+        if (t + 2 < nch) issue(c_beg + t + 2, stg(t + 2));
+        compute(t % NST);
+        if (t + 2 < nch) wait_vmcnt<LOADS>();
+        else wait_vmcnt<0>();
+        lds_barrier();
+    }
+
+    float* Pz = ga.P + (int64_t)z * geo.C_out * geo.K;
+    const int k = k0 + 32 * wn + l32;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        const int i = i0 + 32 * wm + 8 * (r >> 2) + 4 * hi + (r & 3);
+        if (i < geo.C_out && k < geo.K) Pz[(int64_t)i * geo.K + k] = ga.scales[i] * acc[r];
+    }
+}
+
 // One group of LPB lanes per codebook entry (m, k); lanes split into
 // LPB / g entry slots times g positions t.  Each slot sums its entries in
 // list order, then lane t adds the slots in order.
@@ -565,13 +702,14 @@ hipError_t wgrad_dispatch(const Geom& geo, const GradPlan& gp, const GradArgs& g
 
 }  // namespace
 
-// Convolutions whose 64-token chunks are whole output rows of one image take
-// the direct-to-LDS kernel.
+// Linear layers, and convolutions whose 64-token chunks are whole output rows
+// of one image, take the direct-to-LDS kernels.
 static bool grad_dma_ok(const Geom& geo) {
-    if (!geo.conv || geo.stride != 1 || geo.OW != geo.W || geo.OH != geo.H || geo.W % 8 != 0) return false;
-    if (64 % geo.OW != 0 || ((int64_t)geo.OH * geo.OW) % 64 != 0) return false;
-    if (const char* e = std::getenv("AQ_GRAD_DMA")) return std::atoi(e) != 0;
-    return true;
+    if (const char* e = std::getenv("AQ_GRAD_DMA"))
+        if (std::atoi(e) == 0) return false;
+    if (!geo.conv) return true;                  // linear: C_out and K are multiples of 8
+    if (geo.stride != 1 || geo.OW != geo.W || geo.OH != geo.H || geo.W % 8 != 0) return false;
+    return 64 % geo.OW == 0 && ((int64_t)geo.OH * geo.OW) % 64 == 0;
 }
 
 // Tile and split choice: the largest tile that still gives about one
@@ -583,10 +721,14 @@ GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens) {
     gp.dma = grad_dma_ok(geo);
     int want_bm = 0, want_bn = 0;
     if (const char* e = std::getenv("AQ_GRAD_TILE")) std::sscanf(e, "%dx%d", &want_bm, &want_bn);
-    if (gp.dma) {
-        // rows of C_out x (input channel, kernel row) pairs
-        // 64 x 64 measured faster than 128 x 64 on every layer shape here (more
-        // workgroups per CU hide the load latency better)
+    if (gp.dma && !geo.conv) {
+        gp.bm = gp.bn = 64;
+        gp.tiles_m = (geo.C_out + 63) / 64;
+        gp.tiles_n = (geo.K + 63) / 64;
+    } else if (gp.dma) {
+        // rows of C_out x (input channel, kernel row) pairs; 64 x 64 measured
+        // faster than 128 x 64 on every layer shape here (more workgroups per
+        // CU hide the load latency better)
         const int npairs = geo.cin * (geo.kh == 3 ? 3 : 1);
         gp.bm = want_bm == 128 ? 128 : 64;
         gp.bn = 64;
@@ -647,7 +789,14 @@ hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, 
     const int kind = grad_kind(geo);
     hipError_t e;
     const uint8_t* z16 = static_cast<const uint8_t*>(zero);
-    if (gp.dma) {
+    if (gp.dma && kind == 0) {
+        const unsigned grid = (unsigned)(8 * ((ga.S * ga.tiles_m * ga.tiles_n + 7) / 8));
+        if (dtype == AQ_BF16)
+            wgrad_linear_dma_kernel<AQ_BF16><<<grid, 256, 0, st>>>(geo, ga, z16);
+        else
+            wgrad_linear_dma_kernel<AQ_F16><<<grid, 256, 0, st>>>(geo, ga, z16);
+        e = hipGetLastError();
+    } else if (gp.dma) {
         e = kind == 1 ? (dtype == AQ_BF16 ? wgrad_dma_dispatch<1, AQ_BF16>(geo, gp, ga, z16, st)
                                           : wgrad_dma_dispatch<1, AQ_F16>(geo, gp, ga, z16, st))
                       : (dtype == AQ_BF16 ? wgrad_dma_dispatch<2, AQ_BF16>(geo, gp, ga, z16, st)

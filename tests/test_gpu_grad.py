@@ -152,12 +152,13 @@ def _grad_env(spec, inp, gi, dt, **env):
                 os.environ[k] = v
 
 
-DMA_CASES = [c for c in CASES if c[0].name in ("conv3_small", "conv3_g9_kaq", "conv3_w16", "conv1", "conv1_g16")]
+DMA_CASES = [c for c in CASES if c[0].name in ("lin_small", "lin_tiles", "lin_bf16", "lin_one_token", "conv3_small",
+                                                "conv3_g9_kaq", "conv3_w16", "conv1", "conv1_g16")]
 
 
 @pytest.mark.parametrize("spec,dt", DMA_CASES, ids=[c[0].name for c in DMA_CASES])
 def test_direct_to_lds_and_register_staged_kernels_agree(spec, dt):
-    """Convolutions eligible for the direct-to-LDS kernel, also run through the register-staged one."""
+    """Layers eligible for the direct-to-LDS kernels, also run through the register-staged ones."""
     _say(f"[grad dma vs regs] {spec.name}")
     inp = generate(spec, 46)
     gi = generate_grad_inputs(spec, 47, dt)
