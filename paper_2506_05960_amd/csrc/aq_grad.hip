@@ -619,9 +619,14 @@ __global__ void __launch_bounds__(256) cbgrad_gather_kernel(const float* __restr
         const int m = (int)(bucket / nk), k = (int)(bucket - (int64_t)m * nk);
         const int32_t beg = offs[(int64_t)m * (nk + 1) + k], end = offs[(int64_t)m * (nk + 1) + k + 1];
         const int32_t* list = ent + (int64_t)m * nent;
+        // four entries per step, all loads issued before any add (branch-free
+        // buffer loads; an entry past the list reads zero): short lists, as a
+        // large codebook has, finish in one step
+        const __amdgpu_buffer_rsrc_t lr = buffer_rsrc(list, (uint64_t)nent * 4);
+        const __amdgpu_buffer_rsrc_t pr = buffer_rsrc(P, (uint64_t)S * slice * 4);
+        const uint32_t sstride = (uint32_t)(slice * 4);
         int32_t idx = beg + e;
-        // four entries per step keep several independent loads in flight
-        for (; idx + 3 * EP < end; idx += 4 * EP) {
+        for (; idx + 3 * EP < end; idx += 4 * EP) {     // whole steps: no bounds checks
             int64_t base[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) base[u] = (int64_t)list[idx + u * EP] * g + t;
@@ -632,11 +637,22 @@ __global__ void __launch_bounds__(256) cbgrad_gather_kernel(const float* __restr
 #pragma unroll
             for (int u = 0; u < 4; ++u) acc += v[u];
         }
-        for (; idx < end; idx += EP) {
-            const int64_t base = (int64_t)list[idx] * g + t;
-            float v = 0.0f;
-            for (int s = 0; s < S; ++s) v += P[s * slice + base];
-            acc += v;
+        if (idx < end) {                                  // the last, partial step
+            uint32_t boff[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int32_t iu = idx + u * EP;
+                const int32_t p = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(
+                    lr, iu < end ? (uint32_t)iu * 4u : kOutOfRange, 0, 0);
+                boff[u] = iu < end ? (uint32_t)(p * g + t) * 4u : kOutOfRange;
+            }
+            float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+            for (int s = 0; s < S; ++s)
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    v[u] += __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(pr, boff[u] + s * sstride, 0, 0));
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc += v[u];
         }
     }
     red[tid] = acc;

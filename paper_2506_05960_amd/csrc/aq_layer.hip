@@ -642,6 +642,8 @@ aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int
     const int64_t xbytes = geo.conv ? n * geo.cin * (int64_t)geo.H * geo.W * 2 : geo.tokens * geo.K * 2;
     if (xbytes >= lim || geo.tokens * geo.C_out * 2 >= lim)
         return fail(AQ_ERR_UNSUPPORTED, "X or dY of 2 GiB or more: beyond the codebook-gradient kernel's offsets");
+    if ((int64_t)geo.C_out * geo.K * 4 * 16 >= lim)
+        return fail(AQ_ERR_UNSUPPORTED, "C_out * K too large for the codebook-gradient workspace offsets");
     if (!L->grad_ready) {
         // one-time preparation: synchronous and allocating
         const size_t ncodes = (size_t)geo.C_out * geo.G * geo.M;
