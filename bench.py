@@ -299,6 +299,10 @@ def grad_bench(a, torch, P, W):
     reps = (a.steps + per_graph - 1) // per_graph
     us = _graph_time_us(torch, lambda: layer.codebook_grad(x, dy, out=dC), per_graph, trials=reps)
     ms = us * 1e-3
+    if a.copy_bytes > 0:
+        src = torch.empty(a.copy_bytes, dtype=torch.uint8, device="cuda")
+        torch.empty_like(src).copy_(src)
+        torch.cuda.synchronize()
     flops = spec.dense_flops
     tflops = flops / (ms * 1e-3) / 1e12
     out = {
