@@ -48,6 +48,10 @@ __device__ __forceinline__ void wave_sync() {
     asm volatile("" ::: "memory");
 }
 
+// Cache-policy operand of the raw buffer loads (plain loads).
+using kPlainLoadT = std::integral_constant<int, 0>;
+constexpr kPlainLoadT kPlainLoad{};
+
 __device__ __forceinline__ floatx16 mfma_f16(const u32x4& a, const u32x4& b, const floatx16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c, 0, 0,
                                                   0);
@@ -83,25 +87,35 @@ struct GroupRaw {
     u32x4 w[DEC == FUSED_DEC_F32L ? 2 * MC : MC];
 };
 
-// Issue the codebook reads of one group.  `ent` holds the group's M codes.
-// The LDS codebook keeps 256 rows per codebook (rows past 2^B unused), so
-// codebook m starts at a fixed byte offset and a codeword address is a shift.
+// Code i of a lane's packed record words (8- or 16-bit codes, little-endian).
+// Extracted with shifts: reading the 32-bit words through a 16-bit pointer
+// would break type-based aliasing, and the compiler then reuses stale codes.
+template <typename EntT>
+__device__ __forceinline__ uint32_t code_at(const uint32_t* dw, int i) {
+    if constexpr (sizeof(EntT) == 1) return (dw[i >> 2] >> (8 * (i & 3))) & 0xFFu;
+    else return (dw[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+}
+
+// Issue the codebook reads of one group, whose M codes are codes i0 .. i0+M-1
+// of the record words `dw`.  The LDS codebook keeps 256 rows per codebook
+// (rows past 2^B unused), so codebook m starts at a fixed byte offset and a
+// codeword address is a shift.
 template <int DEC, int MC, typename EntT>
-__device__ __forceinline__ void gather_group(GroupRaw<DEC, MC>& g, const EntT* ent, const uint8_t* cb_lds,
+__device__ __forceinline__ void gather_group(GroupRaw<DEC, MC>& g, const uint32_t* dw, int i0, const uint8_t* cb_lds,
                                              const void* cb_glob) {
     if constexpr (DEC == FUSED_DEC_T16G) {
-        g.w[0] = static_cast<const u32x4*>(cb_glob)[ent[0]];
+        g.w[0] = static_cast<const u32x4*>(cb_glob)[code_at<EntT>(dw, i0)];
     } else if constexpr (DEC == FUSED_DEC_F32L) {
 #pragma unroll
         for (int m = 0; m < MC; ++m) {
-            const u32x4* p = reinterpret_cast<const u32x4*>(cb_lds + m * 256 * 32 + (uint32_t)ent[m] * 32u);
+            const u32x4* p = reinterpret_cast<const u32x4*>(cb_lds + m * 256 * 32 + code_at<EntT>(dw, i0 + m) * 32u);
             g.w[2 * m] = p[0];
             g.w[2 * m + 1] = p[1];
         }
     } else {
 #pragma unroll
         for (int m = 0; m < MC; ++m)
-            g.w[m] = *reinterpret_cast<const u32x4*>(cb_lds + m * 256 * 16 + (uint32_t)ent[m] * 16u);
+            g.w[m] = *reinterpret_cast<const u32x4*>(cb_lds + m * 256 * 16 + code_at<EntT>(dw, i0 + m) * 16u);
     }
 }
 
@@ -311,25 +325,29 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                                  : (uint64_t)geo.tokens * geo.K * XB;
     const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(X, xbytes);
     uint32_t stage[UPL][SREG];
-    auto stage_load = [&](int chunk) {
+    // Chunks past the last one read zeros (no branch, so the compiler's wait
+    // counts stay exact across the prefetch).
+    auto stage_load = [&](int chunk, auto aux_c) {
+        constexpr int AUX = decltype(aux_c)::value;
+        const bool cv = chunk < plan.nchunk;
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
             if constexpr (CONV) {
                 // 8 channels x 2 pixels
-                const uint32_t base = g_ok[j] ? (g_off[j] + (uint32_t)(chunk * 16 * CM) * HW) * 2u : kOutOfRange;
+                const uint32_t base = g_ok[j] && cv ? (g_off[j] + (uint32_t)(chunk * 16 * CM) * HW) * 2u : kOutOfRange;
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    stage[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, 0);
+                    stage[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, AUX);
             } else {
                 const int k = chunk * 16 * CM + k_first[j];
-                const bool ok = g_ok[j] && k < geo.K;
+                const bool ok = g_ok[j] && cv && k < geo.K;
                 const uint32_t off = ok ? (g_off[j] + (uint32_t)(chunk * 16 * CM)) * XB : kOutOfRange;
                 if constexpr (XT == AQ_I8) {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 0);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, AUX);
                     stage[j][0] = v[0];
                     stage[j][1] = v[1];
                 } else {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, AUX);
                     stage[j][0] = v[0]; stage[j][1] = v[1]; stage[j][2] = v[2]; stage[j][3] = v[3];
                 }
             }
@@ -364,66 +382,32 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // pre-decoded mode: operand record (chunk, step, channel, lane half), 16 bytes each
     const __amdgpu_buffer_rsrc_t wr = buffer_rsrc(crec, (uint64_t)plan.nchunk * NS * geo.C_out * 32u);
     uint32_t crg[AN][REC_DW];
-    auto codes_load = [&](int chunk) {
+    auto codes_load = [&](int chunk, auto aux_c) {
+        constexpr int AUX = decltype(aux_c)::value;
         if constexpr (DEC == FUSED_DEC_REC) return;
+        const bool cv = chunk < plan.nchunk;
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
-            const uint32_t off = c_ok[b] ? c_off[b] + (uint32_t)chunk * chunk_rec_stride : kOutOfRange;
+            const uint32_t off = c_ok[b] && cv ? c_off[b] + (uint32_t)chunk * chunk_rec_stride : kOutOfRange;
 #pragma unroll
             for (int d = 0; d < REC_DW; d += 4) {
                 if constexpr (true) {
                     if (d + 4 <= REC_DW) {
-                        const auto v = __builtin_amdgcn_raw_buffer_load_b128(cr, off + 4 * d, 0, 0);
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b128(cr, off + 4 * d, 0, AUX);
                         crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2]; crg[b][d + 3] = v[3];
                     } else if (d + 3 == REC_DW) {
-                        const auto v = __builtin_amdgcn_raw_buffer_load_b96(cr, off + 4 * d, 0, 0);
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b96(cr, off + 4 * d, 0, AUX);
                         crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2];
                     } else if (d + 2 == REC_DW) {
-                        const auto v = __builtin_amdgcn_raw_buffer_load_b64(cr, off + 4 * d, 0, 0);
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b64(cr, off + 4 * d, 0, AUX);
                         crg[b][d] = v[0]; crg[b][d + 1] = v[1];
                     } else {
-                        crg[b][d] = __builtin_amdgcn_raw_buffer_load_b32(cr, off + 4 * d, 0, 0);
+                        crg[b][d] = __builtin_amdgcn_raw_buffer_load_b32(cr, off + 4 * d, 0, AUX);
                     }
                 }
             }
         }
     };
-
-    // scales of this thread's epilogue task (one task per thread for every tile used)
-    constexpr int EROWS = CONV ? BN : BM, ECOLS = CONV ? BM : BN;
-    float esc[8];
-    float exs[4];
-    {
-        const int task = tid;
-        const int c8 = (task / (EROWS / 4)) * 8;
-        const int rq = task - (task / (EROWS / 4)) * (EROWS / 4);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) esc[i] = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) exs[e] = 1.0f;
-        if (task < (EROWS / 4) * (ECOLS / 8)) {
-            if constexpr (CONV) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int co = N0 + 4 * rq + e;
-                    esc[e] = co < geo.C_out ? scales[co] : 0.0f;
-                }
-            } else {
-#pragma unroll
-                for (int c = 0; c < 8; ++c) {
-                    const int co = N0 + c8 + c;
-                    esc[c] = co < geo.C_out ? scales[co] : 0.0f;
-                }
-                if (x_scales) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int tok = T0 + 4 * rq + e;
-                        exs[e] = tok < tokens ? x_scales[tok] : 1.0f;
-                    }
-                }
-            }
-        }
-    }
 
     floatx16 acc[AM][AN];
 #pragma unroll
@@ -447,7 +431,6 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L && NS * MC <= 18;
     // weights of one 32-channel block of a chunk, decoded into MFMA operands
     auto decode_block = [&](const uint32_t* codes_dw, int dchunk, int db, u32x4 (&d)[NS]) {
-        const EntT* ev = reinterpret_cast<const EntT*>(codes_dw);
         if constexpr (DEC == FUSED_DEC_REC) {
             const bool ok = c_ok[db] && dchunk < plan.nchunk;
             const uint32_t base = (uint32_t)(((dchunk * NS) * geo.C_out + N0 + 32 * db + l32) * 2 + q) * 16u;
@@ -458,14 +441,14 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         } else if constexpr (LOOKAHEAD) {
             GroupRaw<DEC, MC> raw[NS];
 #pragma unroll
-            for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], ev + g * MC, cb_lds, cb);
+            for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], codes_dw, g * MC, cb_lds, cb);
 #pragma unroll
             for (int g = 0; g < NS; ++g) d[g] = combine_group<DEC, MC>(raw[g]);
         } else {
             GroupRaw<DEC, MC> raw1;
 #pragma unroll
             for (int g = 0; g < NS; ++g) {
-                gather_group<DEC, MC, EntT>(raw1, ev + g * MC, cb_lds, cb);
+                gather_group<DEC, MC, EntT>(raw1, codes_dw, g * MC, cb_lds, cb);
                 d[g] = combine_group<DEC, MC>(raw1);
             }
         }
@@ -476,24 +459,60 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // its staging store, so a chunk starts with its operands in flight.  The
     // look-ahead is used when a block of raw codewords (groups x M x 16 bytes
     // per lane) fits in 72 registers.
+    // Prologue.  The loads go out in the order they are needed (codebook, codes,
+    // activations, scales); the codebook store and the first block's decode
+    // wait only for the first two, so the decode runs while the activations
+    // are still in flight.  The scales are branch-free buffer loads (zero past
+    // the end) that nothing waits for before the epilogue.
     int chunk = wave;
     u32x4 af[NS][AM];
     u32x4 dec[NS];
-    if (chunk < plan.nchunk) {
-        stage_load(chunk);
-        codes_load(chunk);
+    codes_load(chunk, kPlainLoad);
+    stage_load(chunk, kPlainLoad);
+    __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their uses
+    // scales of this thread's epilogue task (one task per thread for every tile used)
+    constexpr int EROWS = CONV ? BN : BM, ECOLS = CONV ? BM : BN;
+    float esc[8];
+    float exs[4];
+    const bool has_xs = !CONV && x_scales != nullptr;
+    {
+        const __amdgpu_buffer_rsrc_t sr = buffer_rsrc(scales, (uint64_t)geo.C_out * 4u);
+        const __amdgpu_buffer_rsrc_t xsr = buffer_rsrc(x_scales, has_xs ? (uint64_t)geo.tokens * 4u : 0u);
+        const int task = tid;
+        const bool tok_task = task < (EROWS / 4) * (ECOLS / 8);
+        const int c8 = (task / (EROWS / 4)) * 8;
+        const int rq = task - (task / (EROWS / 4)) * (EROWS / 4);
+        if constexpr (CONV) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                esc[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    sr, tok_task ? (uint32_t)(N0 + 4 * rq + e) * 4u : kOutOfRange, 0, 0));
+#pragma unroll
+            for (int e = 4; e < 8; ++e) esc[e] = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) exs[e] = 0.0f;
+        } else {
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+                esc[c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    sr, tok_task ? (uint32_t)(N0 + c8 + c) * 4u : kOutOfRange, 0, 0));
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                exs[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    xsr, tok_task && has_xs ? (uint32_t)(T0 + 4 * rq + e) * 4u : kOutOfRange, 0, 0));
+        }
     }
     if constexpr (CB_LDS) {
 #pragma unroll
         for (int i = 0; i < CB_PER_T; ++i) reinterpret_cast<u32x4*>(cb_lds)[tid + 256 * i] = cbr[i];
     }
-    __syncthreads();   // codebook and padding visible
-    if (chunk < plan.nchunk) {
-        stage_store(pbuf0);
-        wave_sync();
-        load_af(pbuf0, af);
-        if constexpr (LOOKAHEAD) decode_block(crg[0], chunk, 0, dec);
-    }
+    lds_barrier();   // codebook and padding visible (global loads stay in flight)
+    // A wave without a chunk runs this on zeros, in its own staging buffer;
+    // no branch here keeps the loads above from being sunk below the barrier.
+    if constexpr (LOOKAHEAD) decode_block(crg[0], chunk, 0, dec);
+    stage_store(pbuf0);
+    wave_sync();
+    load_af(pbuf0, af);
     int it = 0;
     for (; chunk < plan.nchunk; chunk += kWaves, ++it) {
         uint8_t* nxt = (it & 1) ? pbuf0 : pbuf1;
@@ -503,10 +522,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         for (int b = 0; b < AN; ++b)
 #pragma unroll
             for (int d = 0; d < REC_DW; ++d) crn[b][d] = crg[b][d];
-        if (more) {
-            stage_load(chunk + kWaves);   // next chunk's activations and codes
-            codes_load(chunk + kWaves);
-        }
+        codes_load(chunk + kWaves, kPlainLoad);   // next chunk's codes and activations (zeros past the end)
+        stage_load(chunk + kWaves, kPlainLoad);
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
             __builtin_amdgcn_sched_barrier(0);
@@ -630,7 +647,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                 } else {
                     yi0 = (T0 + 4 * rq + e) * geo.C_out + col0;
 #pragma unroll
-                    for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[c] * exs[e];
+                    for (int c = 0; c < 8; ++c) o[c] = v[c][e] * esc[c] * (has_xs ? exs[e] : 1.0f);
                 }
                 if (y_dtype == AQ_F32) {
                     __builtin_amdgcn_raw_buffer_store_b128(
@@ -658,7 +675,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                         o = v[c][e] * esc[e];
                     } else {
                         yi = (T0 + 4 * rq + e) * geo.C_out + col0 + c;
-                        o = v[c][e] * esc[c] * exs[e];
+                        o = v[c][e] * esc[c] * (has_xs ? exs[e] : 1.0f);
                     }
                     if (y_dtype == AQ_F32) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(o), yr, yi * 4, 0, 0);
                     else __builtin_amdgcn_raw_buffer_store_b16(f32_to_f16(o), yr, yi * 2, 0, 0);

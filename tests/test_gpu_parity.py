@@ -242,6 +242,10 @@ FUSED = [
     LayerSpec(name="f_lin_i8", C_out=200, K=136, g=8, M=4, B=8, n=45, x_dtype="i8"),
     LayerSpec(name="f_lin_b16", C_out=96, K=512, g=8, M=1, B=16, n=300),
     LayerSpec(name="f_lin_f32y", C_out=64, K=64, g=8, M=2, B=8, n=1000, y_dtype="f32"),
+    # several chunks per wave: the next chunk's codes are decoded while the
+    # current chunk's products run (16-bit codes once read stale codes there)
+    LayerSpec(name="f_conv3_b16_k", C_out=48, K=128 * 9, g=8, M=1, B=16, n=2, conv=ConvGeom(128, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="f_lin_m4_k", C_out=64, K=1024, g=8, M=4, B=8, n=70),
 ]
 
 
