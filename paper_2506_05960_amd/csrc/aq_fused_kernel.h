@@ -522,8 +522,10 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         for (int b = 0; b < AN; ++b)
 #pragma unroll
             for (int d = 0; d < REC_DW; ++d) crn[b][d] = crg[b][d];
-        codes_load(chunk + kWaves, kPlainLoad);   // next chunk's codes and activations (zeros past the end)
-        stage_load(chunk + kWaves, kPlainLoad);
+        if (more) {
+            stage_load(chunk + kWaves, kPlainLoad);   // next chunk's activations and codes
+            codes_load(chunk + kWaves, kPlainLoad);
+        }
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
             __builtin_amdgcn_sched_barrier(0);

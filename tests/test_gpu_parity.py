@@ -380,6 +380,20 @@ def test_fused_tiles(tile, monkeypatch):
         assert err <= 2e-3
 
 
+@pytest.mark.parametrize("rec", ["0", "1"])
+@pytest.mark.parametrize("tile", ["64x64", "32x128"])
+def test_fused_linear_int8_tiles(tile, rec, monkeypatch):
+    """int8 activations, M = 4, several chunks per wave and a ragged token tail, in both weight modes."""
+    monkeypatch.setenv("AQ_FUSED_TILE", tile)
+    monkeypatch.setenv("AQ_FUSED_REC", rec)
+    spec = LayerSpec(name="t_lin_i8", C_out=136, K=640, g=8, M=4, B=8, n=300, x_dtype="i8")
+    inp = generate(spec, 17)
+    y = _run(spec, inp, "decode")
+    err = O.rel_err_inf(y, O.forward(spec, inp))
+    _say(f"tile {tile} rec={rec} {spec.name} err={err:.3e}")
+    assert err <= 2e-3
+
+
 # ---------------------------------------------------------------------------
 # exact checks through the fused path
 # ---------------------------------------------------------------------------
