@@ -157,6 +157,66 @@ operand_records_kernel(const void* __restrict__ cb, const CodeT* __restrict__ co
     }
 }
 
+// Same records for fp16 codebooks with g = 8 and M in {1, 2, 4}: a codeword is
+// one 16-byte load, the M codewords of a group are summed with packed fp16
+// adds in ascending m (the same IEEE fp16 sums as above), and every load of a
+// thread is issued before any sum.
+template <typename CodeT, bool K3, int MC>
+__global__ void __launch_bounds__(256)
+operand_records_f16_kernel(const u32x4* __restrict__ cb, const CodeT* __restrict__ codes, u32x4* __restrict__ rec,
+                           int nchunk, int C_out, int Gn, int B) {
+    constexpr int ns = K3 ? 9 : 4;
+    constexpr int NG = K3 ? 9 : 4;                 // groups a thread decodes
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // (chunk, channel, half)
+    if (idx >= (int64_t)nchunk * C_out * 2) return;
+    const int c = (int)(idx / (2 * C_out));
+    const int rem = (int)(idx - (int64_t)c * 2 * C_out);
+    const int n = rem >> 1, q = rem & 1;
+    const uint32_t rows = 1u << B;
+    const int j0 = K3 ? (16 * c + 8 * q) * 9 / 8 : 0;
+    uint32_t code[NG][MC];
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+        const int j = K3 ? j0 + s : c * 2 * ns + 2 * s + q;
+        const int jc = j < Gn ? j : Gn - 1;       // groups past the end of K are zeroed below
+#pragma unroll
+        for (int m = 0; m < MC; ++m) code[s][m] = codes[((int64_t)n * Gn + jc) * MC + m];
+    }
+    u32x4 w[NG][MC];
+#pragma unroll
+    for (int s = 0; s < NG; ++s)
+#pragma unroll
+        for (int m = 0; m < MC; ++m) w[s][m] = cb[m * rows + code[s][m]];
+    u32x4 g[NG];
+#pragma unroll
+    for (int s = 0; s < NG; ++s) {
+        const int j = K3 ? j0 + s : c * 2 * ns + 2 * s + q;
+        g[s] = w[s][0];
+#pragma unroll
+        for (int m = 1; m < MC; ++m)
+#pragma unroll
+            for (int d = 0; d < 4; ++d) g[s][d] = add_f16x2(g[s][d], w[s][m][d]);
+        if (j >= Gn) g[s] = u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int s = 0; s < ns; ++s) {
+        u32x4 o;
+        if constexpr (K3) {
+            // position s of channel e (of the lane's 8) is weight 9e + s of the run
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+                const int v0 = 9 * (2 * d) + s, v1 = 9 * (2 * d + 1) + s;
+                const uint32_t lo = (g[v0 >> 3][(v0 & 7) >> 1] >> (16 * (v0 & 1))) & 0xFFFFu;
+                const uint32_t hi = (g[v1 >> 3][(v1 & 7) >> 1] >> (16 * (v1 & 1))) & 0xFFFFu;
+                o[d] = lo | (hi << 16);
+            }
+        } else {
+            o = g[s];
+        }
+        rec[(((int64_t)c * ns + s) * C_out + n) * 2 + q] = o;
+    }
+}
+
 size_t operand_record_bytes(const Geom& geo, const FusedPlan& plan) {
     const int ns = plan.kind == 1 ? 9 : plan.cm;
     return (size_t)plan.nchunk * ns * geo.C_out * 2 * 16;
@@ -171,6 +231,22 @@ static hipError_t records_dispatch(const Geom& geo, const FusedPlan& plan, const
     u32x4* r = static_cast<u32x4*>(rec);
     if (plan.kind != 1 && plan.cm != 4) return hipErrorInvalidConfiguration;
     if (geo.g != 8 && !(geo.g == 9 && plan.kind == 1)) return hipErrorInvalidConfiguration;
+    if (w.cb_dtype == AQ_F16 && geo.g == 8 && (geo.M == 1 || geo.M == 2 || geo.M == 4)) {
+        const u32x4* cb = static_cast<const u32x4*>(w.codebooks);
+#define AQ_REC16(K3, MC) \
+    operand_records_f16_kernel<CodeT, K3, MC><<<grid, block, 0, st>>>(cb, codes, r, plan.nchunk, geo.C_out, geo.G, geo.B)
+        if (plan.kind == 1) {
+            if (geo.M == 1) AQ_REC16(true, 1);
+            else if (geo.M == 2) AQ_REC16(true, 2);
+            else AQ_REC16(true, 4);
+        } else {
+            if (geo.M == 1) AQ_REC16(false, 1);
+            else if (geo.M == 2) AQ_REC16(false, 2);
+            else AQ_REC16(false, 4);
+        }
+#undef AQ_REC16
+        return hipGetLastError();
+    }
 #define AQ_REC(CBT)                                                                                             \
     if (plan.kind == 1 && geo.g == 9)                                                                          \
         operand_records_kernel<CBT, CodeT, true, 9><<<grid, block, 0, st>>>(w.codebooks, codes, r, plan.nchunk, \

@@ -23,6 +23,13 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uin
 }
 constexpr uint32_t kOutOfRange = 0x80000000u;   // byte offset past every buffer the kernels read
 
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+
+// Two IEEE fp16 additions (round to nearest even) on packed halves.
+__device__ __forceinline__ uint32_t add_f16x2(uint32_t a, uint32_t b) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, a) + __builtin_bit_cast(half2v, b));
+}
+
 // ---- direct-to-LDS loads ----
 
 // 16 bytes from global memory into LDS: lane l of the wave writes slot

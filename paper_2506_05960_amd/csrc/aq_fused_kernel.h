@@ -57,12 +57,6 @@ __device__ __forceinline__ floatx16 mfma_f16(const u32x4& a, const u32x4& b, con
                                                   0);
 }
 
-typedef _Float16 half2v __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ uint32_t add_f16x2(uint32_t a, uint32_t b) {
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, a) + __builtin_bit_cast(half2v, b));
-}
-
 // Dword made of fp16 half `hlo` of xlo (low half) and half `hhi` of xhi (high half).
 __device__ __forceinline__ uint32_t pick2(uint32_t xlo, int hlo, uint32_t xhi, int hhi) {
     const uint32_t sel = (uint32_t)(2 * hlo) | ((uint32_t)(2 * hlo + 1) << 8) | ((uint32_t)(4 + 2 * hhi) << 16) |
