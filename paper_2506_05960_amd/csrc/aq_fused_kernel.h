@@ -168,9 +168,11 @@ __device__ __forceinline__ u32x4 i8x8_to_f16(uint64_t q) {
     return r;
 }
 
-// KIND: 0 linear, 1 conv 3x3, 2 conv 1x1.
-template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL>
-__global__ void __launch_bounds__(256, 1)
+// KIND: 0 linear, 1 conv 3x3, 2 conv 1x1.  OCC: waves per SIMD the register
+// budget is sized for (2 lets two workgroups share a compute unit, so one's
+// prologue and epilogue overlap the other's main loop).
+template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL, int OCC = 1>
+__global__ void __launch_bounds__(256, OCC)
 fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const uint8_t* __restrict__ crec,
                  const float* __restrict__ scales, const void* __restrict__ X, const float* __restrict__ x_scales,
                  void* __restrict__ Y, int y_dtype) {
@@ -680,9 +682,9 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     }
 }
 
-template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL>
+template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL, int OCC = 1>
 static hipError_t fused_launch_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
-    auto kern = fused_fwd_kernel<KIND, CM, XT, DEC, MC, BM, BN, UPL>;
+    auto kern = fused_fwd_kernel<KIND, CM, XT, DEC, MC, BM, BN, UPL, OCC>;
     static size_t attr_bytes = 0;
     if (plan.lds_bytes > attr_bytes) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,

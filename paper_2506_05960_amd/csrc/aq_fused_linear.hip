@@ -8,7 +8,13 @@ static hipError_t lin_tiles(const Geom& geo, const FusedPlan& p, const FusedLaun
 #define AQ_TILE(TBM, TBN, TUPL) \
     if (p.bm == TBM && p.bn == TBN && p.upl == TUPL) return fused_launch_cfg<0, 4, XT, DEC, MC, TBM, TBN, TUPL>(geo, p, fl);
     AQ_TILE(64, 96, 8)
-    AQ_TILE(64, 64, 8)
+    if (p.bm == 64 && p.bn == 64 && p.upl == 8) {
+        // pre-decoded operands: two workgroups per compute unit (the tile fits 256
+        // registers per lane); with the in-loop decode they would share the LDS
+        // gather throughput, which measured slower
+        constexpr int occ = DEC == FUSED_DEC_REC ? 2 : 1;
+        return fused_launch_cfg<0, 4, XT, DEC, MC, 64, 64, 8, occ>(geo, p, fl);
+    }
     AQ_TILE(32, 128, 4)
     AQ_TILE(32, 64, 4)
 #undef AQ_TILE
