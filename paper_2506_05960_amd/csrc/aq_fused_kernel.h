@@ -405,13 +405,19 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         }
     };
 
+    // Accumulators start in matrix-core (AGPR) registers: the empty asm pins the
+    // register class of the zero start value, so the loop-carried values stay
+    // there instead of being copied from VGPRs before every block of products.
     floatx16 acc[AM][AN];
 #pragma unroll
     for (int a = 0; a < AM; ++a)
 #pragma unroll
-        for (int b = 0; b < AN; ++b)
+        for (int b = 0; b < AN; ++b) {
+            floatx16 z;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+            for (int r = 0; r < 16; ++r) z[r] = 0.0f;
+            asm volatile("" : "=a"(acc[a][b]) : "0"(z));
+        }
 
     // activation fragments of one chunk: every (step, token block)
     auto load_af = [&](const uint8_t* buf, u32x4 (&af)[NS][AM]) {
@@ -456,48 +462,15 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // look-ahead is used when a block of raw codewords (groups x M x 16 bytes
     // per lane) fits in 72 registers.
     // Prologue.  The loads go out in the order they are needed (codebook, codes,
-    // activations, scales); the codebook store and the first block's decode
-    // wait only for the first two, so the decode runs while the activations
-    // are still in flight.  The scales are branch-free buffer loads (zero past
-    // the end) that nothing waits for before the epilogue.
+    // activations); the codebook store and the first block's decode wait only
+    // for the first two, so the decode runs while the activations are still in
+    // flight.
     int chunk = wave;
     u32x4 af[NS][AM];
     u32x4 dec[NS];
     codes_load(chunk, kPlainLoad);
     stage_load(chunk, kPlainLoad);
     __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their uses
-    // scales of this thread's epilogue task (one task per thread for every tile used)
-    constexpr int EROWS = CONV ? BN : BM, ECOLS = CONV ? BM : BN;
-    float esc[8];
-    float exs[4];
-    const bool has_xs = !CONV && x_scales != nullptr;
-    {
-        const __amdgpu_buffer_rsrc_t sr = buffer_rsrc(scales, (uint64_t)geo.C_out * 4u);
-        const __amdgpu_buffer_rsrc_t xsr = buffer_rsrc(x_scales, has_xs ? (uint64_t)geo.tokens * 4u : 0u);
-        const int task = tid;
-        const bool tok_task = task < (EROWS / 4) * (ECOLS / 8);
-        const int c8 = (task / (EROWS / 4)) * 8;
-        const int rq = task - (task / (EROWS / 4)) * (EROWS / 4);
-        if constexpr (CONV) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                esc[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                    sr, tok_task ? (uint32_t)(N0 + 4 * rq + e) * 4u : kOutOfRange, 0, 0));
-#pragma unroll
-            for (int e = 4; e < 8; ++e) esc[e] = 0.0f;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) exs[e] = 0.0f;
-        } else {
-#pragma unroll
-            for (int c = 0; c < 8; ++c)
-                esc[c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                    sr, tok_task ? (uint32_t)(N0 + c8 + c) * 4u : kOutOfRange, 0, 0));
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                exs[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
-                    xsr, tok_task && has_xs ? (uint32_t)(T0 + 4 * rq + e) * 4u : kOutOfRange, 0, 0));
-        }
-    }
     if constexpr (CB_LDS) {
 #pragma unroll
         for (int i = 0; i < CB_PER_T; ++i) reinterpret_cast<u32x4*>(cb_lds)[tid + 256 * i] = cbr[i];
@@ -596,6 +569,41 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                 red[(wave * (ROWS / 4) + row0 / 4) * COLSP + col] =
                     floatx4{acc[a][b][4 * i], acc[a][b][4 * i + 1], acc[a][b][4 * i + 2], acc[a][b][4 * i + 3]};
             }
+    // Scales of this thread's epilogue task (one task per thread for every tile
+    // used), loaded only once the accumulators are in LDS: live any earlier,
+    // they push the accumulators out of the matrix-core registers (measured
+    // on the linear kernels).  The partial-tile reads below hide their latency.
+    constexpr int EROWS = CONV ? BN : BM, ECOLS = CONV ? BM : BN;
+    float esc[8];
+    float exs[4];
+    const bool has_xs = !CONV && x_scales != nullptr;
+    {
+        const __amdgpu_buffer_rsrc_t sr = buffer_rsrc(scales, (uint64_t)geo.C_out * 4u);
+        const __amdgpu_buffer_rsrc_t xsr = buffer_rsrc(x_scales, has_xs ? (uint64_t)geo.tokens * 4u : 0u);
+        const int task = tid;
+        const bool tok_task = task < (EROWS / 4) * (ECOLS / 8);
+        const int c8 = (task / (EROWS / 4)) * 8;
+        const int rq = task - (task / (EROWS / 4)) * (EROWS / 4);
+        if constexpr (CONV) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                esc[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    sr, tok_task ? (uint32_t)(N0 + 4 * rq + e) * 4u : kOutOfRange, 0, 0));
+#pragma unroll
+            for (int e = 4; e < 8; ++e) esc[e] = 0.0f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) exs[e] = 0.0f;
+        } else {
+#pragma unroll
+            for (int c = 0; c < 8; ++c)
+                esc[c] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    sr, tok_task ? (uint32_t)(N0 + c8 + c) * 4u : kOutOfRange, 0, 0));
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                exs[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(
+                    xsr, tok_task && has_xs ? (uint32_t)(T0 + 4 * rq + e) * 4u : kOutOfRange, 0, 0));
+        }
+    }
     __syncthreads();
     const int ybytes = y_dtype == AQ_F32 ? 4 : 2;
     const __amdgpu_buffer_rsrc_t yr = buffer_rsrc(Y, (uint64_t)geo.tokens * geo.C_out * ybytes);
