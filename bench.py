@@ -401,42 +401,55 @@ def main(argv=None):
         layer.forward(x, xs, out=y)
     torch.cuda.synchronize()
 
-    # The forward allocates nothing and issues no memset, so a run of steps can
-    # be captured once in a HIP graph and replayed: the timed region then
-    # measures the GPU, not Python's per-launch overhead.
-    per_graph = 1 if a.no_graph else max(1, min(a.steps, 50))
-    graph = None
-    if not a.no_graph:
+    # The forward allocates nothing and issues no memset, so runs of steps can
+    # be captured in HIP graphs and replayed: the timed region then measures
+    # the GPU, not Python's per-launch overhead.  Exactly a.steps steps are
+    # timed: a graph of up to 50 forwards replayed a.steps // 50 times, then
+    # one graph of the remaining a.steps % 50.
+    per_graph = max(1, min(a.steps, 50))
+    nfull, tail = divmod(a.steps, per_graph)
+
+    def capture(n):
         stream = torch.cuda.Stream()
         stream.wait_stream(torch.cuda.current_stream())
-        graph = torch.cuda.CUDAGraph()
+        g = torch.cuda.CUDAGraph()
         with torch.cuda.stream(stream):
-            with torch.cuda.graph(graph, stream=stream):
-                for _ in range(per_graph):
+            with torch.cuda.graph(g, stream=stream):
+                for _ in range(n):
                     layer.forward(x, xs, out=y)
         torch.cuda.current_stream().wait_stream(stream)
-        graph.replay()
+        g.replay()
         torch.cuda.synchronize()
-    reps = (a.steps + per_graph - 1) // per_graph
-    steps = reps * per_graph
+        return g
+
+    graph = tail_graph = None
+    if not a.no_graph:
+        graph = capture(per_graph)
+        if tail:
+            tail_graph = capture(tail)
+    steps = a.steps
 
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
-    for _ in range(reps):
-        if graph is not None:
+    if graph is not None:
+        for _ in range(nfull):
             graph.replay()
-        else:
+        if tail_graph is not None:
+            tail_graph.replay()
+    else:
+        for _ in range(steps):
             layer.forward(x, xs, out=y)
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / steps
 
-    # Every decode-path forward is one kernel launch, and graph replay leaves
-    # next to no gap between launches (rocprofv3's kernel trace of this same
-    # command agrees within a few percent), so the per-step time is the
-    # dominant kernel's average duration.  A LUT forward is two launches
-    # (table+gather, then the chunk reduction): its figure covers both.
+    # A decode-path forward with the in-loop decode is one kernel launch, and
+    # graph replay leaves next to no gap between launches (rocprofv3's kernel
+    # trace of this same command agrees within a few percent), so the per-step
+    # time is that kernel's average duration.  A pre-decoded forward is two
+    # launches (operand records, then the product), and a LUT forward is two
+    # (table+gather, then the chunk reduction): their figure covers both.
     kms = ms
     flops = spec.dense_flops
     tflops = flops / (ms * 1e-3) / 1e12
