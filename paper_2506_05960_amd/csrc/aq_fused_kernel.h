@@ -48,10 +48,6 @@ __device__ __forceinline__ void wave_sync() {
     asm volatile("" ::: "memory");
 }
 
-// Cache-policy operand of the raw buffer loads (plain loads).
-using kPlainLoadT = std::integral_constant<int, 0>;
-constexpr kPlainLoadT kPlainLoad{};
-
 __device__ __forceinline__ floatx16 mfma_f16(const u32x4& a, const u32x4& b, const floatx16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(half8, a), __builtin_bit_cast(half8, b), c, 0, 0,
                                                   0);
@@ -323,8 +319,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     uint32_t stage[UPL][SREG];
     // Chunks past the last one read zeros (no branch, so the compiler's wait
     // counts stay exact across the prefetch).
-    auto stage_load = [&](int chunk, auto aux_c) {
-        constexpr int AUX = decltype(aux_c)::value;
+    auto stage_load = [&](int chunk) {
         const bool cv = chunk < plan.nchunk;
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
@@ -333,17 +328,17 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                 const uint32_t base = g_ok[j] && cv ? (g_off[j] + (uint32_t)(chunk * 16 * CM) * HW) * 2u : kOutOfRange;
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    stage[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, AUX);
+                    stage[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, 0);
             } else {
                 const int k = chunk * 16 * CM + k_first[j];
                 const bool ok = g_ok[j] && cv && k < geo.K;
                 const uint32_t off = ok ? (g_off[j] + (uint32_t)(chunk * 16 * CM)) * XB : kOutOfRange;
                 if constexpr (XT == AQ_I8) {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, AUX);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 0);
                     stage[j][0] = v[0];
                     stage[j][1] = v[1];
                 } else {
-                    const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, AUX);
+                    const auto v = __builtin_amdgcn_raw_buffer_load_b128(xr, off, 0, 0);
                     stage[j][0] = v[0]; stage[j][1] = v[1]; stage[j][2] = v[2]; stage[j][3] = v[3];
                 }
             }
@@ -378,8 +373,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // pre-decoded mode: operand record (chunk, step, channel, lane half), 16 bytes each
     const __amdgpu_buffer_rsrc_t wr = buffer_rsrc(crec, (uint64_t)plan.nchunk * NS * geo.C_out * 32u);
     uint32_t crg[AN][REC_DW];
-    auto codes_load = [&](int chunk, auto aux_c) {
-        constexpr int AUX = decltype(aux_c)::value;
+    auto codes_load = [&](int chunk) {
         if constexpr (DEC == FUSED_DEC_REC) return;
         const bool cv = chunk < plan.nchunk;
 #pragma unroll
@@ -389,16 +383,16 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             for (int d = 0; d < REC_DW; d += 4) {
                 if constexpr (true) {
                     if (d + 4 <= REC_DW) {
-                        const auto v = __builtin_amdgcn_raw_buffer_load_b128(cr, off + 4 * d, 0, AUX);
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b128(cr, off + 4 * d, 0, 0);
                         crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2]; crg[b][d + 3] = v[3];
                     } else if (d + 3 == REC_DW) {
-                        const auto v = __builtin_amdgcn_raw_buffer_load_b96(cr, off + 4 * d, 0, AUX);
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b96(cr, off + 4 * d, 0, 0);
                         crg[b][d] = v[0]; crg[b][d + 1] = v[1]; crg[b][d + 2] = v[2];
                     } else if (d + 2 == REC_DW) {
-                        const auto v = __builtin_amdgcn_raw_buffer_load_b64(cr, off + 4 * d, 0, AUX);
+                        const auto v = __builtin_amdgcn_raw_buffer_load_b64(cr, off + 4 * d, 0, 0);
                         crg[b][d] = v[0]; crg[b][d + 1] = v[1];
                     } else {
-                        crg[b][d] = __builtin_amdgcn_raw_buffer_load_b32(cr, off + 4 * d, 0, AUX);
+                        crg[b][d] = __builtin_amdgcn_raw_buffer_load_b32(cr, off + 4 * d, 0, 0);
                     }
                 }
             }
@@ -461,6 +455,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // its staging store, so a chunk starts with its operands in flight.  The
     // look-ahead is used when a block of raw codewords (groups x M x 16 bytes
     // per lane) fits in 72 registers.
+    //
     // Prologue.  The loads go out in the order they are needed (codebook, codes,
     // activations); the codebook store and the first block's decode wait only
     // for the first two, so the decode runs while the activations are still in
@@ -468,8 +463,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     int chunk = wave;
     u32x4 af[NS][AM];
     u32x4 dec[NS];
-    codes_load(chunk, kPlainLoad);
-    stage_load(chunk, kPlainLoad);
+    codes_load(chunk);
+    stage_load(chunk);
     __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their uses
     if constexpr (CB_LDS) {
 #pragma unroll
@@ -492,8 +487,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
 #pragma unroll
             for (int d = 0; d < REC_DW; ++d) crn[b][d] = crg[b][d];
         if (more) {
-            stage_load(chunk + kWaves, kPlainLoad);   // next chunk's activations and codes
-            codes_load(chunk + kWaves, kPlainLoad);
+            stage_load(chunk + kWaves);   // next chunk's activations and codes
+            codes_load(chunk + kWaves);
         }
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
