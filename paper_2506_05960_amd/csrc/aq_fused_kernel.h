@@ -61,12 +61,12 @@ __device__ __forceinline__ uint32_t pick2(uint32_t xlo, int hlo, uint32_t xhi, i
 }
 
 
-// Quotient of non-negative a < 2^24 by d >= 1 through an fp32 reciprocal,
-// corrected to the exact integer quotient.
+// Quotient of non-negative a < 2^24 by 1 <= d < 2^24 through an fp32
+// reciprocal, corrected to the exact integer quotient (24-bit multiplies).
 __device__ __forceinline__ int fdiv(int a, int d, float inv_d) {
     int qt = (int)((float)a * inv_d);
-    qt += (qt + 1) * d <= a;
-    qt -= qt * d > a;
+    qt += (int)__umul24(qt + 1, d) <= a;
+    qt -= (int)__umul24(qt, d) > a;
     return qt;
 }
 
@@ -183,7 +183,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int wave = tid >> 6;
+    // uniform per wave: held in a scalar register, so chunk offsets are scalar arithmetic
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int l32 = lane & 31;
     const int q = lane >> 5;
     // XCD-aware tile order: consecutive workgroup ids go to the 8 XCDs in turn,
@@ -220,20 +221,25 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     u32x4 cbr[CB_PER_T > 0 ? CB_PER_T : 1];
     const int rows_b = 1 << geo.B;
     if constexpr (CB_LDS) {
-        const u32x4* src = static_cast<const u32x4*>(cb);
+        const __amdgpu_buffer_rsrc_t cbs = buffer_rsrc(cb, (uint64_t)MC * rows_b * ROWB);
 #pragma unroll
         for (int i = 0; i < CB_PER_T; ++i) {
             const int idx = tid + 256 * i;                 // 16-byte unit of the LDS layout
             const int m = idx / (256 * ROWB / 16);
             const int rem = idx - m * (256 * ROWB / 16);
             const int row = rem / (ROWB / 16), part = rem - row * (ROWB / 16);
-            cbr[i] = row < rows_b ? src[(m * rows_b + row) * (ROWB / 16) + part] : u32x4{0u, 0u, 0u, 0u};
+            const uint32_t off = row < rows_b ? (uint32_t)(((m * rows_b + row) * (ROWB / 16) + part) * 16) : kOutOfRange;
+            cbr[i] = __builtin_amdgcn_raw_buffer_load_b128(cbs, off, 0, 0);   // rows past 2^B read zeros
         }
     }
     uint8_t* pbuf0 = lds + plan.cb_bytes + wave * 2 * plan.pbuf_bytes;
     uint8_t* pbuf1 = pbuf0 + plan.pbuf_bytes;
 
     // ---- per-lane addressing, computed once (a chunk only adds a uniform offset) ----
+    // Only what the first loads need is computed before they are issued; the
+    // staging destinations and fragment offsets follow them.  Predicates are
+    // bitwise (no branches) and products of small non-negative values use
+    // 24-bit multiplies.
     const int HW = CONV ? geo.H * geo.W : 0;
     uint32_t a_base[AM];            // byte offset of this lane's A slice in a staging buffer
     uint32_t g_off[UPL];            // element offset of the unit's first value for chunk 0
@@ -241,52 +247,29 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     bool g_ok[UPL];                 // the unit loads data (false: zeros)
     bool l_ok[UPL];                 // the unit exists
     int k_first[UPL];               // linear: first k of the unit for chunk 0
+    const int gr0 = CONV ? fdiv(T0, geo.OW, plan.inv_ow) : 0;
     if constexpr (CONV) {
-        const float inv_ow = 1.0f / (float)geo.OW, inv_oh = 1.0f / (float)geo.OH;
-        const float inv_pr = 1.0f / (float)plan.pr;
-        const int gr0 = fdiv(T0, geo.OW, inv_ow);
-#pragma unroll
-        for (int a = 0; a < AM; ++a) {
-            const int T = T0 + 32 * a + l32;
-            const int gT = fdiv(T, geo.OW, inv_ow);
-            const int r = gT - gr0;
-            const int ow = T - gT * geo.OW;
-            a_base[a] = (uint32_t)(q * plan.ps + ((r * KH) * plan.pw + ow * geo.stride) * 16);
-        }
         const int wp = geo.W >> 1;  // pixel pairs per row
-        const float inv_wp = 1.0f / (float)wp;
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
             const int u = lane + 64 * j;
-            const int t = fdiv(u, wp, inv_wp);
-            const int pp = u - t * wp;
-            const int o = fdiv(t, plan.pr, inv_pr);
-            const int pr = t - o * plan.pr;
+            const int t = fdiv(u, wp, plan.inv_wp);
+            const int pp = u - __umul24(t, wp);
+            const int o = fdiv(t, plan.pr, plan.inv_pr);
+            const int pr = t - __umul24(o, plan.pr);
             const int r = pr / KH, kh = pr - r * KH;
             const int gr = gr0 + r;
-            const int b = fdiv(gr, geo.OH, inv_oh), oh = gr - b * geo.OH;
-            const int ih = oh * geo.stride - geo.pad + kh;
+            const int b = fdiv(gr, geo.OH, plan.inv_oh), oh = gr - __umul24(b, geo.OH);
+            const int ih = __umul24(oh, geo.stride) - geo.pad + kh;
             l_ok[j] = u < plan.units;
-            g_ok[j] = l_ok[j] && gr < plan.total_rows && ih >= 0 && ih < geo.H;
-            g_off[j] = g_ok[j] ? (uint32_t)(__umul24(__umul24(b, geo.cin) + 8 * o, geo.H) + ih) * (uint32_t)geo.W + 2u * pp : 0u;
-            l_off[j] = l_ok[j] ? (uint32_t)(o * plan.ps + (pr * plan.pw + 2 * pp + geo.pad) * 16)
-                               : (uint32_t)(plan.pbuf_bytes - 32);
+            g_ok[j] = l_ok[j] & (gr < plan.total_rows) & (ih >= 0) & (ih < geo.H);
+            const uint32_t ga = (uint32_t)(__umul24(__umul24(b, geo.cin) + 8 * o, geo.H) + ih) * (uint32_t)geo.W + 2u * pp;
+            g_off[j] = g_ok[j] ? ga : 0u;
             k_first[j] = 0;
-        }
-        // zero the padding columns of both buffers once: (buffer, plane, row, pad column)
-        const int padc = plan.pw - geo.W;
-        const int nrow = 2 * 2 * CM * plan.pr;
-        for (int i = lane; i < nrow * padc; i += 64) {
-            const int row = i / padc, pcx = i - row * padc;       // padc is 2 * pad, a small constant
-            const int bsel = row & 1, rest = row >> 1;
-            const int o = fdiv(rest, plan.pr, inv_pr), pr = rest - o * plan.pr;
-            const int pcol = pcx < geo.pad ? pcx : geo.W + pcx;
-            uint8_t* dst = (bsel ? pbuf1 : pbuf0) + o * plan.ps + (pr * plan.pw + pcol) * 16;
-            *reinterpret_cast<u32x4*>(dst) = u32x4{0u, 0u, 0u, 0u};
+            l_off[j] = l_ok[j] ? (uint32_t)(__umul24(o, plan.ps) + (__umul24(pr, plan.pw) + 2 * pp + geo.pad) * 16)
+                               : (uint32_t)(plan.pbuf_bytes - 32);
         }
     } else {
-#pragma unroll
-        for (int a = 0; a < AM; ++a) a_base[a] = (uint32_t)(q * plan.ps + (32 * a + l32) * 16);
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
             const int u = lane + 64 * j;
@@ -294,9 +277,10 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             const int tt = u / (2 * CM);
             const int T = T0 + tt;
             l_ok[j] = u < plan.units;
-            g_ok[j] = l_ok[j] && T < tokens;
+            g_ok[j] = l_ok[j] & (T < tokens);
             k_first[j] = 8 * o;
-            g_off[j] = g_ok[j] ? (uint32_t)(T * geo.K + 8 * o) : 0u;
+            const uint32_t ga = (uint32_t)(T * geo.K + 8 * o);
+            g_off[j] = g_ok[j] ? ga : 0u;
             l_off[j] = l_ok[j] ? (uint32_t)(o * plan.ps + tt * 16) : (uint32_t)(plan.pbuf_bytes - 32);
         }
     }
@@ -306,7 +290,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     for (int b = 0; b < AN; ++b) {
         const int n = N0 + 32 * b + l32;
         c_ok[b] = n < geo.C_out;
-        c_off[b] = c_ok[b] ? (uint32_t)((n * 2 + q) * plan.rec_bytes) : 0u;
+        c_off[b] = c_ok[b] ? (uint32_t)__umul24(n * 2 + q, plan.rec_bytes) : 0u;
     }
     const uint32_t chunk_rec_stride = (uint32_t)geo.C_out * 2u * (uint32_t)plan.rec_bytes;
 
@@ -399,6 +383,37 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         }
     };
 
+    // Prologue, first part: the chunk's codes and activations go out right
+    // after the codebook, before the remaining index arithmetic.
+    int chunk = wave;
+    codes_load(chunk);
+    stage_load(chunk);
+    __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their uses
+    if constexpr (CONV) {
+#pragma unroll
+        for (int a = 0; a < AM; ++a) {
+            const int T = T0 + 32 * a + l32;
+            const int gT = fdiv(T, geo.OW, plan.inv_ow);
+            const int r = gT - gr0;
+            const int ow = T - __umul24(gT, geo.OW);
+            a_base[a] = (uint32_t)(q * plan.ps + (__umul24(r * KH, plan.pw) + __umul24(ow, geo.stride)) * 16);
+        }
+        // zero the padding columns of both buffers once: (buffer, plane, row, pad column)
+        const int padc = plan.pw - geo.W;
+        const int nrow = 2 * 2 * CM * plan.pr;
+        for (int i = lane; i < nrow * padc; i += 64) {
+            const int row = i / padc, pcx = i - row * padc;       // padc is 2 * pad, a small constant
+            const int bsel = row & 1, rest = row >> 1;
+            const int o = fdiv(rest, plan.pr, plan.inv_pr), pr = rest - o * plan.pr;
+            const int pcol = pcx < geo.pad ? pcx : geo.W + pcx;
+            uint8_t* dst = (bsel ? pbuf1 : pbuf0) + o * plan.ps + (pr * plan.pw + pcol) * 16;
+            *reinterpret_cast<u32x4*>(dst) = u32x4{0u, 0u, 0u, 0u};
+        }
+    } else {
+#pragma unroll
+        for (int a = 0; a < AM; ++a) a_base[a] = (uint32_t)(q * plan.ps + (32 * a + l32) * 16);
+    }
+
     // Accumulators start in matrix-core (AGPR) registers: the empty asm pins the
     // register class of the zero start value, so the loop-carried values stay
     // there instead of being copied from VGPRs before every block of products.
@@ -456,16 +471,11 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // look-ahead is used when a block of raw codewords (groups x M x 16 bytes
     // per lane) fits in 72 registers.
     //
-    // Prologue.  The loads go out in the order they are needed (codebook, codes,
-    // activations); the codebook store and the first block's decode wait only
-    // for the first two, so the decode runs while the activations are still in
-    // flight.
-    int chunk = wave;
+    // Prologue, second part.  The codebook store and the first block's decode
+    // wait only for the codebook and the codes, so the decode runs while the
+    // activations are still in flight.
     u32x4 af[NS][AM];
     u32x4 dec[NS];
-    codes_load(chunk);
-    stage_load(chunk);
-    __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their uses
     if constexpr (CB_LDS) {
 #pragma unroll
         for (int i = 0; i < CB_PER_T; ++i) reinterpret_cast<u32x4*>(cb_lds)[tid + 256 * i] = cbr[i];

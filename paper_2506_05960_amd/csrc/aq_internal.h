@@ -67,6 +67,9 @@ struct FusedPlan {
     int pbuf_bytes;       // one staging buffer
     int total_rows;       // convolution: images * OH
     size_t lds_bytes;     // dynamic LDS per workgroup
+    // convolution: fp32 reciprocals of OW, OH, pr and W / 2 (correctly rounded)
+    // for the kernel's quotient-with-correction index arithmetic
+    float inv_ow, inv_oh, inv_pr, inv_wp;
 };
 
 struct FusedLaunch {

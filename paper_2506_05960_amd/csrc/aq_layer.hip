@@ -294,8 +294,13 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
             q.ps = q.pr * q.pw * 16;                    // one plane of 8 channels
             q.units = 2 * p->cm * q.pr * (geo.W / 2);   // (plane, row, pixel pair)
             q.total_rows = (int)(geo.tokens / geo.OW);
+            q.inv_ow = 1.0f / (float)geo.OW;
+            q.inv_oh = 1.0f / (float)geo.OH;
+            q.inv_pr = 1.0f / (float)q.pr;
+            q.inv_wp = 1.0f / (float)(geo.W / 2);
         } else {
             q.pr = q.pw = 0;
+            q.inv_ow = q.inv_oh = q.inv_pr = q.inv_wp = 0.0f;
             q.ps = t.bm * 16 + 16;                      // one plane of 8 consecutive k
             q.units = t.bm * 2 * p->cm;                 // (token, plane)
             q.total_rows = 0;
