@@ -197,17 +197,14 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         const int xcd = h & 7, j = h >> 3;
         const int per = nwg >> 3, rem = nwg & 7;
         const int L = xcd * per + min(xcd, rem) + j;
-        if (plan.nmajor) {
-            // channel tile slowest: an XCD's range covers few channel tiles, so the
-            // weight operands it streams stay in its L2
-            const int ntm = (int)((geo.tokens + BM - 1) / BM);
-            tile_n = L / ntm;
-            tile_m = L - tile_n * ntm;
-        } else {
-            const int ntn = (geo.C_out + BN - 1) / BN;
-            tile_m = L / ntn;
-            tile_n = L - tile_m * ntn;
-        }
+        // plan.nmajor: channel tile slowest (an XCD's range then covers few
+        // channel tiles, so the weight operands it streams stay in its L2);
+        // else token tile slowest.  The host supplies the count of the fastest
+        // tile index and its reciprocal, so this is branch-free.
+        const int hi = __builtin_amdgcn_readfirstlane(fdiv(L, plan.tile_div, plan.inv_tile_div));
+        const int lo = L - hi * plan.tile_div;
+        tile_n = plan.nmajor ? hi : lo;
+        tile_m = plan.nmajor ? lo : hi;
     }
     const int T0 = tile_m * BM;                     // token and element counts fit in 31 bits (host check)
     const int N0 = tile_n * BN;
@@ -297,9 +294,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // ---- staging of one chunk: global -> registers (out-of-range offsets read zeros) ----
     constexpr int SREG = CONV ? 8 : 4;    // dwords per unit
     constexpr int XB = XT == AQ_I8 ? 1 : 2;   // bytes per activation
-    const uint64_t xbytes = CONV ? (uint64_t)plan.total_rows / geo.OH * geo.cin * HW * 2
-                                 : (uint64_t)geo.tokens * geo.K * XB;
-    const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(X, xbytes);
+    const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(X, (uint64_t)plan.x_bytes);   // computed on the host
     uint32_t stage[UPL][SREG];
     // Chunks past the last one read zeros (no branch, so the compiler's wait
     // counts stay exact across the prefetch).
@@ -309,13 +304,13 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         for (int j = 0; j < UPL; ++j) {
             if constexpr (CONV) {
                 // 8 channels x 2 pixels
-                const uint32_t base = g_ok[j] && cv ? (g_off[j] + (uint32_t)(chunk * 16 * CM) * HW) * 2u : kOutOfRange;
+                const uint32_t base = g_ok[j] & cv ? (g_off[j] + (uint32_t)(chunk * 16 * CM) * HW) * 2u : kOutOfRange;
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
                     stage[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, 0);
             } else {
                 const int k = chunk * 16 * CM + k_first[j];
-                const bool ok = g_ok[j] && cv && k < geo.K;
+                const bool ok = g_ok[j] & cv & (k < geo.K);
                 const uint32_t off = ok ? (g_off[j] + (uint32_t)(chunk * 16 * CM)) * XB : kOutOfRange;
                 if constexpr (XT == AQ_I8) {
                     const auto v = __builtin_amdgcn_raw_buffer_load_b64(xr, off, 0, 0);
@@ -362,7 +357,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         const bool cv = chunk < plan.nchunk;
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
-            const uint32_t off = c_ok[b] && cv ? c_off[b] + (uint32_t)chunk * chunk_rec_stride : kOutOfRange;
+            const uint32_t off = c_ok[b] & cv ? c_off[b] + (uint32_t)chunk * chunk_rec_stride : kOutOfRange;
 #pragma unroll
             for (int d = 0; d < REC_DW; d += 4) {
                 if constexpr (true) {

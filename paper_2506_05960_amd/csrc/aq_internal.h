@@ -70,6 +70,9 @@ struct FusedPlan {
     // convolution: fp32 reciprocals of OW, OH, pr and W / 2 (correctly rounded)
     // for the kernel's quotient-with-correction index arithmetic
     float inv_ow, inv_oh, inv_pr, inv_wp;
+    int64_t x_bytes;      // bytes of this forward's input X (the bound of the kernel's activation loads)
+    int tile_div;         // tiles along the faster tile index (token tiles if nmajor, else channel tiles)
+    float inv_tile_div;   // its fp32 reciprocal
 };
 
 struct FusedLaunch {

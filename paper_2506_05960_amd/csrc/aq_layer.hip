@@ -606,6 +606,10 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
                 e = aq::launch_operand_records(geo, fp, w, L->d_wrec, st);
                 recs = static_cast<const uint8_t*>(L->d_wrec);
             }
+            fp.x_bytes = geo.conv ? n * (int64_t)geo.cin * geo.H * geo.W * 2
+                                  : geo.tokens * (int64_t)geo.K * (d.x_dtype == AQ_I8 ? 1 : 2);
+            fp.tile_div = fp.nmajor ? (int)((geo.tokens + fp.bm - 1) / fp.bm) : (geo.C_out + fp.bn - 1) / fp.bn;
+            fp.inv_tile_div = 1.0f / (float)fp.tile_div;
             const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
             if (e == hipSuccess) e = aq::launch_fused_forward(geo, fp, fl);
         } else if (geo.g == 8) {
