@@ -101,6 +101,11 @@ size_t rec_gemm_lds_bytes(int kind, int bm, int bn);
 size_t operand_record_bytes(const Geom& geo, const FusedPlan& plan);
 hipError_t launch_operand_records(const Geom& geo, const FusedPlan& plan, const DeviceWeights& w, void* rec,
                                   hipStream_t stream);
+// Linear layer over pre-decoded operand records (plan.cm == 4): 2 x 2 wave
+// split of a 256- or 128-token by 128-channel tile, no K split.
+bool rec_linear_supported(const Geom& geo, const FusedPlan& plan, int x_dtype);
+int rec_linear_tile(const Geom& geo);
+hipError_t launch_rec_linear(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 hipError_t launch_fused_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 hipError_t launch_fused_conv1(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 hipError_t launch_fused_linear(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);

@@ -611,7 +611,12 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
             fp.tile_div = fp.nmajor ? (int)((geo.tokens + fp.bm - 1) / fp.bm) : (geo.C_out + fp.bn - 1) / fp.bn;
             fp.inv_tile_div = 1.0f / (float)fp.tile_div;
             const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
-            if (e == hipSuccess) e = aq::launch_fused_forward(geo, fp, fl);
+            // a linear layer's records feed the 2 x 2 wave-split product (AQ_REC_LINEAR=0: the
+            // fused kernel's own pre-decoded mode, whose partial-tile order matches its in-loop mode)
+            const char* rl = std::getenv("AQ_REC_LINEAR");
+            const bool rlin = fp.dec == aq::FUSED_DEC_REC && !(rl && std::atoi(rl) == 0) &&
+                              aq::rec_linear_supported(geo, fp, d.x_dtype);
+            if (e == hipSuccess) e = rlin ? aq::launch_rec_linear(geo, fp, fl) : aq::launch_fused_forward(geo, fp, fl);
         } else if (geo.g == 8) {
             e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
         } else {

@@ -269,7 +269,9 @@ def test_predecoded_operands_match_in_loop_decode(spec, monkeypatch):
     """Pre-decoded operand records give bit-identical outputs to decoding inside the main loop."""
     inp = generate(spec, 31)
     monkeypatch.setenv("AQ_FUSED_REC", "1")
+    monkeypatch.setenv("AQ_REC_LINEAR", "0")     # the fused kernel's own pre-decoded mode
     y_rec = _run(spec, inp, "decode")
+    monkeypatch.delenv("AQ_REC_LINEAR")
     monkeypatch.setenv("AQ_GEMM", "1")
     y_gemm = _run(spec, inp, "decode")            # dense product over the same records
     monkeypatch.delenv("AQ_GEMM")
@@ -386,12 +388,46 @@ def test_fused_linear_int8_tiles(tile, rec, monkeypatch):
     """int8 activations, M = 4, several chunks per wave and a ragged token tail, in both weight modes."""
     monkeypatch.setenv("AQ_FUSED_TILE", tile)
     monkeypatch.setenv("AQ_FUSED_REC", rec)
+    monkeypatch.setenv("AQ_REC_LINEAR", "0")
     spec = LayerSpec(name="t_lin_i8", C_out=136, K=640, g=8, M=4, B=8, n=300, x_dtype="i8")
     inp = generate(spec, 17)
     y = _run(spec, inp, "decode")
     err = O.rel_err_inf(y, O.forward(spec, inp))
     _say(f"tile {tile} rec={rec} {spec.name} err={err:.3e}")
     assert err <= 2e-3
+
+
+# ---------------------------------------------------------------------------
+# linear layers over pre-decoded records: 2 x 2 wave split, no K split
+# ---------------------------------------------------------------------------
+
+RLIN = [
+    # ragged tokens, K not a multiple of the 64-wide chunk, C_out not a multiple of the 128-wide tile
+    LayerSpec(name="r_tail", C_out=300, K=200, g=8, M=4, B=8, n=333),
+    LayerSpec(name="r_i8", C_out=136, K=640, g=8, M=4, B=8, n=300, x_dtype="i8"),
+    LayerSpec(name="r_f32y", C_out=68, K=72, g=8, M=2, B=8, n=517, y_dtype="f32"),
+    LayerSpec(name="r_b16", C_out=96, K=512, g=8, M=1, B=16, n=130),
+    # one chunk; an odd and an even chunk count
+    LayerSpec(name="r_k64", C_out=128, K=64, g=8, M=2, B=8, n=256),
+    LayerSpec(name="r_k576_i8", C_out=1728, K=576, g=8, M=4, B=8, n=1000, x_dtype="i8"),
+    LayerSpec(name="r_k1024", C_out=260, K=1024, g=8, M=3, B=8, n=600),
+]
+
+
+@pytest.mark.parametrize("spec", RLIN, ids=lambda s: s.name)
+def test_rec_linear_tiles(spec, monkeypatch):
+    """Both tiles against the oracle, and bit-identical to each other (one accumulation order per output)."""
+    monkeypatch.setenv("AQ_FUSED_REC", "1")
+    inp = generate(spec, 41)
+    y_ref = O.forward(spec, inp)
+    ys = {}
+    for tile in ("256", "128"):
+        monkeypatch.setenv("AQ_RLIN_TILE", tile)
+        ys[tile] = _run(spec, inp, "decode")
+        err = O.rel_err_inf(ys[tile], y_ref)
+        _say(f"rec linear {spec.name} tile {tile} err={err:.3e}")
+        assert err <= 2e-3
+    assert np.array_equal(ys["256"], ys["128"])
 
 
 # ---------------------------------------------------------------------------
