@@ -402,7 +402,17 @@ bool use_predecoded(const aq_layer* L, const Geom& geo) {
     // token tile, so the single decode pass wins once tokens x M is large enough
     const int64_t tm = geo.tokens * p.mc;
     if (p.kind == 1) return tm >= 32768 || (tm >= 8192 && geo.K >= 5000);
-    if (p.kind == 0) return p.mc >= 4 && geo.C_out >= 1152 && geo.tokens >= 2048;
+    if (p.kind == 0) {
+        if (aq::rec_linear_supported(geo, p, L->desc.x_dtype)) {
+            // the wave-split product over records (measured on the U-Net linear shapes):
+            // faster once its 128 x 128 tiles cover three quarters of the compute units,
+            // at 2048 tokens and up or M >= 4 (the in-loop decode then gathers 4 codewords
+            // per group); with fewer tiles the in-loop decode's K split keeps more units busy
+            const int64_t tiles = ((geo.tokens + 127) / 128) * (int64_t)((geo.C_out + 127) / 128);
+            return tiles >= 192 && (geo.tokens >= 2048 || p.mc >= 4);
+        }
+        return p.mc >= 4 && geo.C_out >= 1152 && geo.tokens >= 2048;
+    }
     return p.mc >= 4 && geo.tokens >= 32768;
 }
 
