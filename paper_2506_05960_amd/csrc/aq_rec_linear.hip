@@ -33,6 +33,7 @@
 // 4-channel piece is stored directly (8 bytes fp16, 16 bytes fp32).
 #include <algorithm>
 #include <cstdlib>
+#include <cstring>
 #include <type_traits>
 
 #include "aq_device.h"
@@ -89,18 +90,21 @@ __device__ __forceinline__ int qdiv(int a, int d, float inv_d) {
     return qt;
 }
 
-// TM / TN: 32-wide token / channel blocks per wave (tile 64 TM x 64 TN).
-template <int XT, int TM, int TN>
+// TM / TN: 32-wide token / channel blocks per wave; WGT: waves along the
+// tokens (2: a 2 x 2 split, 1: the four waves side by side along the channels).
+// Tile 32 TM WGT tokens x 32 TN (4 / WGT) channels.
+template <int XT, int TM, int TN, int WGT>
 __global__ void __launch_bounds__(256, 1)
 rec_linear_kernel(RecLinArgs ar, const uint8_t* __restrict__ rec, const float* __restrict__ scales,
                   const void* __restrict__ X, const float* __restrict__ x_scales, void* __restrict__ Y) {
-    constexpr int BM = 64 * TM, BN = 64 * TN;
+    constexpr int WGN = 4 / WGT;                 // waves along the channels
+    constexpr int BM = 32 * TM * WGT, BN = 32 * TN * WGN;
     constexpr int UPL = BM / 32;                 // staging units (token, plane) per thread
     constexpr int PS = BM * 16 + 32;             // plane stride: consecutive planes 2 banks apart
     constexpr int BUF = 8 * PS;                  // one staging buffer
     constexpr int XB = XT == AQ_I8 ? 1 : 2;      // bytes per activation
     constexpr int SW = XT == AQ_I8 ? 2 : 4;      // dwords per staging unit (8 values)
-    constexpr int RS = 144;                      // epilogue: bytes per fp16 output row of 64 channels, padded
+    constexpr int RS = 64 * TN + 16;             // epilogue: bytes per fp16 output row of a wave, padded
 
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     const int tid = threadIdx.x;
@@ -122,8 +126,8 @@ rec_linear_kernel(RecLinArgs ar, const uint8_t* __restrict__ rec, const float* _
         tile_m = ar.nmajor ? lo : hi;
     }
     const int T0 = tile_m * BM, N0 = tile_n * BN;
-    const int WT = (wave & 1) * 32 * TM;         // the wave's token offset in the tile
-    const int WN = (wave >> 1) * 32 * TN;        // the wave's channel offset in the tile
+    const int WT = (wave % WGT) * 32 * TM;       // the wave's token offset in the tile
+    const int WN = (wave / WGT) * 32 * TN;       // the wave's channel offset in the tile
 
     // ---- activation staging: unit j of this thread is (token tt + 32 j, plane o) ----
     const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(X, ar.x_bytes);
@@ -280,8 +284,8 @@ rec_linear_kernel(RecLinArgs ar, const uint8_t* __restrict__ rec, const float* _
     typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
     if (ar.y_dtype != AQ_F32 && (ar.C_out & 7) == 0) {
         // fp16 rows through LDS (the staging buffers are free after the last
-        // barrier): each wave writes its 32 TM x 64 sub-tile as rows of RS bytes,
-        // then 8 lanes store one row's 128 contiguous bytes
+        // barrier): each wave writes its 32 TM x 32 TN sub-tile as rows of RS
+        // bytes, then 4 TN lanes store one row's 64 TN contiguous bytes
         uint8_t* ew = lds + wave * (32 * TM * RS);
 #pragma unroll
         for (int a = 0; a < TM; ++a) {
@@ -302,8 +306,8 @@ rec_linear_kernel(RecLinArgs ar, const uint8_t* __restrict__ rec, const float* _
         __builtin_amdgcn_wave_barrier();   // one wave's LDS accesses execute in order
         asm volatile("" ::: "memory");
 #pragma unroll
-        for (int i = 0; i < 4 * TM; ++i) {
-            const int R = 8 * i + (lane >> 3), C = lane & 7;
+        for (int i = 0; i < 2 * TM * TN; ++i) {
+            const int R = (16 / TN) * i + lane / (4 * TN), C = lane % (4 * TN);
             const u32x4 v = *reinterpret_cast<const u32x4*>(ew + R * RS + 16 * C);
             const int t = T0 + WT + R, ch = N0 + WN + 8 * C;
             const bool ok = (t < ar.tokens) & (ch < ar.C_out);   // C_out % 8 == 0: the segment is whole
@@ -339,17 +343,18 @@ rec_linear_kernel(RecLinArgs ar, const uint8_t* __restrict__ rec, const float* _
     }
 }
 
-// staging (two buffers of 8 planes) or the epilogue's fp16 rows (4 waves x 32 TM rows of 144 bytes)
-constexpr size_t rec_linear_lds_bytes(int TM) {
-    return (size_t)2 * 8 * (64 * TM * 16 + 32) > (size_t)4 * 32 * TM * 144 ? (size_t)2 * 8 * (64 * TM * 16 + 32)
-                                                                          : (size_t)4 * 32 * TM * 144;
+// staging (two buffers of 8 planes) or the epilogue's fp16 rows (4 waves x 32 TM rows of 64 TN + 16 bytes)
+constexpr size_t rec_linear_lds_bytes(int BM, int TM, int TN) {
+    return (size_t)2 * 8 * (BM * 16 + 32) > (size_t)4 * 32 * TM * (64 * TN + 16)
+               ? (size_t)2 * 8 * (BM * 16 + 32)
+               : (size_t)4 * 32 * TM * (64 * TN + 16);
 }
 
-template <int XT, int TM, int TN>
+template <int XT, int TM, int TN, int WGT>
 hipError_t rec_linear_cfg(const RecLinArgs& ar, const FusedLaunch& fl) {
-    auto kern = rec_linear_kernel<XT, TM, TN>;
-    constexpr int BM = 64 * TM, BN = 64 * TN;
-    constexpr size_t lds = rec_linear_lds_bytes(TM);
+    auto kern = rec_linear_kernel<XT, TM, TN, WGT>;
+    constexpr int BM = 32 * TM * WGT, BN = 32 * TN * (4 / WGT);
+    constexpr size_t lds = rec_linear_lds_bytes(BM, TM, TN);
     static bool attr = false;
     if (!attr) {
         const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -374,14 +379,20 @@ bool rec_linear_supported(const Geom& geo, const FusedPlan& plan, int x_dtype) {
     return geo.tokens * (int64_t)std::max(geo.K, geo.C_out) * 4 < lim && rec_bytes < lim && geo.tokens < (1 << 24);
 }
 
+// Tile variant: 0 = 128 x 128 in a 2 x 2 wave split, 1 = 256 x 128 in a 2 x 2
+// split, 2 = 128 x 128 with the four waves side by side along the channels.
 int rec_linear_tile(const Geom& geo) {
-    if (const char* s = std::getenv("AQ_RLIN_TILE")) return std::atoi(s) == 256 ? 256 : 128;
-    // The 128-token tile fits 256 registers per lane, so two workgroups share a
+    if (const char* s = std::getenv("AQ_RLIN_TILE")) {
+        if (std::strcmp(s, "256") == 0) return 1;
+        if (std::strcmp(s, "128w") == 0) return 2;
+        return 0;
+    }
+    // The 128-token tiles fit 256 registers per lane, so two workgroups share a
     // compute unit and overlap one's prologue and epilogue with the other's
     // products; measured faster than the 256-token tile on the 8192-token qkv
     // layer (34.0 vs 36.2 us per forward).
     (void)geo;
-    return 128;
+    return 0;
 }
 
 hipError_t launch_rec_linear(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
@@ -390,7 +401,8 @@ hipError_t launch_rec_linear(const Geom& geo, const FusedPlan& plan, const Fused
     ar.K = geo.K;
     ar.C_out = geo.C_out;
     ar.nchunk = plan.nchunk;
-    const int bm = rec_linear_tile(geo), bn = 128;
+    const int var = rec_linear_tile(geo);
+    const int bm = var == 1 ? 256 : 128, bn = 128;
     const int tm = (int)((geo.tokens + bm - 1) / bm), tn = (geo.C_out + bn - 1) / bn;
     ar.nmajor = plan.nmajor;
     ar.tile_div = ar.nmajor ? tm : tn;
@@ -402,11 +414,13 @@ hipError_t launch_rec_linear(const Geom& geo, const FusedPlan& plan, const Fused
     ar.y_bytes = (uint32_t)(geo.tokens * geo.C_out * (fl.y_dtype == AQ_F32 ? 4 : 2));
     ar.step_bytes = (uint32_t)geo.C_out * 32u;
     if (fl.x_dtype == AQ_I8) {
-        if (bm == 256) return rec_linear_cfg<AQ_I8, 4, 2>(ar, fl);
-        return rec_linear_cfg<AQ_I8, 2, 2>(ar, fl);
+        if (var == 1) return rec_linear_cfg<AQ_I8, 4, 2, 2>(ar, fl);
+        if (var == 2) return rec_linear_cfg<AQ_I8, 4, 1, 1>(ar, fl);
+        return rec_linear_cfg<AQ_I8, 2, 2, 2>(ar, fl);
     }
-    if (bm == 256) return rec_linear_cfg<AQ_F16, 4, 2>(ar, fl);
-    return rec_linear_cfg<AQ_F16, 2, 2>(ar, fl);
+    if (var == 1) return rec_linear_cfg<AQ_F16, 4, 2, 2>(ar, fl);
+    if (var == 2) return rec_linear_cfg<AQ_F16, 4, 1, 1>(ar, fl);
+    return rec_linear_cfg<AQ_F16, 2, 2, 2>(ar, fl);
 }
 
 }  // namespace aq

@@ -416,18 +416,18 @@ RLIN = [
 
 @pytest.mark.parametrize("spec", RLIN, ids=lambda s: s.name)
 def test_rec_linear_tiles(spec, monkeypatch):
-    """Both tiles against the oracle, and bit-identical to each other (one accumulation order per output)."""
+    """Every tile against the oracle, and bit-identical to each other (one accumulation order per output)."""
     monkeypatch.setenv("AQ_FUSED_REC", "1")
     inp = generate(spec, 41)
     y_ref = O.forward(spec, inp)
     ys = {}
-    for tile in ("256", "128"):
+    for tile in ("256", "128", "128w"):
         monkeypatch.setenv("AQ_RLIN_TILE", tile)
         ys[tile] = _run(spec, inp, "decode")
         err = O.rel_err_inf(ys[tile], y_ref)
         _say(f"rec linear {spec.name} tile {tile} err={err:.3e}")
         assert err <= 2e-3
-    assert np.array_equal(ys["256"], ys["128"])
+    assert np.array_equal(ys["256"], ys["128"]) and np.array_equal(ys["128w"], ys["128"])
 
 
 # ---------------------------------------------------------------------------
