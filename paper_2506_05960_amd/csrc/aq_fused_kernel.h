@@ -181,6 +181,17 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     static_assert(KIND != 1 || CM == 1, "3x3 chunks are 16 channels");
 
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+    // Every kernel argument the prologue reads is pinned to scalar registers
+    // here, so they arrive in one scalar-memory round trip.  Left to itself the
+    // compiler loads each group next to its first use and waits for it there:
+    // four round trips before the first activation load, each a scalar-cache
+    // miss while every wave of the launch starts at once.
+    asm volatile("" ::"s"(geo.tokens), "s"(geo.C_out), "s"(geo.K), "s"(geo.B), "s"(geo.H), "s"(geo.W),
+                 "s"(geo.cin), "s"(geo.OW), "s"(geo.OH), "s"(geo.stride), "s"(geo.pad));
+    asm volatile("" ::"s"(plan.nchunk), "s"(plan.ps), "s"(plan.pw), "s"(plan.pr), "s"(plan.pbuf_bytes),
+                 "s"(plan.nmajor), "s"(plan.units), "s"(plan.tile_div), "s"(plan.rec_bytes), "s"(plan.inv_pr),
+                 "s"(plan.inv_ow), "s"(plan.cb_bytes), "s"(plan.x_bytes), "s"(plan.total_rows), "s"(plan.inv_wp),
+                 "s"(plan.inv_tile_div), "s"(plan.inv_oh), "s"(cb), "s"(crec), "s"(X), "s"(gridDim.x));
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     // uniform per wave: held in a scalar register, so chunk offsets are scalar arithmetic
@@ -423,16 +434,17 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             asm volatile("" : "=a"(acc[a][b]) : "0"(z));
         }
 
-    // activation fragments of one chunk: every (step, token block)
+    // activation fragments of one step (every token block), and of a whole chunk
+    auto load_af_step = [&](const uint8_t* buf, u32x4 (&af)[NS][AM], int s) {
+        uint32_t soff;
+        if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
+        else soff = (uint32_t)(2 * s * plan.ps);
+#pragma unroll
+        for (int a = 0; a < AM; ++a) af[s][a] = *reinterpret_cast<const u32x4*>(buf + a_base[a] + soff);
+    };
     auto load_af = [&](const uint8_t* buf, u32x4 (&af)[NS][AM]) {
 #pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            uint32_t soff;
-            if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
-            else soff = (uint32_t)(2 * s * plan.ps);
-#pragma unroll
-            for (int a = 0; a < AM; ++a) af[s][a] = *reinterpret_cast<const u32x4*>(buf + a_base[a] + soff);
-        }
+        for (int s = 0; s < NS; ++s) load_af_step(buf, af, s);
     };
     constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L && NS * MC <= 18;
     // weights of one 32-channel block of a chunk, decoded into MFMA operands
@@ -482,6 +494,11 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     stage_store(pbuf0);
     wave_sync();
     load_af(pbuf0, af);
+    // Next-chunk staging inside the last channel block (below) for pre-decoded
+    // operands (conv8: 101.7 -> 97.7 us).  Not with the in-loop decode: its main
+    // loop is bound by LDS codeword gathers, which the staging then competes
+    // with (conv64: 12.1 -> 12.4 us), and with four token blocks it spills.
+    constexpr bool OVL = DEC == FUSED_DEC_REC;
     int it = 0;
     for (; chunk < plan.nchunk; chunk += kWaves, ++it) {
         uint8_t* nxt = (it & 1) ? pbuf0 : pbuf1;
@@ -498,6 +515,16 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
             __builtin_amdgcn_sched_barrier(0);
+            if (OVL && b == AN - 1) {
+                // The next chunk's activations go to the staging buffer this chunk
+                // does not read, and each step's fragments are read back right
+                // after that step's last products (their registers are free from
+                // there on), so neither waits for the products to drain.  Past
+                // the last chunk this moves stale data into the unused buffer.
+                wave_sync();
+                stage_store(nxt);
+                wave_sync();
+            }
             u32x4 dnext[NS];
             bool have_next = false;
             if constexpr (LOOKAHEAD) {
@@ -529,6 +556,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                     if constexpr (CONV) acc[a][b] = mfma_f16(bf, af[s][a], acc[a][b]);   // rows: channels
                     else acc[a][b] = mfma_f16(af[s][a], bf, acc[a][b]);                  // rows: tokens
                 }
+                if (OVL && b == AN - 1) load_af_step(nxt, af, s);
             }
             if (have_next) {
 #pragma unroll
@@ -536,11 +564,13 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             }
         }
         __builtin_amdgcn_sched_barrier(0);
-        if (more) {
-            wave_sync();
-            stage_store(nxt);
-            wave_sync();
-            load_af(nxt, af);
+        if constexpr (!OVL) {
+            if (more) {
+                wave_sync();
+                stage_store(nxt);
+                wave_sync();
+                load_af(nxt, af);
+            }
         }
     }
 
