@@ -10,6 +10,7 @@ static hipError_t conv_tiles(const Geom& geo, const FusedPlan& p, const FusedLau
     if constexpr (KIND == 1) {
         AQ_TILE(64, 96, 3)
         AQ_TILE(64, 64, 3)
+        AQ_TILE(128, 64, 3)
         AQ_TILE(128, 64, 6)
         AQ_TILE(64, 64, 6)
     } else {

@@ -191,7 +191,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     asm volatile("" ::"s"(plan.nchunk), "s"(plan.ps), "s"(plan.pw), "s"(plan.pr), "s"(plan.pbuf_bytes),
                  "s"(plan.nmajor), "s"(plan.units), "s"(plan.tile_div), "s"(plan.rec_bytes), "s"(plan.inv_pr),
                  "s"(plan.inv_ow), "s"(plan.cb_bytes), "s"(plan.x_bytes), "s"(plan.total_rows), "s"(plan.inv_wp),
-                 "s"(plan.inv_tile_div), "s"(plan.inv_oh), "s"(cb), "s"(crec), "s"(X), "s"(gridDim.x));
+                 "s"(plan.inv_tile_div), "s"(plan.inv_oh), "s"(cb), "s"(crec), "s"(X), "s"(gridDim.x),
+                 "s"(plan.sr), "s"(plan.rpb), "s"(plan.inv_sr), "s"(plan.inv_rpb));
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     // uniform per wave: held in a scalar register, so chunk offsets are scalar arithmetic
@@ -265,10 +266,12 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             const int pp = u - __umul24(t, wp);
             const int o = fdiv(t, plan.pr, plan.inv_pr);
             const int pr = t - __umul24(o, plan.pr);
-            const int r = pr / KH, kh = pr - r * KH;
-            const int gr = gr0 + r;
+            // staged row pr: row jr of block blk, the input rows of plan.rpb
+            // consecutive output rows starting at output row gr (one image)
+            const int blk = fdiv(pr, plan.sr, plan.inv_sr), jr = pr - __umul24(blk, plan.sr);
+            const int gr = gr0 + __umul24(blk, plan.rpb);
             const int b = fdiv(gr, geo.OH, plan.inv_oh), oh = gr - __umul24(b, geo.OH);
-            const int ih = __umul24(oh, geo.stride) - geo.pad + kh;
+            const int ih = __umul24(oh, geo.stride) - geo.pad + jr;
             l_ok[j] = u < plan.units;
             g_ok[j] = l_ok[j] & (gr < plan.total_rows) & (ih >= 0) & (ih < geo.H);
             const uint32_t ga = (uint32_t)(__umul24(__umul24(b, geo.cin) + 8 * o, geo.H) + ih) * (uint32_t)geo.W + 2u * pp;
@@ -402,7 +405,10 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             const int gT = fdiv(T, geo.OW, plan.inv_ow);
             const int r = gT - gr0;
             const int ow = T - __umul24(gT, geo.OW);
-            a_base[a] = (uint32_t)(q * plan.ps + (__umul24(r * KH, plan.pw) + __umul24(ow, geo.stride)) * 16);
+            // output row r: block r / rpb, whose row (r % rpb) * stride is kernel row 0
+            const int blk = fdiv(r, plan.rpb, plan.inv_rpb), rr = r - __umul24(blk, plan.rpb);
+            const int R0 = __umul24(blk, plan.sr) + __umul24(rr, geo.stride);
+            a_base[a] = (uint32_t)(q * plan.ps + (__umul24(R0, plan.pw) + __umul24(ow, geo.stride)) * 16);
         }
         // zero the padding columns of both buffers once: (buffer, plane, row, pad column)
         const int padc = plan.pw - geo.W;

@@ -64,6 +64,11 @@ struct FusedPlan {
     int bm, bn, upl;      // tile and staging units per lane
     int units;            // staging units per chunk
     int pr, pw, ps;       // patch rows, patch width (pixels), pixel / token-row stride (bytes)
+    // convolution: the staged rows are blocks of sr rows, each holding every input
+    // row of rpb consecutive output rows of one image (output row i of a block
+    // reads block rows i * stride + kernel row)
+    int sr, rpb;
+    float inv_sr, inv_rpb;
     int pbuf_bytes;       // one staging buffer
     int total_rows;       // convolution: images * OH
     size_t lds_bytes;     // dynamic LDS per workgroup

@@ -258,11 +258,11 @@ struct TileCand {
 // Per-forward tile choice; fills the remaining plan fields.  Returns false when
 // no instantiated tile fits (the caller then uses the generic kernel).
 bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
-    static const TileCand conv3[] = {{64, 96, 3}, {64, 64, 3}, {128, 64, 6}, {64, 64, 6}};
+    static const TileCand conv3[] = {{64, 96, 3}, {64, 64, 3}, {128, 64, 3}, {128, 64, 6}, {64, 64, 6}};
     static const TileCand conv1[] = {{64, 96, 4}, {64, 64, 4}};
     static const TileCand lin[] = {{64, 96, 8}, {64, 64, 8}, {32, 128, 4}, {32, 64, 4}};
     const TileCand* cands = p->kind == 1 ? conv3 : p->kind == 2 ? conv1 : lin;
-    const int ncand = p->kind == 1 ? 4 : p->kind == 2 ? 2 : 4;
+    const int ncand = p->kind == 1 ? 5 : p->kind == 2 ? 2 : 4;
     int want_bm = 0, want_bn = 0;
     if (const char* s = std::getenv("AQ_FUSED_TILE")) std::sscanf(s, "%dx%d", &want_bm, &want_bn);
     double best = 0;
@@ -287,10 +287,33 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
             if (!(t.bm % geo.OW == 0 || geo.OW % t.bm == 0)) continue;
             const int tr = t.bm >= geo.OW ? t.bm / geo.OW : 1;
             const int kh = p->kind == 1 ? 3 : 1;
-            q.pr = tr * kh;
+            // Staged rows: each input row once per block of output rows of one image
+            // (a tile of whole images, or of consecutive rows of one image), instead
+            // of kh rows per output row, when that stages fewer rows.
+            // AQ_FUSED_ROWS=each keeps kh rows per output row.
+            const int img = geo.OH * geo.OW;
+            int rpb = 1;
+            const char* rows_env = std::getenv("AQ_FUSED_ROWS");
+            if (!(rows_env && std::strcmp(rows_env, "each") == 0)) {
+                if (t.bm % img == 0) rpb = geo.OH;
+                else if (img % t.bm == 0 && tr > 1) rpb = tr;
+            }
+            int sr = (rpb - 1) * geo.stride + kh;
+            if (rpb > 1 && (tr / rpb) * sr >= tr * kh) {
+                rpb = 1;
+                sr = kh;
+            }
+            q.rpb = rpb;
+            q.sr = sr;
+            q.inv_rpb = 1.0f / (float)rpb;
+            q.inv_sr = 1.0f / (float)sr;
+            q.pr = (tr / rpb) * sr;
             q.pw = geo.W + 2 * geo.pad;
+            // consecutive output rows of a block are `stride` staged rows apart (kh
+            // apart with one output row per block)
+            const int rstep = rpb > 1 ? geo.stride : kh;
             if (widen)
-                while ((kh * q.pw - geo.OW) % 16 != 0) ++q.pw;
+                while ((rstep * q.pw - geo.OW) % 16 != 0) ++q.pw;
             q.ps = q.pr * q.pw * 16;                    // one plane of 8 channels
             q.units = 2 * p->cm * q.pr * (geo.W / 2);   // (plane, row, pixel pair)
             q.total_rows = (int)(geo.tokens / geo.OW);
@@ -300,7 +323,8 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
             q.inv_wp = 1.0f / (float)(geo.W / 2);
         } else {
             q.pr = q.pw = 0;
-            q.inv_ow = q.inv_oh = q.inv_pr = q.inv_wp = 0.0f;
+            q.sr = q.rpb = 1;
+            q.inv_ow = q.inv_oh = q.inv_pr = q.inv_wp = q.inv_sr = q.inv_rpb = 0.0f;
             q.ps = t.bm * 16 + 16;                      // one plane of 8 consecutive k
             q.units = t.bm * 2 * p->cm;                 // (token, plane)
             q.total_rows = 0;

@@ -341,6 +341,21 @@ def test_predecoded_formats(spec):
     assert err <= 2e-3
 
 
+@pytest.mark.parametrize("spec", [f for f in FUSED + KAQ if f.conv is not None], ids=lambda s: s.name)
+def test_fused_conv_row_staging(spec, monkeypatch):
+    """Input rows staged once per image block fill the fragments exactly as kh rows per output row do."""
+    inp = generate(spec, 78)
+    for rec in ("0", "1"):
+        monkeypatch.setenv("AQ_FUSED_REC", rec)
+        y_once = _run(spec, inp, "decode")
+        monkeypatch.setenv("AQ_FUSED_ROWS", "each")
+        y_each = _run(spec, inp, "decode")
+        monkeypatch.delenv("AQ_FUSED_ROWS")
+        _say(f"row staging {spec.name} rec={rec} identical={np.array_equal(y_once, y_each)}")
+        assert np.array_equal(y_once, y_each)
+    assert O.rel_err_inf(y_once, O.forward(spec, inp)) <= 2e-3
+
+
 def test_kaq_codebook_doubling_is_exact():
     """g = 9: codebook values on a 2^-10 grid make every decode exact, so Y(2C) == 2 Y(C) bitwise."""
     spec = LayerSpec(name="kaq_alpha", C_out=48, K=32 * 9, g=9, M=2, B=8, n=2, y_dtype="f32",
