@@ -494,6 +494,76 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         for (int i = 0; i < CB_PER_T; ++i) reinterpret_cast<u32x4*>(cb_lds)[tid + 256 * i] = cbr[i];
     }
     lds_barrier();   // codebook and padding visible (global loads stay in flight)
+    if constexpr (DEC == FUSED_DEC_REC) {
+        // Pre-decoded operands, steps outermost.  Each step's activation
+        // fragments are read from LDS one step ahead of its products (two steps
+        // of registers instead of a whole chunk's), the records of every channel
+        // block of a step are loaded a chunk ahead into two register sets (chunk
+        // parity P, static), and the next chunk is staged mid-chunk: the products
+        // never drain at a chunk end.  Loads past the last chunk read zeros.
+        u32x4 rec[2][NS][AN];
+        u32x4 afb[2][AM];
+        auto rec_step = [&](u32x4 (&dst)[AN], int c, int s) {
+            const bool cv = c < plan.nchunk;
+#pragma unroll
+            for (int b = 0; b < AN; ++b) {
+                const uint32_t base = (uint32_t)(((c * NS + s) * geo.C_out + N0 + 32 * b + l32) * 2 + q) * 16u;
+                dst[b] = __builtin_amdgcn_raw_buffer_load_b128(wr, c_ok[b] & cv ? base : kOutOfRange, 0, 0);
+            }
+        };
+        auto frag_step = [&](const uint8_t* buf, u32x4 (&dst)[AM], int s) {
+            uint32_t soff;
+            if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
+            else soff = (uint32_t)(2 * s * plan.ps);
+#pragma unroll
+            for (int a = 0; a < AM; ++a) dst[a] = *reinterpret_cast<const u32x4*>(buf + a_base[a] + soff);
+        };
+#pragma unroll
+        for (int s = 0; s < NS; ++s) rec_step(rec[0][s], chunk, s);
+        stage_store(pbuf0);
+        wave_sync();
+        frag_step(pbuf0, afb[0], 0);
+        // step s of a chunk of parity P uses fragment buffer (s + P NS) & 1, so
+        // the buffers alternate across chunk boundaries for odd NS too
+        auto body = [&](auto pc, int c) {
+            constexpr int P = decltype(pc)::value;
+            const uint8_t* cur = P ? pbuf1 : pbuf0;
+            uint8_t* nxt = P ? pbuf0 : pbuf1;
+            stage_load(c + kWaves);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                rec_step(rec[1 - P][s], c + kWaves, s);
+                if (s == NS / 2) {
+                    wave_sync();
+                    stage_store(nxt);
+                    wave_sync();
+                }
+                if (s + 1 < NS) frag_step(cur, afb[(s + 1 + P * NS) & 1], s + 1);
+                else frag_step(nxt, afb[(s + 1 + P * NS) & 1], 0);
+#pragma unroll
+                for (int b = 0; b < AN; ++b)
+#pragma unroll
+                    for (int a = 0; a < AM; ++a) {
+                        if constexpr (CONV) acc[a][b] = mfma_f16(rec[P][s][b], afb[(s + P * NS) & 1][a], acc[a][b]);
+                        else acc[a][b] = mfma_f16(afb[(s + P * NS) & 1][a], rec[P][s][b], acc[a][b]);
+                    }
+                // each product followed by a share of the loads and fragment reads
+#pragma unroll
+                for (int i = 0; i < AN * AM; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                 // MFMA
+                    if (i < AN) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                    // VMEM read
+                    if (i >= AN * AM - AM) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);         // DS read
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+        for (; chunk + kWaves < plan.nchunk; chunk += 2 * kWaves) {
+            body(std::integral_constant<int, 0>{}, chunk);
+            body(std::integral_constant<int, 1>{}, chunk + kWaves);
+        }
+        if (chunk < plan.nchunk) body(std::integral_constant<int, 0>{}, chunk);
+    } else {
     // A wave without a chunk runs this on zeros, in its own staging buffer;
     // no branch here keeps the loads above from being sunk below the barrier.
     if constexpr (LOOKAHEAD) decode_block(crg[0], chunk, 0, dec);
@@ -579,6 +649,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             }
         }
     }
+
+    }   // in-loop decode
 
     // ---- epilogue: the four partial tiles meet in LDS, interleaved by 4 along
     // the MFMA row so that each lane writes float4s; then every thread sums 8
