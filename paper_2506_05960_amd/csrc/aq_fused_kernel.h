@@ -455,14 +455,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     constexpr bool LOOKAHEAD = DEC != FUSED_DEC_F32L && NS * MC <= 18;
     // weights of one 32-channel block of a chunk, decoded into MFMA operands
     auto decode_block = [&](const uint32_t* codes_dw, int dchunk, int db, u32x4 (&d)[NS]) {
-        if constexpr (DEC == FUSED_DEC_REC) {
-            const bool ok = c_ok[db] && dchunk < plan.nchunk;
-            const uint32_t base = (uint32_t)(((dchunk * NS) * geo.C_out + N0 + 32 * db + l32) * 2 + q) * 16u;
-#pragma unroll
-            for (int g = 0; g < NS; ++g)
-                d[g] = __builtin_amdgcn_raw_buffer_load_b128(
-                    wr, ok ? base + (uint32_t)(g * geo.C_out * 32) : kOutOfRange, 0, 0);
-        } else if constexpr (LOOKAHEAD) {
+        if constexpr (LOOKAHEAD) {
             GroupRaw<DEC, MC> raw[NS];
 #pragma unroll
             for (int g = 0; g < NS; ++g) gather_group<DEC, MC, EntT>(raw[g], codes_dw, g * MC, cb_lds, cb);
@@ -570,11 +563,6 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     stage_store(pbuf0);
     wave_sync();
     load_af(pbuf0, af);
-    // Next-chunk staging inside the last channel block (below) for pre-decoded
-    // operands (conv8: 101.7 -> 97.7 us).  Not with the in-loop decode: its main
-    // loop is bound by LDS codeword gathers, which the staging then competes
-    // with (conv64: 12.1 -> 12.4 us), and with four token blocks it spills.
-    constexpr bool OVL = DEC == FUSED_DEC_REC;
     int it = 0;
     for (; chunk < plan.nchunk; chunk += kWaves, ++it) {
         uint8_t* nxt = (it & 1) ? pbuf0 : pbuf1;
@@ -591,16 +579,6 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
             __builtin_amdgcn_sched_barrier(0);
-            if (OVL && b == AN - 1) {
-                // The next chunk's activations go to the staging buffer this chunk
-                // does not read, and each step's fragments are read back right
-                // after that step's last products (their registers are free from
-                // there on), so neither waits for the products to drain.  Past
-                // the last chunk this moves stale data into the unused buffer.
-                wave_sync();
-                stage_store(nxt);
-                wave_sync();
-            }
             u32x4 dnext[NS];
             bool have_next = false;
             if constexpr (LOOKAHEAD) {
@@ -632,7 +610,6 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                     if constexpr (CONV) acc[a][b] = mfma_f16(bf, af[s][a], acc[a][b]);   // rows: channels
                     else acc[a][b] = mfma_f16(af[s][a], bf, acc[a][b]);                  // rows: tokens
                 }
-                if (OVL && b == AN - 1) load_af_step(nxt, af, s);
             }
             if (have_next) {
 #pragma unroll
@@ -640,13 +617,11 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             }
         }
         __builtin_amdgcn_sched_barrier(0);
-        if constexpr (!OVL) {
-            if (more) {
-                wave_sync();
-                stage_store(nxt);
-                wave_sync();
-                load_af(nxt, af);
-            }
+        if (more) {
+            wave_sync();
+            stage_store(nxt);
+            wave_sync();
+            load_af(nxt, af);
         }
     }
 

@@ -425,7 +425,15 @@ bool use_predecoded(const aq_layer* L, const Geom& geo) {
     // measured on the U-Net layer shapes: the in-loop decode is repeated for every
     // token tile, so the single decode pass wins once tokens x M is large enough
     const int64_t tm = geo.tokens * p.mc;
-    if (p.kind == 1) return tm >= 32768 || (tm >= 8192 && geo.K >= 5000);
+    if (p.kind == 1) {
+        // 3x3 convolutions of the U-Net shapes (both routes timed per shape): with
+        // M = 4 the pre-decoded route won on every shape from 512 tokens up; with
+        // M = 2 once the reduction is long for the token count (conv64, 8192
+        // tokens x K = 1728, stays in-loop: 13.5 vs 15.1 us)
+        if (p.mc >= 4 && geo.tokens >= 512) return true;
+        return tm >= 32768 || (geo.K >= 3456 && geo.tokens >= 8192) || (geo.K >= 5000 && geo.tokens >= 2048) ||
+               geo.K >= 13000;
+    }
     if (p.kind == 0) {
         if (aq::rec_linear_supported(geo, p, L->desc.x_dtype)) {
             // the wave-split product over records (measured on the U-Net linear shapes):
