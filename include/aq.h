@@ -10,18 +10,30 @@
  *     W[i][j*g + t] = s[i] * sum_{m<M} C[m][ b[i][j][m] ][t]
  *
  * with M codebooks C[m] of 2^B rows of g values and one scale s[i] per output
- * channel.  The forward computes Y = X * W^T (tokens as rows) without ever
- * writing W to memory.  A convolution runs on NCHW input; its token order is
- * (image, output row, output column) and its K order is (input channel,
- * kernel row, kernel column) with the channel outermost (Sec. 3.1.1).
+ * channel.  The forward computes Y = X * W^T (tokens as rows).  A convolution
+ * runs on NCHW input; its token order is (image, output row, output column)
+ * and its K order is (input channel, kernel row, kernel column) with the
+ * channel outermost (Sec. 3.1.1).
  *
  * Two device paths implement the forward:
  *   - LUT: per token and group, tabulate x_g . C[m][k] for every codeword k,
  *     then sum code-indexed table entries (the appendix's rearrangement,
- *     eq. (12)).  Needs B <= 8.
- *   - DECODE: expand code tiles into fp16/bf16 (or fp32) weight tiles on chip
- *     and contract them with matrix-core instructions.
- * aq_layer_forward picks one per call (AQ_PATH_AUTO) unless a path is forced.
+ *     eq. (12)).  Needs B <= 8.  W is never formed.
+ *   - DECODE: expand codes into fp16/bf16 (or fp32) weight operands and
+ *     contract them with matrix-core instructions.  Its weights come from one
+ *     of two sources:
+ *       * in-loop decode: each workgroup decodes its weight tile on chip
+ *         (registers / LDS) right before the products; W never reaches
+ *         memory;
+ *       * pre-decoded records: a first kernel writes the unscaled decoded
+ *         weights, C_out * K fp16 values (2 * C_out * K bytes), to a
+ *         layer-owned buffer, which the product kernel then reads.  This is
+ *         the paper's decompress-then-compute route (Sec. 4.4), with the
+ *         decompressed weights a per-forward temporary.
+ *     The dispatcher takes the records per layer shape where they measured
+ *     faster (formats without an in-loop decode always take them);
+ *     AQ_OPT_WEIGHTS forces either source.
+ * aq_layer_forward picks a path per call (AQ_PATH_AUTO) unless one is forced.
  *
  * Conventions for every entry point:
  *   - Return value is an aq_status; nothing aborts or throws across the ABI.
@@ -88,8 +100,9 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
 
 /*
  * Forward Y = X * W^T on `stream`; asynchronous, allocates nothing and never
- * synchronises.  The layer's workspace makes concurrent forwards on one layer
- * a race: serialise them on one stream.
+ * synchronises.  The layer's workspace (table partial sums, pre-decoded
+ * records, split-K partial tiles and arrival counters) makes concurrent
+ * forwards on one layer a race: serialise them on one stream.
  *   X          device; linear: [n][K] row-major; conv: NCHW [n][cin][in_h][in_w];
  *              dtype desc->x_dtype; 16-byte aligned
  *   x_scales   device [n] fp32 per-token scales, required iff x_dtype == I8
@@ -108,7 +121,8 @@ aq_status aq_layer_forward(aq_layer* layer, const void* X, const float* x_scales
  * when both codebooks and tile are fp16, otherwise in fp32 -- then times s[i]
  * in fp32, then one round-to-nearest-even to the tile dtype.  (For M <= 2
  * the fp16 sum equals the fp32 sum rounded once.)  Asynchronous on `stream`.
- * A test hook for bit-exact checks; the forward never materialises W.
+ * A test hook for bit-exact checks (the pre-decoded records of the forward
+ * hold the same values before the scale, in the matrix-core operand order).
  */
 aq_status aq_layer_decode(aq_layer* layer, void* W, void* stream);
 
@@ -142,6 +156,69 @@ aq_status aq_layer_codebook_grad(aq_layer* layer, const void* X, const void* dY,
 /* Force a path for later forwards (AUTO restores the dispatcher).  Forcing an
  * unavailable path returns AQ_ERR_UNSUPPORTED and leaves the setting as is. */
 aq_status aq_layer_set_path(aq_layer* layer, aq_path path);
+
+/*
+ * Per-layer options of the dispatcher and planners, for benchmarks and tests
+ * that compare routes.  Every option defaults to 0 (the measured rule) unless
+ * stated; setting 0 restores the default.  The library reads no environment
+ * variables.  Options are read on the host at each call; setting one while a
+ * forward of the same layer is being issued on another thread is a race.
+ * Forward results are identical across routes only where the entry says so.
+ *   AQ_OPT_LUT_MAX_TOKENS   table path for tokens <= value when both paths
+ *                           exist; 0 = the measured rule, -1 = never
+ *   AQ_OPT_WEIGHTS          decode path weight source: 0 auto, 1 in-loop
+ *                           decode (W never in memory), 2 pre-decoded
+ *                           records (W written per forward); formats with
+ *                           no in-loop decode (g = 9, M not in {1, 2, 4},
+ *                           fp32/bf16 codebooks) always take the records
+ *   AQ_OPT_GENERIC          1 = generic decode kernel instead of the fused
+ *                           decode kernel (0: fused kernel where it applies)
+ *   AQ_OPT_RECORD_PRODUCT   product kernel over records: 0 auto (linear
+ *                           layers: the wave-split linear kernel), 1 the
+ *                           fused kernel's own pre-decoded loop (outputs
+ *                           bit-identical to its in-loop decode), 2 the
+ *                           dense product with both operands staged in LDS
+ *   AQ_OPT_FUSED_TILE       fused kernel tile BM * 1000 + BN (0 = planner);
+ *                           a tile that does not fit falls back to the planner
+ *   AQ_OPT_DENSE_TILE       dense product tile BM * 1000 + BN (0 = planner)
+ *   AQ_OPT_REC_LINEAR_TILE  wave-split linear kernel: 0 = 128 x 128 in 2 x 2
+ *                           waves, 1 = 256 x 128 in 2 x 2, 2 = 128 x 128 in
+ *                           1 x 4 (bit-identical outputs)
+ *   AQ_OPT_TILE_ORDER       workgroup order: 0 auto, 1 token tiles slowest,
+ *                           2 channel tiles slowest (bit-identical outputs)
+ *   AQ_OPT_STAGE_ROWS       convolution staging: 0 each input row once per
+ *                           block of output rows, 1 kh rows per output row
+ *                           (bit-identical outputs)
+ *   AQ_OPT_SPLIT_K          fused kernel: workgroups sharing one output tile
+ *                           along K (0 = planner, 1 = none, up to 8); partial
+ *                           tiles are summed in a fixed order, so repeated
+ *                           runs are bitwise identical
+ *   AQ_OPT_GRAD_SPLITS      codebook gradient: most token splits (0 = planner)
+ *   AQ_OPT_GRAD_REGS        codebook gradient: 1 = register-staged kernels
+ *                           (0: direct-to-LDS kernels where they apply)
+ *   AQ_OPT_GRAD_TILE        codebook gradient tile BM * 1000 + BN (0 = planner)
+ * The gradient options take effect at the next gradient call; if they need a
+ * larger partial-gradient workspace, that call reallocates it (synchronous).
+ * Unknown options or out-of-range values return AQ_ERR_INVALID_ARGUMENT.
+ */
+typedef enum {
+    AQ_OPT_LUT_MAX_TOKENS = 1,
+    AQ_OPT_WEIGHTS = 2,
+    AQ_OPT_GENERIC = 3,
+    AQ_OPT_RECORD_PRODUCT = 4,
+    AQ_OPT_FUSED_TILE = 5,
+    AQ_OPT_DENSE_TILE = 6,
+    AQ_OPT_REC_LINEAR_TILE = 7,
+    AQ_OPT_TILE_ORDER = 8,
+    AQ_OPT_STAGE_ROWS = 9,
+    AQ_OPT_SPLIT_K = 10,
+    AQ_OPT_GRAD_SPLITS = 11,
+    AQ_OPT_GRAD_REGS = 12,
+    AQ_OPT_GRAD_TILE = 13
+} aq_option;
+
+aq_status aq_layer_set_option(aq_layer* layer, int32_t option, int64_t value);
+aq_status aq_layer_get_option(const aq_layer* layer, int32_t option, int64_t* value);
 
 /* The path a forward over `tokens` tokens would take (pure host function). */
 aq_status aq_layer_choose_path(const aq_layer* layer, int64_t tokens, aq_path* out);

@@ -18,6 +18,10 @@ from .aq_oracle import (  # noqa: F401
     f32_to_bf16_bits,
     bf16_bits_to_f32,
     rel_err_inf,
+    rel_err_rms,
+    rel_err_elem,
+    abs_inputs,
+    rounding_bound,
     dense_conv_flops,
     lut_conv_flops,
     lut_breakpoint_cout,

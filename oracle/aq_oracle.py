@@ -250,7 +250,8 @@ def decode_emulate(codebooks: np.ndarray, codes: np.ndarray, scales: np.ndarray,
 
 
 # ---------------------------------------------------------------------------
-# O6: error metric
+# O6: error metrics (whole-output infinity-norm and RMS, per-element with an
+# RMS floor, and a per-element rounding bound)
 # ---------------------------------------------------------------------------
 
 def rel_err_inf(y: np.ndarray, y_ref: np.ndarray) -> float:
@@ -261,6 +262,74 @@ def rel_err_inf(y: np.ndarray, y_ref: np.ndarray) -> float:
     if den == 0.0:
         return float(np.max(np.abs(y)))
     return float(np.max(np.abs(y - y_ref)) / den)
+
+
+def rel_err_rms(y: np.ndarray, y_ref: np.ndarray) -> float:
+    """||y - y_ref||_2 / ||y_ref||_2 over the whole output (RMS-relative error)."""
+    y = np.asarray(y, dtype=np.float64)
+    y_ref = np.asarray(y_ref, dtype=np.float64)
+    den = np.sqrt(np.mean(y_ref * y_ref))
+    num = np.sqrt(np.mean((y - y_ref) ** 2))
+    return float(num if den == 0.0 else num / den)
+
+
+def rel_err_elem(y: np.ndarray, y_ref: np.ndarray, floor: float = 1e-3) -> float:
+    """max_i |y_i - y_ref_i| / max(|y_ref_i|, floor * rms(y_ref)): the worst
+    per-element relative error, each element judged against its own magnitude
+    but never against less than ``floor`` times the output's RMS."""
+    y = np.asarray(y, dtype=np.float64)
+    y_ref = np.asarray(y_ref, dtype=np.float64)
+    rms = np.sqrt(np.mean(y_ref * y_ref))
+    den = np.maximum(np.abs(y_ref), floor * rms)
+    den = np.where(den == 0.0, 1.0, den)
+    return float(np.max(np.abs(y - y_ref) / den))
+
+
+def abs_inputs(spec, inputs) -> dict:
+    """The same layer with every codebook value, scale and activation replaced
+    by its magnitude.  Its forward is A[n, i] = sum_k |x[n, k]| |W[i, k]| with
+    |W[i, k]| taken as s_i * sum_m |C[m, b, t]| (never smaller than |W|): the
+    quantity that bounds every rounding error of a computed product."""
+    cb = np.asarray(inputs["codebooks"])
+    if spec.codebook_dtype == "bf16":
+        cb_abs = (cb.astype(np.uint16) & np.uint16(0x7FFF)).astype(np.uint16)
+    else:
+        cb_abs = np.abs(cb)
+    x = np.asarray(inputs["x"])
+    x_abs = (x.astype(np.uint16) & np.uint16(0x7FFF)).astype(np.uint16) if spec.x_dtype == "bf16" else np.abs(x)
+    xs = inputs.get("x_scales")
+    return {"codebooks": cb_abs, "codes": inputs["codes"], "scales": np.abs(np.asarray(inputs["scales"])),
+            "x": x_abs, "x_scales": None if xs is None else np.abs(np.asarray(xs))}
+
+
+_UNIT = {"f16": 2.0 ** -11, "bf16": 2.0 ** -8, "f32": 2.0 ** -24}
+
+
+def rounding_bound(spec, y_ref: np.ndarray, a_ref: np.ndarray, path: str) -> np.ndarray:
+    """Per-element bound on |y - y_ref| for a correctly rounded computation.
+
+    ``y_ref`` is the exact output and ``a_ref`` the forward of
+    ``abs_inputs`` at the same positions.  A computed output can differ from
+    the exact one only by rounding:
+    * the decoded weight (path "decode"): M codewords summed with at most M-1
+      roundings, times the scale, rounded once to the tile dtype, so
+      |w_hat - w| <= M u_tile (1 + eps) s_i sum_m |C_m|;
+    * the products and the fp32 sums over K (and, on the table path, over the
+      g values of a table entry and the G M gathered entries), the scale and
+      the int8 activation scale: an fp32 sum of n terms errs by at most
+      gamma_n = n 2^-24 / (1 - n 2^-24) times the sum of their magnitudes;
+    * the output rounding u_out |y|.
+    Hence |y - y_ref| <= u_out |y_ref| + (1 + u_out) (M u_tile + gamma_n) a_ref
+    (with a 1% margin on the second term), for every element.  fp16 and bf16
+    activations and their products with fp16 weights are exact in fp32.
+    """
+    u_out = _UNIT[spec.y_dtype]
+    u_tile = _UNIT[spec.tile_dtype] if path == "decode" else 0.0
+    n = spec.K + spec.G * spec.M + spec.g + spec.M + 8
+    e32 = 2.0 ** -24
+    gamma = n * e32 / (1.0 - n * e32)
+    a = np.asarray(a_ref, dtype=np.float64)
+    return u_out * np.abs(np.asarray(y_ref, dtype=np.float64)) + (1.0 + u_out) * 1.01 * (spec.M * u_tile + gamma) * a
 
 
 # ---------------------------------------------------------------------------

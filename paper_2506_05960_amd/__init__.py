@@ -16,6 +16,9 @@ from .aq import (  # noqa: F401
     aq_layer_decode,
     aq_layer_codebook_grad,
     aq_layer_set_path,
+    aq_layer_set_option,
+    aq_layer_get_option,
+    OPTION_CODES,
     aq_layer_choose_path,
     aq_layer_destroy,
     aq_version,

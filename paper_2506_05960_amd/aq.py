@@ -23,9 +23,15 @@ PATH_CODES = {"auto": AQ_PATH_AUTO, "lut": AQ_PATH_LUT, "decode": AQ_PATH_DECODE
 PATH_NAMES = {v: k for k, v in PATH_CODES.items()}
 STATUS_NAMES = {0: "AQ_OK", 1: "AQ_ERR_INVALID_ARGUMENT", 2: "AQ_ERR_UNSUPPORTED", 3: "AQ_ERR_OUT_OF_MEMORY",
                 4: "AQ_ERR_DEVICE"}
+# aq_option (include/aq.h)
+OPTION_CODES = {"lut_max_tokens": 1, "weights": 2, "generic": 3, "record_product": 4, "fused_tile": 5,
+                "dense_tile": 6, "rec_linear_tile": 7, "tile_order": 8, "stage_rows": 9, "split_k": 10,
+                "grad_splits": 11, "grad_regs": 12, "grad_tile": 13}
+_TILE_OPTIONS = ("fused_tile", "dense_tile", "grad_tile")
 
 EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
-            "aq_layer_set_path", "aq_layer_choose_path", "aq_layer_destroy", "aq_last_error", "aq_version")
+            "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_choose_path",
+            "aq_layer_destroy", "aq_last_error", "aq_version")
 
 
 class AQError(RuntimeError):
@@ -71,10 +77,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_decode.argtypes = [vp, vp, vp]
     lib.aq_layer_codebook_grad.argtypes = [vp, vp, vp, i32, vp, i64, vp]
     lib.aq_layer_set_path.argtypes = [vp, i32]
+    lib.aq_layer_set_option.argtypes = [vp, i32, i64]
+    lib.aq_layer_get_option.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_int64)]
     lib.aq_layer_choose_path.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_int)]
     lib.aq_layer_destroy.argtypes = [vp]
     for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
-              "aq_layer_set_path", "aq_layer_choose_path", "aq_layer_destroy"):
+              "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_choose_path",
+              "aq_layer_destroy"):
         getattr(lib, f).restype = ctypes.c_int
     lib.aq_last_error.restype = ctypes.c_char_p
     lib.aq_last_error.argtypes = []
@@ -134,6 +143,16 @@ def aq_layer_set_path(handle: int, path: str) -> None:
     _check(load_library().aq_layer_set_path(handle, PATH_CODES[path]))
 
 
+def aq_layer_set_option(handle: int, option: int, value: int) -> None:
+    _check(load_library().aq_layer_set_option(handle, option, value))
+
+
+def aq_layer_get_option(handle: int, option: int) -> int:
+    out = ctypes.c_int64()
+    _check(load_library().aq_layer_get_option(handle, option, ctypes.byref(out)))
+    return out.value
+
+
 def aq_layer_choose_path(handle: int, tokens: int) -> str:
     out = ctypes.c_int()
     _check(load_library().aq_layer_choose_path(handle, tokens, ctypes.byref(out)))
@@ -150,12 +169,34 @@ def aq_version() -> str:
 
 # ---- convenience object over the same calls ----
 
-_TORCH_DT = None
+def _torch_dtypes(name: str):
+    """torch dtypes accepted for a storage dtype (bf16 also as its int16 bit pattern)."""
+    import torch
+    return {"f32": (torch.float32,), "f16": (torch.float16,), "bf16": (torch.bfloat16, torch.int16),
+            "i8": (torch.int8,)}[name]
 
 
 def _torch_dtype(name: str):
+    return _torch_dtypes(name)[0]
+
+
+_NP_DTYPES = {"f32": (np.float32,), "f16": (np.float16,), "bf16": (np.uint16, np.int16)}
+_DEVICE_TYPE = "cuda"   # where every tensor argument must live (host-side tests of the checks change it)
+
+
+def _check_tensor(what: str, t, dtypes, shape, device) -> None:
+    """ValueError unless ``t`` is a contiguous device tensor of one of ``dtypes`` and exactly ``shape``."""
     import torch
-    return {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16, "i8": torch.int8}[name]
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{what} must be a torch tensor, got {type(t).__name__}")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{what} must have dtype {' or '.join(str(d) for d in dtypes)}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    if t.device.type != _DEVICE_TYPE or (device is not None and t.device.index != device):
+        raise ValueError(f"{what} must be on {_DEVICE_TYPE}:{device}, got {t.device}")
 
 
 class AQLayer:
@@ -163,15 +204,34 @@ class AQLayer:
 
     ``spec`` carries C_out, K, g, M, B, the dtypes and ``conv`` geometry (or
     None); ``inputs`` carries host numpy ``codebooks``, ``codes`` and ``scales``.
+    Every tensor argument is checked (dtype, exact shape, contiguity, device)
+    before the library is called: the C ABI cannot see buffer extents.
     """
 
     def __init__(self, spec, inputs, max_tokens: Optional[int] = None):
         self.spec = spec
-        mt = max_tokens if max_tokens is not None else spec.tokens
-        self.desc = make_desc(spec.C_out, spec.K, spec.codebook_dtype, spec.x_dtype, spec.y_dtype,
-                              spec.tile_dtype, mt, spec.conv)
-        self.handle = aq_layer_create(self.desc, inputs["codebooks"], inputs["codes"], inputs["scales"],
-                                      spec.g, spec.M, spec.B)
+        s = spec
+        mt = max_tokens if max_tokens is not None else s.tokens
+        cb = np.asarray(inputs["codebooks"])
+        if cb.shape != (s.M, 1 << s.B, s.g):
+            raise ValueError(f"codebooks must have shape {(s.M, 1 << s.B, s.g)}, got {cb.shape}")
+        if cb.dtype.type not in _NP_DTYPES[s.codebook_dtype]:
+            raise ValueError(f"codebooks must be {s.codebook_dtype} storage, got {cb.dtype}")
+        codes = np.asarray(inputs["codes"])
+        if codes.shape != (s.C_out, s.K // s.g, s.M):
+            raise ValueError(f"codes must have shape {(s.C_out, s.K // s.g, s.M)}, got {codes.shape}")
+        if not np.issubdtype(codes.dtype, np.integer):
+            raise ValueError(f"codes must be integers, got {codes.dtype}")
+        if codes.size and (int(codes.min()) < 0 or int(codes.max()) >= (1 << s.B)):
+            raise ValueError(f"codes must lie in [0, 2^{s.B})")
+        codes = codes.astype(np.uint8 if s.B <= 8 else np.uint16, copy=False)
+        scales = np.asarray(inputs["scales"])
+        if scales.shape != (s.C_out,):
+            raise ValueError(f"scales must have shape {(s.C_out,)}, got {scales.shape}")
+        self.desc = make_desc(s.C_out, s.K, s.codebook_dtype, s.x_dtype, s.y_dtype, s.tile_dtype, mt, s.conv)
+        import torch
+        self.device = torch.cuda.current_device() if torch.cuda.is_available() else None
+        self.handle = aq_layer_create(self.desc, cb, codes, scales, s.g, s.M, s.B)
 
     def out_shape(self, n: int):
         s = self.spec
@@ -179,12 +239,33 @@ class AQLayer:
             return (n, s.C_out)
         return (n, s.C_out, s.conv.OH, s.conv.OW)
 
+    def in_shape(self, n: int):
+        s = self.spec
+        if s.conv is None:
+            return (n, s.K)
+        return (n, s.conv.cin, s.conv.H, s.conv.W)
+
+    def tokens(self, n: int) -> int:
+        s = self.spec
+        return n if s.conv is None else n * s.conv.OH * s.conv.OW
+
     def forward(self, x, x_scales=None, out=None, stream=None):
         """Y for device tensor ``x`` (token-major [n, K] or NCHW); returns ``out``."""
         import torch
+        s = self.spec
+        if not isinstance(x, torch.Tensor) or x.dim() < 1 or x.shape[0] < 1:
+            raise ValueError("x must be a torch tensor with at least one row or image")
         n = x.shape[0]
+        _check_tensor("x", x, _torch_dtypes(s.x_dtype), self.in_shape(n), self.device)
+        if s.x_dtype == "i8":
+            if x_scales is None:
+                raise ValueError("int8 activations need x_scales")
+            _check_tensor("x_scales", x_scales, (torch.float32,), (self.tokens(n),), self.device)
+        elif x_scales is not None:
+            raise ValueError("x_scales apply to int8 activations only")
         if out is None:
-            out = torch.empty(self.out_shape(n), dtype=_torch_dtype(self.spec.y_dtype), device=x.device)
+            out = torch.empty(self.out_shape(n), dtype=_torch_dtype(s.y_dtype), device=x.device)
+        _check_tensor("out", out, _torch_dtypes(s.y_dtype), self.out_shape(n), self.device)
         st = stream if stream is not None else torch.cuda.current_stream(x.device).cuda_stream
         xs = 0 if x_scales is None else x_scales.data_ptr()
         aq_layer_forward(self.handle, x.data_ptr(), xs, out.data_ptr(), n, st)
@@ -195,9 +276,10 @@ class AQLayer:
     def decode(self, out=None, stream=None):
         import torch
         s = self.spec
-        dt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.int16}[s.tile_dtype]
+        dts = {"f32": (torch.float32,), "f16": (torch.float16,), "bf16": (torch.int16, torch.bfloat16)}[s.tile_dtype]
         if out is None:
-            out = torch.empty((s.C_out, s.K), dtype=dt, device="cuda")
+            out = torch.empty((s.C_out, s.K), dtype=dts[0], device=f"cuda:{self.device}")
+        _check_tensor("out", out, dts, (s.C_out, s.K), self.device)
         st = stream if stream is not None else torch.cuda.current_stream().cuda_stream
         aq_layer_decode(self.handle, out.data_ptr(), st)
         return out
@@ -206,17 +288,37 @@ class AQLayer:
         """dC [M, 2**B, g] fp32 for input ``x`` and output gradient ``dy`` (both fp16 or bf16 device tensors)."""
         import torch
         s = self.spec
+        if not isinstance(x, torch.Tensor) or not isinstance(dy, torch.Tensor):
+            raise ValueError("x and dy must be torch tensors")
         if x.dtype != dy.dtype or x.dtype not in (torch.float16, torch.bfloat16):
             raise ValueError("x and dy must share one dtype, float16 or bfloat16")
+        if x.dim() < 1 or x.shape[0] < 1:
+            raise ValueError("x must have at least one row or image")
+        n = x.shape[0]
+        _check_tensor("x", x, (x.dtype,), self.in_shape(n), self.device)
+        _check_tensor("dy", dy, (x.dtype,), self.out_shape(n), self.device)
         if out is None:
             out = torch.empty((s.M, 1 << s.B, s.g), dtype=torch.float32, device=x.device)
+        _check_tensor("out", out, (torch.float32,), (s.M, 1 << s.B, s.g), self.device)
         st = stream if stream is not None else torch.cuda.current_stream(x.device).cuda_stream
         dt = "f16" if x.dtype == torch.float16 else "bf16"
-        aq_layer_codebook_grad(self.handle, x.data_ptr(), dy.data_ptr(), dt, out.data_ptr(), x.shape[0], st)
+        aq_layer_codebook_grad(self.handle, x.data_ptr(), dy.data_ptr(), dt, out.data_ptr(), n, st)
         return out
 
     def set_path(self, path: str) -> None:
         aq_layer_set_path(self.handle, path)
+
+    def set_option(self, name: str, value) -> None:
+        """Set an ``aq_option`` by name; tile options also take ``"BMxBN"`` strings."""
+        if name not in OPTION_CODES:
+            raise ValueError(f"unknown option {name!r}; known: {sorted(OPTION_CODES)}")
+        if name in _TILE_OPTIONS and isinstance(value, str):
+            bm, bn = (int(v) for v in value.split("x"))
+            value = bm * 1000 + bn
+        aq_layer_set_option(self.handle, OPTION_CODES[name], int(value))
+
+    def get_option(self, name: str) -> int:
+        return aq_layer_get_option(self.handle, OPTION_CODES[name])
 
     def choose_path(self, tokens: int) -> str:
         return aq_layer_choose_path(self.handle, tokens)

@@ -776,13 +776,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
 template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL, int OCC = 1>
 static hipError_t fused_launch_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
     auto kern = fused_fwd_kernel<KIND, CM, XT, DEC, MC, BM, BN, UPL, OCC>;
-    static size_t attr_bytes = 0;
-    if (plan.lds_bytes > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)plan.lds_bytes);
-        if (e != hipSuccess) return e;
-        attr_bytes = plan.lds_bytes;
-    }
+    hipError_t e = ensure_dynamic_lds((const void*)kern, plan.lds_bytes);
+    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN)));
     kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.cb, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y,
                                                    fl.y_dtype);

@@ -720,9 +720,8 @@ hipError_t wgrad_dispatch(const Geom& geo, const GradPlan& gp, const GradArgs& g
 
 // Linear layers, and convolutions whose 64-token chunks are whole output rows
 // of one image, take the direct-to-LDS kernels.
-static bool grad_dma_ok(const Geom& geo) {
-    if (const char* e = std::getenv("AQ_GRAD_DMA"))
-        if (std::atoi(e) == 0) return false;
+static bool grad_dma_ok(const Geom& geo, const Options& opt) {
+    if (opt.grad_regs) return false;
     if (!geo.conv) return true;                  // linear: C_out and K are multiples of 8
     if (geo.stride != 1 || geo.OW != geo.W || geo.OH != geo.H || geo.W % 8 != 0) return false;
     return 64 % geo.OW == 0 && ((int64_t)geo.OH * geo.OW) % 64 == 0;
@@ -732,11 +731,10 @@ static bool grad_dma_ok(const Geom& geo) {
 // workgroup per CU, then token splits up to about four workgroups per CU
 // while the partial gradients stay within 32 MiB (each split adds a full
 // C_out x K fp32 partial to write and to sum).
-GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens) {
+GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens, const Options& opt) {
     GradPlan gp{};
-    gp.dma = grad_dma_ok(geo);
-    int want_bm = 0, want_bn = 0;
-    if (const char* e = std::getenv("AQ_GRAD_TILE")) std::sscanf(e, "%dx%d", &want_bm, &want_bn);
+    gp.dma = grad_dma_ok(geo, opt);
+    const int want_bm = opt.grad_bm, want_bn = opt.grad_bn;
     if (gp.dma && !geo.conv) {
         gp.bm = gp.bn = 64;
         gp.tiles_m = (geo.C_out + 63) / 64;
@@ -778,7 +776,7 @@ GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens) {
     const int64_t slice = (int64_t)geo.C_out * geo.K * 4;
     gp.s_max = (int)std::min<int64_t>({16, nchunk, std::max<int64_t>(1, (960 + tiles - 1) / tiles),
                                        std::max<int64_t>(1, (int64_t(32) << 20) / slice)});
-    if (const char* e = std::getenv("AQ_GRAD_SPLITS")) gp.s_max = (int)std::min<int64_t>({16, nchunk, std::max(1, std::atoi(e))});
+    if (opt.grad_splits > 0) gp.s_max = (int)std::min<int64_t>({16, nchunk, (int64_t)opt.grad_splits});
     return gp;
 }
 

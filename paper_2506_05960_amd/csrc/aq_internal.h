@@ -20,6 +20,29 @@ struct Geom {
     int cin, kh, kw, stride, pad, H, W, OH, OW;
 };
 
+// Per-layer route options (aq_layer_set_option); 0 everywhere is the default.
+struct Options {
+    int64_t lut_max_tokens;   // 0: the measured rule, -1: never, else the token limit
+    int weights;              // 0 auto, 1 in-loop decode, 2 pre-decoded records
+    int generic;              // 1: generic decode kernel instead of the fused kernel
+    int rec_product;          // 0 auto, 1 fused kernel's pre-decoded loop, 2 dense product
+    int fused_bm, fused_bn;   // forced fused tile (0: planner)
+    int dense_bm, dense_bn;   // forced dense-product tile (0: planner)
+    int rlin_tile;            // wave-split linear kernel tile variant (0, 1, 2)
+    int tile_order;           // 0 auto, 1 token tiles slowest, 2 channel tiles slowest
+    int stage_rows;           // 1: kh staged rows per output row
+    int split_k;              // fused kernel K split over workgroups (0: planner)
+    int grad_splits;          // codebook gradient token splits (0: planner)
+    int grad_regs;            // 1: register-staged weight-gradient kernels
+    int grad_bm, grad_bn;     // forced weight-gradient tile (0: planner)
+};
+
+constexpr int kMaxSplitK = 8;   // most workgroups sharing one output tile along K
+
+// Raise a kernel's dynamic-LDS limit to at least `bytes` on the current
+// device (once per kernel and device; thread-safe).
+hipError_t ensure_dynamic_lds(const void* kernel, size_t bytes);
+
 // Device-resident copy of a layer's quantized weights.
 struct DeviceWeights {
     const void* codebooks;        // [M][2^B][g] in codebook dtype
@@ -60,6 +83,7 @@ struct FusedPlan {
     int cb_bytes;         // LDS codebook bytes (0 when read from global memory)
     int rec_only;         // no in-loop decode for this format: always the pre-decoded mode
     int nmajor;           // workgroup order: channel tile slowest (else token tile slowest)
+    int rlin_var;         // wave-split linear kernel tile variant (rec_linear_tile)
     // chosen per forward
     int bm, bn, upl;      // tile and staging units per lane
     int units;            // staging units per chunk
@@ -109,7 +133,7 @@ hipError_t launch_operand_records(const Geom& geo, const FusedPlan& plan, const 
 // Linear layer over pre-decoded operand records (plan.cm == 4): 2 x 2 wave
 // split of a 256- or 128-token by 128-channel tile, no K split.
 bool rec_linear_supported(const Geom& geo, const FusedPlan& plan, int x_dtype);
-int rec_linear_tile(const Geom& geo);
+int rec_linear_tile(const Geom& geo, int forced);
 hipError_t launch_rec_linear(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 hipError_t launch_fused_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 hipError_t launch_fused_conv1(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
@@ -147,7 +171,7 @@ struct GradPlan {
     int s_max;                    // most token splits (partial buffers in the workspace)
 };
 
-GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens);
+GradPlan grad_plan_create(const Geom& geo, int64_t max_tokens, const Options& opt);
 // X, dY: fp16 or bf16 (dtype); P: [s_max][C_out][K] fp32 workspace; offs / ent: the code index
 hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, const void* X, const void* dY,
                                 const float* scales, float* P, const int32_t* offs, const int32_t* ent, float* dC,

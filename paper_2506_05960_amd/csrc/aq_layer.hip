@@ -5,7 +5,10 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <map>
+#include <mutex>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "aq_internal.h"
@@ -37,10 +40,31 @@ struct aq_layer {
     int32_t* d_gidx_offs;     // [M][2^B + 1] list offsets per codebook entry
     int32_t* d_gidx_ent;      // [M][C_out * G] (row, group) pairs i * G + j, sorted by code
     float* d_gpart;           // [s_max][C_out][K] fp32 partial weight gradients
+    bool grad_stale;          // a gradient option changed since the plan was made
+    size_t gpart_bytes;       // bytes allocated at d_gpart
     bool lut_ok, dec_ok, fused_ok;
     aq_path path;
-    int64_t lut_max_tokens;
+    int64_t lut_max_tokens;   // the measured rule for this layer
+    aq::Options opt;
 };
+
+namespace aq {
+
+hipError_t ensure_dynamic_lds(const void* kernel, size_t bytes) {
+    static std::mutex mu;
+    static std::map<std::pair<const void*, int>, size_t> done;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    std::lock_guard<std::mutex> lock(mu);
+    size_t& have = done[{kernel, dev}];
+    if (bytes <= have) return hipSuccess;
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+    if (e == hipSuccess) have = bytes;
+    return e;
+}
+
+}  // namespace aq
 
 namespace {
 
@@ -127,7 +151,9 @@ Geom make_geom(const aq_layer* L, int64_t n) {
 
 aq_path choose(const aq_layer* L, int64_t tokens) {
     if (L->path != AQ_PATH_AUTO) return L->path;
-    if (L->lut_ok && (!L->dec_ok || tokens <= L->lut_max_tokens)) return AQ_PATH_LUT;
+    const int64_t lim = L->opt.lut_max_tokens == 0 ? L->lut_max_tokens : L->opt.lut_max_tokens < 0 ? 0
+                                                                                                     : L->opt.lut_max_tokens;
+    if (L->lut_ok && (!L->dec_ok || tokens <= lim)) return AQ_PATH_LUT;
     return AQ_PATH_DECODE;
 }
 
@@ -257,14 +283,13 @@ struct TileCand {
 
 // Per-forward tile choice; fills the remaining plan fields.  Returns false when
 // no instantiated tile fits (the caller then uses the generic kernel).
-bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
+bool fused_plan_tile(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) {
     static const TileCand conv3[] = {{64, 96, 3}, {64, 64, 3}, {128, 64, 3}, {128, 64, 6}, {64, 64, 6}};
     static const TileCand conv1[] = {{64, 96, 4}, {64, 64, 4}};
     static const TileCand lin[] = {{64, 96, 8}, {64, 64, 8}, {32, 128, 4}, {32, 64, 4}};
     const TileCand* cands = p->kind == 1 ? conv3 : p->kind == 2 ? conv1 : lin;
     const int ncand = p->kind == 1 ? 5 : p->kind == 2 ? 2 : 4;
-    int want_bm = 0, want_bn = 0;
-    if (const char* s = std::getenv("AQ_FUSED_TILE")) std::sscanf(s, "%dx%d", &want_bm, &want_bn);
+    const int want_bm = opt.fused_bm, want_bn = opt.fused_bn;
     double best = 0;
     aq::FusedPlan bestp{};
     bool found = false;
@@ -289,12 +314,11 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
             const int kh = p->kind == 1 ? 3 : 1;
             // Staged rows: each input row once per block of output rows of one image
             // (a tile of whole images, or of consecutive rows of one image), instead
-            // of kh rows per output row, when that stages fewer rows.
-            // AQ_FUSED_ROWS=each keeps kh rows per output row.
+            // of kh rows per output row, when that stages fewer rows (option
+            // AQ_OPT_STAGE_ROWS = 1 keeps kh rows per output row).
             const int img = geo.OH * geo.OW;
             int rpb = 1;
-            const char* rows_env = std::getenv("AQ_FUSED_ROWS");
-            if (!(rows_env && std::strcmp(rows_env, "each") == 0)) {
+            if (opt.stage_rows != 1) {
                 if (t.bm % img == 0) rpb = geo.OH;
                 else if (img % t.bm == 0 && tr > 1) rpb = tr;
             }
@@ -350,6 +374,11 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
             found = true;
         }
     }
+    if (!found && want_bm) {
+        aq::Options o = opt;
+        o.fused_bm = o.fused_bn = 0;      // the forced tile does not fit: the planner's choice
+        return fused_plan_tile(geo, o, p);
+    }
     if (found) *p = bestp;
     return found;
 }
@@ -357,10 +386,9 @@ bool fused_plan_tile(const Geom& geo, aq::FusedPlan* p) {
 // Tile of the dense product over pre-decoded records: the workgroup stages
 // each chunk's activations (all BM tokens) and weight records (BN channels)
 // in two LDS stages.  Returns false when no tile fits.
-bool gemm_plan_tile(const Geom& geo, aq::FusedPlan* p) {
+bool gemm_plan_tile(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) {
     static const TileCand cands[] = {{128, 128, 0}, {128, 64, 0}, {64, 128, 0}};
-    int want_bm = 0, want_bn = 0;
-    if (const char* s = std::getenv("AQ_GEMM_TILE")) std::sscanf(s, "%dx%d", &want_bm, &want_bn);
+    const int want_bm = opt.dense_bm, want_bn = opt.dense_bn;
     double best = 0;
     aq::FusedPlan bestp{};
     bool found = false;
@@ -415,10 +443,10 @@ bool gemm_plan_tile(const Geom& geo, aq::FusedPlan* p) {
 // loop reads with plain 16-byte loads) instead of decoding inside the main
 // loop: chosen for codebooks too large for LDS (their codeword reads from L2
 // repeat for every token tile) once there are enough token tiles to repay the
-// extra pass.  AQ_FUSED_REC=1 / 0 forces it on / off.
+// extra pass.  Option AQ_OPT_WEIGHTS = 2 / 1 forces it on / off.
 bool use_predecoded(const aq_layer* L, const Geom& geo) {
     if (L->fplan.rec_only) return true;
-    if (const char* s = std::getenv("AQ_FUSED_REC")) return std::atoi(s) != 0;
+    if (L->opt.weights != 0) return L->opt.weights == 2;
     const int64_t token_tiles = (geo.tokens + 63) / 64;
     const aq::FusedPlan& p = L->fplan;
     if (p.dec == aq::FUSED_DEC_T16G) return token_tiles >= 8;
@@ -504,7 +532,6 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
     // table path beats the matrix-core path only when K is large enough that
     // the latter's few workgroups each walk a long reduction, up to 16 tokens.
     L->lut_max_tokens = desc->in_features >= 4096 ? 16 : 0;
-    if (const char* s = std::getenv("AQ_LUT_MAX_TOKENS")) L->lut_max_tokens = std::atoll(s);
     e = hipGetDevice(&L->device);
     if (e != hipSuccess) {
         free_layer(L);
@@ -583,10 +610,6 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
     }
 #undef AQ_TRY
 
-    if (const char* s = std::getenv("AQ_PATH")) {
-        if (!std::strcmp(s, "lut") && lut_ok) L->path = AQ_PATH_LUT;
-        else if (!std::strcmp(s, "decode") && dec_ok) L->path = AQ_PATH_DECODE;
-    }
     *out = L;
     return AQ_OK;
 }
@@ -620,16 +643,16 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
             fp.cb_bytes = 0;
         }
         aq::FusedPlan gp = fp;
-        // dense product over the records: a comparator route (AQ_GEMM=1); measured
-        // slower than the fused kernel's pre-decoded mode on every layer shape here
-        const char* ge = std::getenv("AQ_GEMM");
-        const bool gemm = L->fused_ok && fits31 && fp.dec == aq::FUSED_DEC_REC && ge && std::atoi(ge) != 0 &&
-                          gemm_plan_tile(geo, &gp);
-        auto order = [](aq::FusedPlan& q) {
+        const aq::Options& opt = L->opt;
+        // dense product over the records: a comparator route (AQ_OPT_RECORD_PRODUCT = 2);
+        // measured slower than the fused kernel's pre-decoded mode on most layer shapes here
+        const bool gemm = L->fused_ok && fits31 && fp.dec == aq::FUSED_DEC_REC && opt.rec_product == 2 &&
+                          gemm_plan_tile(geo, opt, &gp);
+        auto order = [&opt](aq::FusedPlan& q) {
             // channel-major order for pre-decoded convolution operands; linear layers
             // measured faster token-major (qkv 8192 x 576 -> 1728: 59.5 vs 61.8 us)
             q.nmajor = q.dec == aq::FUSED_DEC_REC && q.kind != 0;
-            if (const char* s = std::getenv("AQ_TILE_ORDER")) q.nmajor = s[0] == 'n';
+            if (opt.tile_order != 0) q.nmajor = opt.tile_order == 2;
         };
         order(fp);
         order(gp);
@@ -638,7 +661,7 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
             const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(L->d_wrec), L->d_scales, X, xs, Y,
                                      d.y_dtype, d.x_dtype, st};
             if (e == hipSuccess) e = aq::launch_rec_gemm(geo, gp, fl, L->d_xpack, L->d_zero);
-        } else if (L->fused_ok && fits31 && !std::getenv("AQ_NO_FUSED") && fused_plan_tile(geo, &fp)) {
+        } else if (L->fused_ok && fits31 && opt.generic != 1 && fused_plan_tile(geo, opt, &fp)) {
             const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
                                 : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
                                                                : L->d_cbtile;
@@ -653,11 +676,11 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
             fp.tile_div = fp.nmajor ? (int)((geo.tokens + fp.bm - 1) / fp.bm) : (geo.C_out + fp.bn - 1) / fp.bn;
             fp.inv_tile_div = 1.0f / (float)fp.tile_div;
             const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
-            // a linear layer's records feed the 2 x 2 wave-split product (AQ_REC_LINEAR=0: the
-            // fused kernel's own pre-decoded mode, whose partial-tile order matches its in-loop mode)
-            const char* rl = std::getenv("AQ_REC_LINEAR");
-            const bool rlin = fp.dec == aq::FUSED_DEC_REC && !(rl && std::atoi(rl) == 0) &&
+            // a linear layer's records feed the 2 x 2 wave-split product (AQ_OPT_RECORD_PRODUCT = 1:
+            // the fused kernel's own pre-decoded mode, whose partial-tile order matches its in-loop mode)
+            const bool rlin = fp.dec == aq::FUSED_DEC_REC && opt.rec_product != 1 &&
                               aq::rec_linear_supported(geo, fp, d.x_dtype);
+            fp.rlin_var = aq::rec_linear_tile(geo, opt.rlin_tile);
             if (e == hipSuccess) e = rlin ? aq::launch_rec_linear(geo, fp, fl) : aq::launch_fused_forward(geo, fp, fl);
         } else if (geo.g == 8) {
             e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
@@ -710,18 +733,14 @@ aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int
         if (e != hipSuccess) return hip_fail(e, "codes readback");
         std::vector<int32_t> offs, ent;
         aq::build_code_index(host.data(), geo.B, geo.C_out, geo.G, geo.M, offs, ent);
-        L->gplan = aq::grad_plan_create(geo, d.max_tokens);
         aq_status s = dev_upload(&L->d_gidx_offs, offs.data(), offs.size() * sizeof(int32_t), "code index");
         if (s == AQ_OK) s = dev_upload(&L->d_gidx_ent, ent.data(), ent.size() * sizeof(int32_t), "code index");
-        if (s == AQ_OK)
-            s = dev_upload(&L->d_gpart, nullptr, (size_t)L->gplan.s_max * geo.C_out * geo.K * sizeof(float),
-                           "gradient workspace");
         if (s == AQ_OK && !L->d_zero) {
             s = dev_upload(&L->d_zero, nullptr, 256, "zero block");
             if (s == AQ_OK && (e = hipMemset(L->d_zero, 0, 256)) != hipSuccess) s = hip_fail(e, "zero block");
         }
         if (s != AQ_OK) {
-            for (void** p : {(void**)&L->d_gidx_offs, (void**)&L->d_gidx_ent, (void**)&L->d_gpart})
+            for (void** p : {(void**)&L->d_gidx_offs, (void**)&L->d_gidx_ent})
                 if (*p) {
                     (void)hipFree(*p);
                     *p = nullptr;
@@ -729,12 +748,31 @@ aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int
             return s;
         }
         L->grad_ready = true;
+        L->grad_stale = true;
     }
-    int splits = 0;
-    if (const char* sv = std::getenv("AQ_GRAD_SPLITS")) splits = std::atoi(sv);
+    if (L->grad_stale) {
+        // plan (again, after a gradient option changed); the partial-gradient
+        // workspace grows when the new plan needs more splits (synchronous)
+        const aq::GradPlan gp = aq::grad_plan_create(geo, d.max_tokens, L->opt);
+        const size_t need = (size_t)gp.s_max * geo.C_out * geo.K * sizeof(float);
+        if (need > L->gpart_bytes) {
+            if (L->d_gpart) {
+                hipError_t e = hipDeviceSynchronize();
+                if (e != hipSuccess) return hip_fail(e, "gradient workspace");
+                (void)hipFree(L->d_gpart);
+                L->d_gpart = nullptr;
+                L->gpart_bytes = 0;
+            }
+            aq_status s = dev_upload(&L->d_gpart, nullptr, need, "gradient workspace");
+            if (s != AQ_OK) return s;
+            L->gpart_bytes = need;
+        }
+        L->gplan = gp;
+        L->grad_stale = false;
+    }
     const hipError_t e =
         aq::launch_codebook_grad(geo, L->gplan, dtype, X, dY, L->d_scales, L->d_gpart, L->d_gidx_offs, L->d_gidx_ent,
-                                 dC, L->d_zero, splits, static_cast<hipStream_t>(stream));
+                                 dC, L->d_zero, L->opt.grad_splits, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "codebook gradient launch");
     return AQ_OK;
 }
@@ -758,6 +796,100 @@ aq_status aq_layer_set_path(aq_layer* L, aq_path path) {
         return fail(AQ_ERR_UNSUPPORTED, "fp16/bf16 decode path needs g == 8 (or g == 9 on a 3x3 convolution)");
     L->path = path;
     return AQ_OK;
+}
+
+aq_status aq_layer_set_option(aq_layer* L, int32_t option, int64_t value) {
+    if (!L) return fail(AQ_ERR_INVALID_ARGUMENT, "null layer");
+    aq::Options& o = L->opt;
+    auto in = [&](int64_t lo, int64_t hi) { return value >= lo && value <= hi; };
+    auto bad = [&]() { return fail(AQ_ERR_INVALID_ARGUMENT, "option " + std::to_string(option) +
+                                                                ": value " + std::to_string(value) + " out of range"); };
+    auto tile = [&](int* bm, int* bn) {
+        if (value == 0) {
+            *bm = *bn = 0;
+            return true;
+        }
+        const int64_t m = value / 1000, nn = value % 1000;
+        if (m < 16 || m > 512 || nn < 16 || nn > 512 || m % 16 || nn % 16) return false;
+        *bm = (int)m;
+        *bn = (int)nn;
+        return true;
+    };
+    switch (option) {
+    case AQ_OPT_LUT_MAX_TOKENS:
+        if (!in(-1, int64_t(1) << 40)) return bad();
+        o.lut_max_tokens = value;
+        return AQ_OK;
+    case AQ_OPT_WEIGHTS:
+        if (!in(0, 2)) return bad();
+        o.weights = (int)value;
+        return AQ_OK;
+    case AQ_OPT_GENERIC:
+        if (!in(0, 1)) return bad();
+        o.generic = (int)value;
+        return AQ_OK;
+    case AQ_OPT_RECORD_PRODUCT:
+        if (!in(0, 2)) return bad();
+        o.rec_product = (int)value;
+        return AQ_OK;
+    case AQ_OPT_FUSED_TILE:
+        return tile(&o.fused_bm, &o.fused_bn) ? AQ_OK : bad();
+    case AQ_OPT_DENSE_TILE:
+        return tile(&o.dense_bm, &o.dense_bn) ? AQ_OK : bad();
+    case AQ_OPT_REC_LINEAR_TILE:
+        if (!in(0, 2)) return bad();
+        o.rlin_tile = (int)value;
+        return AQ_OK;
+    case AQ_OPT_TILE_ORDER:
+        if (!in(0, 2)) return bad();
+        o.tile_order = (int)value;
+        return AQ_OK;
+    case AQ_OPT_STAGE_ROWS:
+        if (!in(0, 1)) return bad();
+        o.stage_rows = (int)value;
+        return AQ_OK;
+    case AQ_OPT_SPLIT_K:
+        if (!in(0, aq::kMaxSplitK)) return bad();
+        o.split_k = (int)value;
+        return AQ_OK;
+    case AQ_OPT_GRAD_SPLITS:
+        if (!in(0, 16)) return bad();
+        o.grad_splits = (int)value;
+        L->grad_stale = true;
+        return AQ_OK;
+    case AQ_OPT_GRAD_REGS:
+        if (!in(0, 1)) return bad();
+        o.grad_regs = (int)value;
+        L->grad_stale = true;
+        return AQ_OK;
+    case AQ_OPT_GRAD_TILE:
+        if (!tile(&o.grad_bm, &o.grad_bn)) return bad();
+        L->grad_stale = true;
+        return AQ_OK;
+    default:
+        return fail(AQ_ERR_INVALID_ARGUMENT, "unknown option " + std::to_string(option));
+    }
+}
+
+aq_status aq_layer_get_option(const aq_layer* L, int32_t option, int64_t* value) {
+    if (!L || !value) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    const aq::Options& o = L->opt;
+    switch (option) {
+    case AQ_OPT_LUT_MAX_TOKENS: *value = o.lut_max_tokens; return AQ_OK;
+    case AQ_OPT_WEIGHTS: *value = o.weights; return AQ_OK;
+    case AQ_OPT_GENERIC: *value = o.generic; return AQ_OK;
+    case AQ_OPT_RECORD_PRODUCT: *value = o.rec_product; return AQ_OK;
+    case AQ_OPT_FUSED_TILE: *value = o.fused_bm * 1000 + o.fused_bn; return AQ_OK;
+    case AQ_OPT_DENSE_TILE: *value = o.dense_bm * 1000 + o.dense_bn; return AQ_OK;
+    case AQ_OPT_REC_LINEAR_TILE: *value = o.rlin_tile; return AQ_OK;
+    case AQ_OPT_TILE_ORDER: *value = o.tile_order; return AQ_OK;
+    case AQ_OPT_STAGE_ROWS: *value = o.stage_rows; return AQ_OK;
+    case AQ_OPT_SPLIT_K: *value = o.split_k; return AQ_OK;
+    case AQ_OPT_GRAD_SPLITS: *value = o.grad_splits; return AQ_OK;
+    case AQ_OPT_GRAD_REGS: *value = o.grad_regs; return AQ_OK;
+    case AQ_OPT_GRAD_TILE: *value = o.grad_bm * 1000 + o.grad_bn; return AQ_OK;
+    default: return fail(AQ_ERR_INVALID_ARGUMENT, "unknown option " + std::to_string(option));
+    }
 }
 
 aq_status aq_layer_choose_path(const aq_layer* L, int64_t tokens, aq_path* out) {

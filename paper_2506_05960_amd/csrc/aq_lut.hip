@@ -459,13 +459,8 @@ size_t lut_lds_bytes(const Geom& geo, const LutPlan& plan, int nt) {
 template <int NT, bool MF, int CBT, int XT>
 static hipError_t launch_table(const Geom& geo, const LutPlan& plan, const LutArgs& a, hipStream_t st) {
     const size_t lds = lut_lds_bytes(geo, plan, NT);
-    static size_t attr_bytes = 64 * 1024;
-    if (lds > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)lut_fwd_kernel<NT, MF, CBT, XT>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (e != hipSuccess) return e;
-        attr_bytes = lds;
-    }
+    hipError_t e = ensure_dynamic_lds((const void*)lut_fwd_kernel<NT, MF, CBT, XT>, lds);
+    if (e != hipSuccess) return e;
     const int rows_wg = 4 * (64 / (plan.jc * geo.M / 16)) * a.rpl;
     const dim3 grid((unsigned)((geo.C_out + rows_wg - 1) / rows_wg), (unsigned)((a.nchunk + a.cpw - 1) / a.cpw),
                     (unsigned)((a.ntok + NT - 1) / NT));

@@ -295,12 +295,8 @@ static hipError_t launch_cfg(const Geom& geo, const DeviceWeights& w, const void
     size_t dyn = 0;
     if constexpr (MODE == DEC_LDS_F32) {
         dyn = (size_t)geo.M * (1 << geo.B) * 8 * sizeof(float);
-        static size_t attr_bytes = 0;
-        if (dyn > attr_bytes) {
-            hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-            if (e != hipSuccess) return e;
-            attr_bytes = dyn;
-        }
+        hipError_t e = ensure_dynamic_lds((const void*)kern, dyn);
+        if (e != hipSuccess) return e;
     }
     const dim3 grid((unsigned)((geo.tokens + BM - 1) / BM), (unsigned)((geo.C_out + BN - 1) / BN));
     const int acc16 = w.cb_dtype == AQ_F16 && TILE == AQ_F16;

@@ -343,13 +343,8 @@ rec_gemm_kernel(Geom geo, FusedPlan plan, GemmArgs ga) {
 template <int KIND, int XT, int BM, int BN>
 static hipError_t rec_gemm_cfg(const Geom& geo, const FusedPlan& plan, const GemmArgs& ga, hipStream_t st) {
     auto kern = rec_gemm_kernel<KIND, XT, BM, BN>;
-    static size_t attr_bytes = 0;
-    if (plan.lds_bytes > attr_bytes) {
-        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)plan.lds_bytes);
-        if (e != hipSuccess) return e;
-        attr_bytes = plan.lds_bytes;
-    }
+    hipError_t e = ensure_dynamic_lds((const void*)kern, plan.lds_bytes);
+    if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN)));
     kern<<<grid, 256, plan.lds_bytes, st>>>(geo, plan, ga);
     return hipGetLastError();

@@ -355,13 +355,8 @@ hipError_t rec_linear_cfg(const RecLinArgs& ar, const FusedLaunch& fl) {
     auto kern = rec_linear_kernel<XT, TM, TN, WGT>;
     constexpr int BM = 32 * TM * WGT, BN = 32 * TN * (4 / WGT);
     constexpr size_t lds = rec_linear_lds_bytes(BM, TM, TN);
-    static bool attr = false;
-    if (!attr) {
-        const hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 (int)lds);
-        if (e != hipSuccess) return e;
-        attr = true;
-    }
+    const hipError_t e = ensure_dynamic_lds((const void*)kern, lds);
+    if (e != hipSuccess) return e;
     const int64_t tm = (ar.tokens + BM - 1) / BM, tn = (ar.C_out + BN - 1) / BN;
     const dim3 grid((unsigned)(tm * tn));
     kern<<<grid, 256, lds, fl.stream>>>(ar, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y);
@@ -381,12 +376,8 @@ bool rec_linear_supported(const Geom& geo, const FusedPlan& plan, int x_dtype) {
 
 // Tile variant: 0 = 128 x 128 in a 2 x 2 wave split, 1 = 256 x 128 in a 2 x 2
 // split, 2 = 128 x 128 with the four waves side by side along the channels.
-int rec_linear_tile(const Geom& geo) {
-    if (const char* s = std::getenv("AQ_RLIN_TILE")) {
-        if (std::strcmp(s, "256") == 0) return 1;
-        if (std::strcmp(s, "128w") == 0) return 2;
-        return 0;
-    }
+int rec_linear_tile(const Geom& geo, int forced) {
+    if (forced >= 1 && forced <= 2) return forced;
     // The 128-token tiles fit 256 registers per lane, so two workgroups share a
     // compute unit and overlap one's prologue and epilogue with the other's
     // products; measured faster than the 256-token tile on the 8192-token qkv
@@ -401,7 +392,7 @@ hipError_t launch_rec_linear(const Geom& geo, const FusedPlan& plan, const Fused
     ar.K = geo.K;
     ar.C_out = geo.C_out;
     ar.nchunk = plan.nchunk;
-    const int var = rec_linear_tile(geo);
+    const int var = plan.rlin_var;
     const int bm = var == 1 ? 256 : 128, bn = 128;
     const int tm = (int)((geo.tokens + bm - 1) / bm), tn = (geo.C_out + bn - 1) / bn;
     ar.nmajor = plan.nmajor;

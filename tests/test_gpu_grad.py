@@ -46,24 +46,20 @@ def _dev(a, dt):
     return torch.from_numpy(a).cuda()
 
 
-def _grad(spec, inp, gi, dt, splits=None, layer=None):
+def _grad(spec, inp, gi, dt, splits=None, layer=None, opts=None):
     import paper_2506_05960_amd as P
     own = layer is None
     if own:
         layer = P.AQLayer(spec, inp)
-    old = os.environ.get("AQ_GRAD_SPLITS")
+    for k, v in (opts or {}).items():
+        layer.set_option(k, v)
     if splits is not None:
-        os.environ["AQ_GRAD_SPLITS"] = str(splits)
-    try:
-        x, dy = _dev(gi["x"], dt), _dev(gi["dy"], dt)
-        out = layer.codebook_grad(x, dy)
-        torch.cuda.synchronize()
-    finally:
-        if splits is not None:
-            if old is None:
-                os.environ.pop("AQ_GRAD_SPLITS", None)
-            else:
-                os.environ["AQ_GRAD_SPLITS"] = old
+        layer.set_option("grad_splits", splits)
+    x, dy = _dev(gi["x"], dt), _dev(gi["dy"], dt)
+    out = layer.codebook_grad(x, dy)
+    torch.cuda.synchronize()
+    if splits is not None:
+        layer.set_option("grad_splits", 0)
     res = out.cpu().numpy().astype(np.float64)
     if own:
         layer.close()
@@ -139,19 +135,6 @@ def test_token_splits_agree(spec, dt):
     assert O.rel_err_inf(b, ref) <= TOL
 
 
-def _grad_env(spec, inp, gi, dt, **env):
-    old = {k: os.environ.get(k) for k in env}
-    os.environ.update({k: str(v) for k, v in env.items()})
-    try:
-        return _grad(spec, inp, gi, dt)
-    finally:
-        for k, v in old.items():
-            if v is None:
-                os.environ.pop(k, None)
-            else:
-                os.environ[k] = v
-
-
 DMA_CASES = [c for c in CASES if c[0].name in ("lin_small", "lin_tiles", "lin_bf16", "lin_one_token", "conv3_small",
                                                 "conv3_g9_kaq", "conv3_w16", "conv1", "conv1_g16")]
 
@@ -164,9 +147,9 @@ def test_direct_to_lds_and_register_staged_kernels_agree(spec, dt):
     gi = generate_grad_inputs(spec, 47, dt)
     ref = _ref(spec, inp, gi, dt)
     for tile in ("64x64", "128x64"):
-        a = _grad_env(spec, inp, gi, dt, AQ_GRAD_TILE=tile)
+        a = _grad(spec, inp, gi, dt, opts={"grad_tile": tile})
         assert O.rel_err_inf(a, ref) <= TOL, tile
-    b = _grad_env(spec, inp, gi, dt, AQ_GRAD_DMA=0)
+    b = _grad(spec, inp, gi, dt, opts={"grad_regs": 1})
     assert O.rel_err_inf(b, ref) <= TOL
 
 

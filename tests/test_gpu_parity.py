@@ -41,11 +41,13 @@ def _dev(a, dtype_name):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
 
-def _run(spec, inp, path="auto", max_tokens=None, stream=None):
+def _run(spec, inp, path="auto", max_tokens=None, stream=None, opts=None):
     import paper_2506_05960_amd as P
     layer = P.AQLayer(spec, inp, max_tokens=max_tokens)
     if path != "auto":
         layer.set_path(path)
+    for k, v in (opts or {}).items():
+        layer.set_option(k, v)
     x = _dev(inp["x"], spec.x_dtype)
     xs = None if inp["x_scales"] is None else torch.from_numpy(inp["x_scales"]).cuda()
     if stream is not None:
@@ -250,34 +252,26 @@ FUSED = [
 
 
 @pytest.mark.parametrize("spec", FUSED, ids=lambda s: s.name)
-def test_fused_matches_oracle_and_generic(spec, monkeypatch):
+def test_fused_matches_oracle_and_generic(spec):
     inp = generate(spec, 2024)
     y_ref = O.forward(spec, inp)
     _say(f"fused {spec.name}")
     y_fused = _run(spec, inp, "decode")
     e1 = O.rel_err_inf(y_fused, y_ref)
-    monkeypatch.setenv("AQ_NO_FUSED", "1")
-    y_gen = _run(spec, inp, "decode")
-    monkeypatch.delenv("AQ_NO_FUSED")
+    y_gen = _run(spec, inp, "decode", opts={"generic": 1})
     e2 = O.rel_err_inf(y_gen, y_ref)
     _say(f"  fused err={e1:.3e} generic err={e2:.3e}")
     assert e1 <= 2e-3 and e2 <= 2e-3
 
 
 @pytest.mark.parametrize("spec", FUSED, ids=lambda s: s.name)
-def test_predecoded_operands_match_in_loop_decode(spec, monkeypatch):
+def test_predecoded_operands_match_in_loop_decode(spec):
     """Pre-decoded operand records give bit-identical outputs to decoding inside the main loop."""
     inp = generate(spec, 31)
-    monkeypatch.setenv("AQ_FUSED_REC", "1")
-    monkeypatch.setenv("AQ_REC_LINEAR", "0")     # the fused kernel's own pre-decoded mode
-    y_rec = _run(spec, inp, "decode")
-    monkeypatch.delenv("AQ_REC_LINEAR")
-    monkeypatch.setenv("AQ_GEMM", "1")
-    y_gemm = _run(spec, inp, "decode")            # dense product over the same records
-    monkeypatch.delenv("AQ_GEMM")
-    monkeypatch.setenv("AQ_FUSED_REC", "0")
-    y_loop = _run(spec, inp, "decode")
-    monkeypatch.delenv("AQ_FUSED_REC")
+    # the fused kernel's own pre-decoded mode
+    y_rec = _run(spec, inp, "decode", opts={"weights": 2, "record_product": 1})
+    y_gemm = _run(spec, inp, "decode", opts={"weights": 2, "record_product": 2})   # dense product, same records
+    y_loop = _run(spec, inp, "decode", opts={"weights": 1})
     y_ref = O.forward(spec, inp)
     err, err_g = O.rel_err_inf(y_rec, y_ref), O.rel_err_inf(y_gemm, y_ref)
     _say(f"predecoded {spec.name} err={err:.3e} gemm err={err_g:.3e} identical={np.array_equal(y_rec, y_loop)}")
@@ -298,13 +292,10 @@ GEMM_CASES = [
 
 @pytest.mark.parametrize("tile", ["128x128", "128x64", "64x128"])
 @pytest.mark.parametrize("spec", GEMM_CASES, ids=lambda s: s.name)
-def test_dense_product_over_records(spec, tile, monkeypatch):
+def test_dense_product_over_records(spec, tile):
     """Every tile of the dense product over pre-decoded records, against the oracle."""
-    monkeypatch.setenv("AQ_FUSED_REC", "1")
-    monkeypatch.setenv("AQ_GEMM", "1")
-    monkeypatch.setenv("AQ_GEMM_TILE", tile)
     inp = generate(spec, 8)
-    y = _run(spec, inp, "decode")
+    y = _run(spec, inp, "decode", opts={"weights": 2, "record_product": 2, "dense_tile": tile})
     err = O.rel_err_inf(y, O.forward(spec, inp))
     _say(f"gemm {spec.name} {tile} err={err:.3e}")
     assert err <= 2e-3
@@ -342,15 +333,13 @@ def test_predecoded_formats(spec):
 
 
 @pytest.mark.parametrize("spec", [f for f in FUSED + KAQ if f.conv is not None], ids=lambda s: s.name)
-def test_fused_conv_row_staging(spec, monkeypatch):
+def test_fused_conv_row_staging(spec):
     """Input rows staged once per image block fill the fragments exactly as kh rows per output row do."""
     inp = generate(spec, 78)
     for rec in ("0", "1"):
-        monkeypatch.setenv("AQ_FUSED_REC", rec)
-        y_once = _run(spec, inp, "decode")
-        monkeypatch.setenv("AQ_FUSED_ROWS", "each")
-        y_each = _run(spec, inp, "decode")
-        monkeypatch.delenv("AQ_FUSED_ROWS")
+        w = 2 if rec == "1" else 1
+        y_once = _run(spec, inp, "decode", opts={"weights": w})
+        y_each = _run(spec, inp, "decode", opts={"weights": w, "stage_rows": 1})
         _say(f"row staging {spec.name} rec={rec} identical={np.array_equal(y_once, y_each)}")
         assert np.array_equal(y_once, y_each)
     assert O.rel_err_inf(y_once, O.forward(spec, inp)) <= 2e-3
@@ -384,14 +373,13 @@ def test_kaq_large_k_few_tokens_takes_the_table_path():
 
 
 @pytest.mark.parametrize("tile", ["64x96", "64x64", "128x64", "32x128", "32x64"])
-def test_fused_tiles(tile, monkeypatch):
+def test_fused_tiles(tile):
     """Every instantiated tile of the fused kernel on a conv and a linear layer."""
-    monkeypatch.setenv("AQ_FUSED_TILE", tile)
     for spec in (LayerSpec(name="t_conv", C_out=200, K=32 * 9, g=8, M=2, B=8, n=2,
                            conv=ConvGeom(32, 3, 3, 1, 1, 16, 16)),
                  LayerSpec(name="t_lin", C_out=200, K=192, g=8, M=2, B=8, n=150)):
         inp = generate(spec, 7)
-        y = _run(spec, inp, "decode")
+        y = _run(spec, inp, "decode", opts={"fused_tile": tile})
         err = O.rel_err_inf(y, O.forward(spec, inp))
         _say(f"tile {tile} {spec.name} err={err:.3e}")
         assert err <= 2e-3
@@ -399,14 +387,11 @@ def test_fused_tiles(tile, monkeypatch):
 
 @pytest.mark.parametrize("rec", ["0", "1"])
 @pytest.mark.parametrize("tile", ["64x64", "32x128"])
-def test_fused_linear_int8_tiles(tile, rec, monkeypatch):
+def test_fused_linear_int8_tiles(tile, rec):
     """int8 activations, M = 4, several chunks per wave and a ragged token tail, in both weight modes."""
-    monkeypatch.setenv("AQ_FUSED_TILE", tile)
-    monkeypatch.setenv("AQ_FUSED_REC", rec)
-    monkeypatch.setenv("AQ_REC_LINEAR", "0")
     spec = LayerSpec(name="t_lin_i8", C_out=136, K=640, g=8, M=4, B=8, n=300, x_dtype="i8")
     inp = generate(spec, 17)
-    y = _run(spec, inp, "decode")
+    y = _run(spec, inp, "decode", opts={"fused_tile": tile, "weights": 2 if rec == "1" else 1, "record_product": 1})
     err = O.rel_err_inf(y, O.forward(spec, inp))
     _say(f"tile {tile} rec={rec} {spec.name} err={err:.3e}")
     assert err <= 2e-3
@@ -430,15 +415,13 @@ RLIN = [
 
 
 @pytest.mark.parametrize("spec", RLIN, ids=lambda s: s.name)
-def test_rec_linear_tiles(spec, monkeypatch):
+def test_rec_linear_tiles(spec):
     """Every tile against the oracle, and bit-identical to each other (one accumulation order per output)."""
-    monkeypatch.setenv("AQ_FUSED_REC", "1")
     inp = generate(spec, 41)
     y_ref = O.forward(spec, inp)
     ys = {}
-    for tile in ("256", "128", "128w"):
-        monkeypatch.setenv("AQ_RLIN_TILE", tile)
-        ys[tile] = _run(spec, inp, "decode")
+    for tile, var in (("256", 1), ("128", 0), ("128w", 2)):
+        ys[tile] = _run(spec, inp, "decode", opts={"weights": 2, "rec_linear_tile": var})
         err = O.rel_err_inf(ys[tile], y_ref)
         _say(f"rec linear {spec.name} tile {tile} err={err:.3e}")
         assert err <= 2e-3
@@ -451,14 +434,13 @@ def test_rec_linear_tiles(spec, monkeypatch):
 
 @pytest.mark.parametrize("M,B,rec", [(3, 8, "0"), (2, 12, "0"), (1, 16, "0"), (2, 8, "0"), (4, 8, "0"), (4, 6, "0"),
                                      (1, 16, "1"), (2, 8, "1"), (4, 8, "1")])
-def test_one_hot_rows_read_back_decoded_tile(M, B, rec, monkeypatch):
+def test_one_hot_rows_read_back_decoded_tile(M, B, rec):
     """X = identity (fp16) through the matrix-core path returns fl32(W_tile * s) exactly."""
-    monkeypatch.setenv("AQ_FUSED_REC", rec)
     spec = LayerSpec(name="onehot", C_out=160, K=256, g=8, M=M, B=B, n=256, y_dtype="f32")
     inp = generate(spec, 99)
     inp["x"] = np.eye(256, dtype=np.float16)
     _say(f"onehot M={M} B={B}")
-    y = _run(spec, inp, "decode").astype(np.float32)
+    y = _run(spec, inp, "decode", opts={"weights": 2 if rec == "1" else 1}).astype(np.float32)
     wt = O.decode_emulate(inp["codebooks"], inp["codes"], inp["scales"], 8, "f16", "f16", scaled=False)
     ref = (wt.astype(np.float32) * inp["scales"][:, None]).astype(np.float32)   # [C_out, K]
     assert np.array_equal(y.view(np.uint32), ref.T.copy().view(np.uint32))
@@ -549,6 +531,92 @@ def test_sweep_layer_sampled(layer, M):
         flat = y.transpose(0, 2, 3, 1).reshape(spec.tokens, spec.C_out)
         got = flat[np.ix_(tok, ch)]
     assert O.rel_err_inf(got, ref) <= 2e-3
+
+
+# ---------------------------------------------------------------------------
+# every distinct layer shape of the U-Net sweep at its full size (batch 8):
+# W2 and W4 for every shape, and the kernel-aware g = 9 format (W2K, W4K) for
+# every 3x3 convolution; the dispatcher picks the route (auto path)
+# ---------------------------------------------------------------------------
+
+def _sweep_shape_cases():
+    seen = {}
+    for lay in W.sweep_layers(full=True):
+        seen.setdefault((lay.kind, lay.cin, lay.cout, lay.res, lay.stride, lay.tokens_per_image), lay)
+    cases = []
+    for lay in seen.values():
+        for var in ("W2", "W4") + (("W2K", "W4K") if lay.kind == "conv3x3" else ()):
+            cases.append((lay, var))
+    return cases
+
+
+def _edge_samples(spec, rng, n_tok=64, n_ch=48):
+    """Sampled output positions: first and last token and channel, the image
+    border pixels of the first and last image, token and channel tile edges,
+    then random positions."""
+    T, C = spec.tokens, spec.C_out
+    tok = [0, T - 1]
+    if spec.conv is not None:
+        OH, OW = spec.conv.OH, spec.conv.OW
+        for b in (0, spec.n - 1):
+            for oh, ow in ((0, 0), (0, OW - 1), (OH - 1, 0), (OH - 1, OW - 1), (0, OW // 2), (OH // 2, 0),
+                           (OH - 1, OW // 2), (OH // 2, OW - 1)):
+                tok.append((b * OH + oh) * OW + ow)
+    for e in (32, 64, 128, 256):
+        for t in (e - 1, e, T - e, T - e - 1):
+            tok.append(t)
+    ch = [0, C - 1]
+    for e in (32, 64, 96, 128, 192, 256):
+        ch += [e - 1, e, C - e]
+    tok = sorted(set(t for t in tok if 0 <= t < T))
+    ch = sorted(set(c for c in ch if 0 <= c < C))
+    while len(tok) < min(n_tok, T):
+        tok = sorted(set(tok) | {int(rng.integers(0, T))})
+    while len(ch) < min(n_ch, C):
+        ch = sorted(set(ch) | {int(rng.integers(0, C))})
+    return np.array(tok), np.array(ch)
+
+
+def _sampled_outputs(spec, y, tok, ch):
+    if spec.conv is None:
+        return y[np.ix_(tok, ch)]
+    flat = y.transpose(0, 2, 3, 1).reshape(spec.tokens, spec.C_out)
+    return flat[np.ix_(tok, ch)]
+
+
+def check_against_oracle(spec, inp, got, tok, ch, path, tol):
+    """The GPU outputs at (tok, ch) against the oracle: infinity-norm and RMS
+    relative errors within ``tol``, and every element within its rounding bound."""
+    ref = O.forward_sampled(spec, inp, tok, ch)
+    a_ref = O.forward_sampled(spec, O.abs_inputs(spec, inp), tok, ch)
+    bound = O.rounding_bound(spec, ref, a_ref, path)
+    e_inf, e_rms, e_el = O.rel_err_inf(got, ref), O.rel_err_rms(got, ref), O.rel_err_elem(got, ref)
+    over = np.argwhere(np.abs(got - ref) > bound)
+    _say(f"  inf={e_inf:.2e} rms={e_rms:.2e} elem(floor 1e-3 rms)={e_el:.2e} over_bound={len(over)}")
+    for i, j in over[:5]:
+        _say(f"    token {tok[i]} channel {ch[j]}: got {got[i, j]!r} ref {ref[i, j]!r} bound {bound[i, j]:.3e}")
+    assert e_inf <= tol and e_rms <= tol
+    assert len(over) == 0
+
+
+@pytest.mark.parametrize("layer,variant", _sweep_shape_cases(),
+                         ids=[f"{l.name}-{v}" for l, v in _sweep_shape_cases()])
+def test_sweep_shape_parity(layer, variant):
+    M = {"W2": 2, "W4": 4, "W2K": 2, "W4K": 4}[variant]
+    g = 9 if variant.endswith("K") else 8
+    spec = W.sweep_spec(layer, M, batch=8, g=g)
+    import paper_2506_05960_amd as P
+    inp = generate(spec, 5151 + 7 * M + g)
+    _say(f"sweep shape {spec.name} g={g} tokens={spec.tokens} K={spec.K} C_out={spec.C_out}")
+    lay = P.AQLayer(spec, inp)
+    path = lay.choose_path(spec.tokens)
+    x = _dev(inp["x"], spec.x_dtype)
+    y = lay.forward(x)
+    torch.cuda.synchronize()
+    out = y.float().cpu().numpy().astype(np.float64)
+    lay.close()
+    tok, ch = _edge_samples(spec, np.random.default_rng(17))
+    check_against_oracle(spec, inp, _sampled_outputs(spec, out, tok, ch), tok, ch, path, 2e-3)
 
 
 def test_graph_replay_matches_eager():

@@ -425,3 +425,85 @@ def test_error_metric():
     y_ref = np.array([[1.0, -4.0], [2.0, 0.5]])
     y = y_ref + np.array([[0.0, 0.004], [-0.002, 0.0]])
     assert O.rel_err_inf(y, y_ref) == pytest.approx(0.001)
+
+
+# ---------------------------------------------------------------------------
+# O6: RMS-relative and floored per-element errors, and the rounding bound
+# ---------------------------------------------------------------------------
+
+def test_rms_and_elementwise_errors_closed_forms():
+    rng = np.random.default_rng(12)
+    y = rng.normal(size=(40, 7))
+    # a uniform relative perturbation eps gives exactly eps in both forms
+    assert math.isclose(O.rel_err_rms(y * 1.003, y), 0.003, rel_tol=1e-9)
+    assert math.isclose(O.rel_err_elem(y * 1.003, y), 0.003, rel_tol=1e-9)
+    # a constant offset c gives c / rms(y) in RMS form
+    rms = math.sqrt(float(np.mean(y * y)))
+    assert math.isclose(O.rel_err_rms(y + 0.01, y), 0.01 / rms, rel_tol=1e-9)
+    # one element near zero: judged against the floor, not against its own magnitude
+    z = y.copy()
+    z[3, 2] = 1e-9
+    w = z.copy()
+    w[3, 2] += 1e-4
+    assert math.isclose(O.rel_err_elem(w, z), 1e-4 / (1e-3 * math.sqrt(float(np.mean(z * z)))), rel_tol=1e-9)
+    # a localised error the infinity norm over the whole output dilutes
+    v = y.copy()
+    v[:, 0] *= 1e-3
+    u = v.copy()
+    u[5, 0] *= 2.0
+    assert O.rel_err_inf(u, v) < 2e-3 < O.rel_err_elem(u, v)
+
+
+def test_abs_inputs_forward_is_sum_of_magnitudes():
+    """forward(abs_inputs) == fsum over (k, m) of |x_k| s_i |C_m[b][t]|, brute force; it dominates |Y*|."""
+    rng = np.random.default_rng(13)
+    g, M, B, C_out, G, N = 4, 3, 4, 5, 3, 4
+    cb, codes, s, x = _rand_layer(rng, C_out, G, g, M, B, N)
+    from workloads import LayerSpec
+    spec = LayerSpec(name="abs", C_out=C_out, K=G * g, g=g, M=M, B=B, n=N, codebook_dtype="f32", x_dtype="f32",
+                     y_dtype="f32", tile_dtype="f32")
+    inp = {"codebooks": cb.astype(np.float32), "codes": codes, "scales": s, "x": x.astype(np.float32),
+           "x_scales": None}
+    a = O.forward(spec, O.abs_inputs(spec, inp))
+    for n in range(N):
+        for i in range(C_out):
+            terms = [abs(float(inp["x"][n, j * g + t])) * float(s[i]) * abs(float(inp["codebooks"][m, codes[i, j, m], t]))
+                     for j in range(G) for m in range(M) for t in range(g)]
+            assert math.isclose(a[n, i], math.fsum(terms), rel_tol=1e-13)
+    assert np.all(a >= np.abs(O.forward(spec, inp)) * (1 - 1e-13))
+
+
+def _emulated_gpu_forward(spec, inp):
+    """The decode path's arithmetic written out in numpy: fp16 tile weights
+    (unscaled, decode emulation), products and sums in fp32, scale on the fp32
+    sum, one rounding to the output dtype."""
+    wt = O.decode_emulate(inp["codebooks"], inp["codes"], inp["scales"], spec.g, spec.codebook_dtype,
+                          spec.tile_dtype, scaled=False).astype(np.float32)
+    x = inp["x"].astype(np.float32)
+    acc = (x @ wt.T).astype(np.float32)
+    y = (acc * inp["scales"].astype(np.float32)[None, :]).astype(np.float32)
+    return y.astype(np.float16 if spec.y_dtype == "f16" else np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("M", [1, 2, 4])
+def test_rounding_bound_holds_for_emulated_arithmetic_and_catches_one_wrong_element(M):
+    from workloads import LayerSpec, generate
+    spec = LayerSpec(name="bound", C_out=48, K=256, g=8, M=M, B=8, n=200)
+    inp = generate(spec, 21 + M)
+    y_ref = O.forward(spec, inp)
+    a_ref = O.forward(spec, O.abs_inputs(spec, inp))
+    bound = O.rounding_bound(spec, y_ref, a_ref, "decode")
+    y = _emulated_gpu_forward(spec, inp)
+    assert np.all(np.abs(y - y_ref) <= bound)
+    # the bound stays a small fraction of the output's scale, and an error of
+    # twice the bound in one element is flagged there and nowhere else
+    rms = math.sqrt(float(np.mean(y_ref * y_ref)))
+    assert float(np.max(bound)) < 0.1 * rms
+    bad = y.copy()
+    bad[17, 5] += 2.0 * bound[17, 5]
+    viol = np.argwhere(np.abs(bad - y_ref) > bound)
+    assert [tuple(v) for v in viol] == [(17, 5)]
+    # a swapped pair of output channels (a plausible indexing mistake) is caught
+    sw = y.copy()
+    sw[:, [3, 4]] = sw[:, [4, 3]]
+    assert np.any(np.abs(sw - y_ref) > bound)
