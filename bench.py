@@ -1,13 +1,17 @@
 """Benchmark of the AQ layer forward on one MI355X.
 
-One step = one forward of the whole hot path (dispatch, activation staging,
-weight decode or table build, contraction, epilogue) over the workload's
-synthetic inputs, which are resident in HBM before timing starts.  Prints ONE
-JSON line with dense-equivalent TFLOP/s (2 FLOP per multiply-accumulate), the
-algorithmic HBM GB/s, the roofline fraction of the dominant kernel and the
-CPU oracle timed on this host.
+One step = the whole hot path (dispatch, activation staging, weight decode or
+table build, contraction, epilogue) over one batch of synthetic input that is
+resident in HBM before timing starts.  The default workload is the
+LDM-4-shaped U-Net pass at batch 8 (W2: g = 8, M = 2, B = 8): its 97
+quantized layers chained, one step per pass.  ``--config conv64|qkv16|conv8|
+tiny`` times one layer instead (one step per forward).  Prints ONE JSON line
+with dense-equivalent TFLOP/s (2 FLOP per multiply-accumulate), the
+algorithmic HBM GB/s, the roofline fraction of the dominant kernel (timed
+live with HIP events around every launch) and the CPU oracle timed on this
+host.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config conv64]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config sweep]
 """
 from __future__ import annotations
 
@@ -65,36 +69,35 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch from the committed counter summary, if it matches these sources.
-
-    The summary holds FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the
-    kernel, each divided by the ratio the same counter shows for a plain
-    device copy of known size; it is used only when it was taken on the
-    current kernel sources.
-    """
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+def host_info():
+    """CPU model, usable cores and the BLAS library numpy's matmul runs on."""
+    model = "unknown"
     try:
-        with open(path) as f:
-            d = json.load(f)
-    except (OSError, ValueError):
-        return None
-    ent = d.get(workload)
-    if not ent or ent.get("source_hash") != kernel_source_hash():
-        return None
-    return ent.get("traffic_bytes")
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    blas, threads = "unknown", cores
+    try:
+        from threadpoolctl import threadpool_info
+        info = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')}"
+            threads = int(info[0].get("num_threads", cores))
+    except Exception:
+        pass
+    return {"cpu": model, "cores_available": cores, "blas": blas, "threads": threads}
 
 
 def cpu_baseline(spec, inp, budget_s: float = 12.0):
     """Time the fp64 oracle on this host's cores (bounded number of repetitions)."""
-    import numpy as np
     import oracle as O
 
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
-    except Exception:
-        threads = os.cpu_count() or 1
+    hi = host_info()
     t0 = time.perf_counter()
     O.forward(spec, inp)       # warm-up
     first = time.perf_counter() - t0
@@ -108,10 +111,12 @@ def cpu_baseline(spec, inp, budget_s: float = 12.0):
     return {
         "value": round(spec.dense_flops / t / 1e12, 6),
         "unit": "TFLOP/s",
-        "cores": int(threads),
+        "cores": int(hi["threads"]),
         "kind": "oracle",
         "sample": f"whole layer ({spec.name}): fp64 dequantize + im2col + BLAS matmul, "
                   f"median of {reps} runs after 1 warm-up, {t:.3f} s per forward",
+        "cpu": hi["cpu"],
+        "blas": hi["blas"],
     }
 
 
@@ -140,77 +145,259 @@ def _graph_time_us(torch, fn, reps: int, trials: int = 5) -> float:
     return statistics.median(times)
 
 
-def sweep_bench(a, torch, P, W):
-    """Every layer of the LDM-4-shaped U-Net sweep at batch 8: per-layer and whole-pass time.
+PRODUCT_KERNELS = ("fused_fwd_kernel", "rec_linear_kernel", "rec_gemm_kernel", "mfma_fwd_kernel", "f32_fwd_kernel",
+                   "lut_fwd_kernel")
 
-    Weights come from the seeded generators (one seed per layer); activations
-    are fp16 N(0, 1) drawn on the device from a seeded generator.  The whole
-    pass runs the layers back to back in one HIP graph, as a U-Net forward
-    would (each layer reads its own input; inter-layer glue is not part of
-    this measurement).
+
+def launch_times(torch, items, replays: int = 5):
+    """Per-launch kernel durations of a pass of forwards, timed with HIP events.
+
+    ``items`` is a list of (layer, fn): ``fn()`` runs the layer's forward.  Each
+    layer gets one timing event per kernel launch plus one, which the library
+    records on the launch stream around every launch.  The runtime cannot
+    record events inside a captured graph, so the pass runs eagerly: it is
+    queued twice back to back and the second pass's events are read (while
+    the GPU runs the first pass the host queues the second, so no launch of
+    the second waits for the host; ``items`` may repeat a layer).  Returns (per-layer list of (kernel name,
+    median us), "eager", median pass us with the events).
     """
+    layouts = []
+    for layer, fn in items:
+        fn()
+        torch.cuda.synchronize()
+        n, names = layer.last_launches()
+        layouts.append(names[:n])
+    evs = []
+    for (layer, _), names in zip(items, layouts):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+        for x in e:
+            x.record()
+        evs.append(e)
+    torch.cuda.synchronize()
+    samples = [[[] for _ in names] for names in layouts]
+    pass_us = []
+    for _ in range(replays):
+        # the first pass records no events; in the second each forward gets its
+        # own events (an event is never re-recorded while a record is pending)
+        for layer, fn in items:
+            layer.set_launch_events([])
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for (layer, fn), e in zip(items, evs):
+            layer.set_launch_events(e)
+            fn()
+        b.record()
+        for layer, _ in items:
+            layer.set_launch_events([])
+        torch.cuda.synchronize()
+        pass_us.append(a.elapsed_time(b) * 1e3)
+        for li, e in enumerate(evs):
+            for k in range(len(e) - 1):
+                samples[li][k].append(e[k].elapsed_time(e[k + 1]) * 1e3)
+    for layer, _ in items:
+        layer.set_launch_events([])
+    per_layer = [[(names[k], statistics.median(samples[li][k])) for k in range(len(names))]
+                 for li, names in enumerate(layouts)]
+    return per_layer, "eager", statistics.median(pass_us)
+
+
+def dominant_kernel(per_layer, flops):
+    """Group launches by kernel; the dominant one takes the most time.  Its
+    achieved rate is the dense FLOPs of the layers it computes over its
+    total duration (auxiliary launches: record decoding, reductions, packing,
+    carry no FLOPs of their own)."""
+    tot, cnt, fl = {}, {}, {}
+    for li, launches in enumerate(per_layer):
+        for name, us in launches:
+            tot[name] = tot.get(name, 0.0) + us
+            cnt[name] = cnt.get(name, 0) + 1
+            if name.startswith(PRODUCT_KERNELS):
+                fl[name] = fl.get(name, 0) + flops[li]
+    name = max(tot, key=tot.get)
+    table = sorted(((n, tot[n], cnt[n], fl.get(n, 0)) for n in tot), key=lambda r: -r[1])
+    return name, tot[name], cnt[name], fl.get(name, 0), table
+
+
+def measured_traffic_kernel(workload: str, kernel: str):
+    """HBM bytes per launch of ``kernel`` in ``workload`` from the committed counter summary (or None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    ent = d.get(f"{workload}:{kernel}")
+    if not ent or ent.get("source_hash") != kernel_source_hash():
+        return None
+    return ent.get("traffic_bytes")
+
+
+def sweep_cpu_baseline(specs, seeds, budget_s: float = 20.0):
+    """The fp64 oracle over a bounded, stratified sample of the pass's layers
+    (every 6th layer, in order, until the budget is spent), each with its own
+    weights and a seeded N(0, 1) input of the full batch."""
+    import numpy as np
+
+    import oracle as O
+    import workloads as W
+
+    hi = host_info()
+    done, flops, t_all = [], 0, 0.0
+    for i in range(0, len(specs), 6):
+        spec = specs[i]
+        inp = W.generate(spec, seeds[i])
+        t0 = time.perf_counter()
+        O.forward(spec, inp)
+        t_all += time.perf_counter() - t0
+        flops += spec.dense_flops
+        done.append(spec.name)
+        if t_all > budget_s:
+            break
+    return {
+        "value": round(flops / t_all / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": int(hi["threads"]),
+        "kind": "oracle",
+        "sample": f"{len(done)} of the pass's {len(specs)} layers (every 6th, {flops / 1e9:.1f} GFLOP): fp64 "
+                  f"dequantize + im2col + BLAS matmul, one run each, {t_all:.2f} s",
+        "cpu": hi["cpu"],
+        "blas": hi["blas"],
+    }
+
+
+def sweep_bench(a, torch, P, W):
+    """The LDM-4-shaped U-Net pass at batch 8: every quantized layer, chained.
+
+    Layer i reads layer i-1's output buffer whenever its element count allows
+    (``workloads.chain_sources``; the glue between U-Net layers is not part of
+    the pass), else a seeded N(0, 1) buffer of its own.  Codebooks have the
+    unit-scale standard deviation, so activations stay near unit scale along
+    the chain.  One step = one whole pass, replayed from a HIP graph.
+    """
+    import numpy as np
+
     layers = W.sweep_layers(full=a.full)
     M = {"W2": 2, "W4": 4, "W2K": 2, "W4K": 4}[a.variant]
     kaq = a.variant.endswith("K")       # 3x3 convolutions in the kernel-aware format (g = 9)
+    src = W.chain_sources(layers, batch=8)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(W.SEED_BASE + 4)
-    rows, calls, total_flops, total_bytes = [], [], 0, 0
-    objs = []
+    specs, seeds, objs, items = [], [], [], []
+    total_flops = total_bytes = 0
+    prev_y = None
     for i, lay in enumerate(layers):
-        spec = W.sweep_spec(lay, M, batch=8, g=9 if kaq and lay.kind == "conv3x3" else 8)
-        wts = W.generate(spec.with_n(1), W.SEED_BASE + 100 + i)       # weights are drawn before activations
+        spec = W.sweep_spec(lay, M, batch=8, g=9 if kaq and lay.kind == "conv3x3" else 8, codebook_std="chain")
+        seed = W.SEED_BASE + 100 + i
+        wts = W.generate(spec.with_n(1), seed)         # weights are drawn before activations
         layer = P.AQLayer(spec, wts, max_tokens=spec.tokens)
-        xshape = (spec.n, spec.K) if spec.conv is None else (spec.n, spec.conv.cin, spec.conv.H, spec.conv.W)
-        x = torch.randn(xshape, generator=gen, device="cuda", dtype=torch.float32).to(torch.float16)
+        xshape = layer.in_shape(spec.n)
+        if src[i] is not None:
+            x = prev_y.view(xshape)
+        else:
+            x = torch.randn(xshape, generator=gen, device="cuda", dtype=torch.float32).to(torch.float16)
         y = torch.empty(layer.out_shape(spec.n), dtype=torch.float16, device="cuda")
         fn = (lambda layer=layer, x=x, y=y: layer.forward(x, None, out=y))
-        us = _graph_time_us(torch, fn, reps=20)
-        flops, nbytes = spec.dense_flops, algorithmic_bytes(spec)
-        total_flops += flops
-        total_bytes += nbytes
-        rows.append((spec.name, lay.kind, spec.tokens, spec.K, spec.C_out, layer.choose_path(spec.tokens), us,
-                     flops / (us * 1e-6) / 1e12, lay.role))
-        calls.append(fn)
+        specs.append(spec)
+        seeds.append(seed)
         objs.append((layer, x, y))
-    whole_us = _graph_time_us(torch, lambda: [f() for f in calls], reps=1, trials=7)
-    per_layer_sum = sum(r[6] for r in rows)
+        items.append((layer, fn))
+        total_flops += spec.dense_flops
+        total_bytes += algorithmic_bytes(spec)
+        prev_y = y
+
+    def run_pass():
+        for _, fn in items:
+            fn()
+
+    # the timed steps: whole passes replayed from one graph
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    run_pass()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph, stream=stream):
+            run_pass()
+    torch.cuda.current_stream().wait_stream(stream)
+    for _ in range(max(0, a.warmup)):
+        graph.replay()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(a.steps):
+        graph.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    pass_us = start.elapsed_time(stop) * 1e3 / a.steps
+
+    # per-launch kernel durations inside the same pass (events around every launch)
+    per_layer, tmode, pass_us_ev = launch_times(torch, items)
+    flops = [sp.dense_flops for sp in specs]
+    kname, k_us, k_n, k_flops, ktable = dominant_kernel(per_layer, flops)
+    workload = f"unet_sweep_b8_{a.variant}{'_full' if a.full else ''}_chained"
+    k_tflops = k_flops / (k_us * 1e-6) / 1e12
+    # every layer's output at unit scale (no overflow, no collapse along the chain)
+    rms = [float(y.float().pow(2).mean().sqrt()) for _, _, y in objs]
+
     if a.table:
         with open(a.table, "w") as f:
             fmt = "g=9 for 3x3 convolutions, g=8 elsewhere" if kaq else "g=8"
-            f.write(f"# U-Net layer sweep, batch 8, {a.variant} ({fmt}, M={M}, B=8), fp16\n\n")
+            f.write(f"# U-Net pass, batch 8, {a.variant} ({fmt}, M={M}, B=8), fp16, chained\n\n")
             f.write(f"Command: `python bench.py --config sweep --variant {a.variant}"
                     f"{' --full' if a.full else ''} --table <this file>`\n\n")
-            f.write(f"{len(rows)} layers, {total_flops / 1e9:.1f} dense-equivalent GFLOP.  Whole pass in one HIP "
-                    f"graph: {whole_us:.1f} us ({total_flops / (whole_us * 1e-6) / 1e12:.1f} TFLOP/s); sum of "
-                    f"per-layer times: {per_layer_sum:.1f} us.\n\n")
-            f.write("| layer | kind | tokens | K | C_out | path | us | TFLOP/s | note |\n|---|---|---|---|---|---|---|---|---|\n")
-            for r in rows:
-                f.write(f"| {r[0]} | {r[1]} | {r[2]} | {r[3]} | {r[4]} | {r[5]} | {r[6]:.2f} | {r[7]:.1f} | {r[8]} |\n")
-    for layer, _, _ in objs:
-        layer.close()
-    tflops = total_flops / (whole_us * 1e-6) / 1e12
-    return {
+            f.write(f"{len(layers)} layers, {sum(s is not None for s in src)} reading the previous layer's output; "
+                    f"{total_flops / 1e9:.1f} dense-equivalent GFLOP.  Whole pass in one HIP graph: "
+                    f"{pass_us:.1f} us ({total_flops / (pass_us * 1e-6) / 1e12:.1f} TFLOP/s, "
+                    f"{total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS:.3f} of 2.5 PFLOP/s).  "
+                    f"With timing events around every launch ({tmode}): {pass_us_ev:.1f} us.\n\n")
+            f.write("Per kernel (sum over the pass):\n\n| kernel | launches | total us | share | TFLOP/s |\n"
+                    "|---|---|---|---|---|\n")
+            ksum = sum(r[1] for r in ktable)
+            for n, t, c, fl in ktable:
+                f.write(f"| `{n}` | {c} | {t:.1f} | {t / ksum:.3f} | "
+                        f"{(fl / (t * 1e-6) / 1e12) if fl else 0:.1f} |\n")
+            f.write("\nPer layer (kernels in launch order, us each):\n\n"
+                    "| layer | kind | tokens | K | C_out | input | launches | us | TFLOP/s | out rms |\n"
+                    "|---|---|---|---|---|---|---|---|---|---|\n")
+            for i, (lay, sp) in enumerate(zip(layers, specs)):
+                us = sum(t for _, t in per_layer[i])
+                ks = " + ".join(f"`{n.split('<')[0]}` {t:.1f}" for n, t in per_layer[i])
+                f.write(f"| {sp.name} | {lay.kind}{' s2' if lay.stride == 2 else ''} | {sp.tokens} | {sp.K} | "
+                        f"{sp.C_out} | {'prev' if src[i] is not None else 'own'} | {ks} | {us:.2f} | "
+                        f"{sp.dense_flops / (us * 1e-6) / 1e12:.1f} | {rms[i]:.3f} |\n")
+    out = {
         "metric": "dense-equivalent TFLOP/s of the AQ layer forward",
-        "value": round(tflops, 3),
+        "value": round(total_flops / (pass_us * 1e-6) / 1e12, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,
-        "steps": 7,
-        "warmup": 1,
-        "ms_per_step": round(whole_us / 1e3, 6),
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(pass_us / 1e3, 6),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f16",
-        "data": "synthetic (seeded; LDM-4-shaped U-Net layers, random codebooks/codes/activations)",
-        "config": {"workload": f"unet_sweep_b8_{a.variant}{'_full' if a.full else ''}", "layers": len(rows),
-                   "launch": "hip graph of the whole pass"},
-        "hbm_gbs_algorithmic": round(total_bytes / (whole_us * 1e-6) / 1e9, 3),
+        "data": "synthetic (seeded; LDM-4-shaped U-Net layers at batch 8, random codebooks/codes/activations, "
+                "chained where shapes allow)",
+        "config": {"workload": workload, "layers": len(layers), "chained_inputs": sum(s is not None for s in src),
+                   "launch": "hip graph of the whole pass", "format": f"{a.variant}: g={9 if kaq else 8}/8, M={M}, B=8"},
+        "hbm_gbs_algorithmic": round(total_bytes / (pass_us * 1e-6) / 1e9, 3),
         "algorithmic_bytes": total_bytes,
         "dense_flops": total_flops,
-        "per_layer_sum_us": round(per_layer_sum, 3),
-        "roofline": {"bound": "mfma", "achieved": round(tflops, 3), "peak": PEAK_MFMA_F16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / PEAK_MFMA_F16_TFLOPS, 4), "traffic": None},
+        "roofline": {"bound": "mfma", "achieved": round(k_tflops, 3), "peak": PEAK_MFMA_F16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(k_tflops / PEAK_MFMA_F16_TFLOPS, 4),
+                     "traffic": measured_traffic_kernel(workload, kname), "kernel": kname, "launches": k_n,
+                     "kernel_avg_us": round(k_us / k_n, 3), "kernel_flops": k_flops, "timing": tmode,
+                     "pass_frac": round(total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS, 4)},
+        "kernels": [{"kernel": n, "launches": c, "total_us": round(t, 2)} for n, t, c, _ in ktable[:6]],
+        "activation_rms": [round(min(rms), 4), round(max(rms), 4)],
     }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = sweep_cpu_baseline(specs, seeds)
+    for layer, _, _ in objs:
+        layer.close()
+    return out
 
 
 def lut_regime_bench(a, torch, P, W):
@@ -348,9 +535,10 @@ def grad_bench(a, torch, P, W):
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="conv64")
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 20 passes, 200 forwards)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 3 passes, 20 forwards)")
+    ap.add_argument("--config", default="sweep", help="sweep (default), lutregime, or one layer: tiny, conv64, "
+                                                      "qkv16, conv8")
     ap.add_argument("--path", default="auto", choices=["auto", "lut", "decode"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="launch every step from Python instead of a HIP graph")
@@ -367,6 +555,14 @@ def main(argv=None):
     if a.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {a.gpus}); the AQ layer forward is not sharded "
               "across GPUs in this build", file=sys.stderr)
+        return 2
+
+    if a.steps is None:
+        a.steps = 20 if a.config == "sweep" else 200
+    if a.warmup is None:
+        a.warmup = 3 if a.config == "sweep" else 20
+    if a.steps < 1:
+        print("--steps must be >= 1", file=sys.stderr)
         return 2
 
     import numpy as np
@@ -444,24 +640,23 @@ def main(argv=None):
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / steps
 
-    # A decode-path forward with the in-loop decode is one kernel launch, and
-    # graph replay leaves next to no gap between launches (rocprofv3's kernel
-    # trace of this same command agrees within a few percent), so the per-step
-    # time is that kernel's average duration.  A pre-decoded forward is two
-    # launches (operand records, then the product), and a LUT forward is two
-    # (table+gather, then the chunk reduction): their figure covers both.
-    kms = ms
+    # The dominant kernel's own duration: timing events around every launch of
+    # ten forwards in one graph (a pre-decoded forward is two launches, records
+    # then product; a table-path forward is table+gather then reduction).
+    per_layer, tmode, _ = launch_times(torch, [(layer, lambda: layer.forward(x, xs, out=y))] * 10)
     flops = spec.dense_flops
+    kname, k_us_tot, k_n, k_flops, ktable = dominant_kernel(per_layer, [flops] * len(per_layer))
+    kms = k_us_tot / k_n / 1e3
     tflops = flops / (ms * 1e-3) / 1e12
     gbs = algorithmic_bytes(spec) / (ms * 1e-3) / 1e9
-    k_tflops = flops / (kms * 1e-3) / 1e12
+    k_tflops = (k_flops / k_n) / (kms * 1e-3) / 1e12
     k_gbs = algorithmic_bytes(spec) / (kms * 1e-3) / 1e9
     if a.copy_bytes > 0:
         src = torch.empty(a.copy_bytes, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
-    traffic = measured_traffic(a.config)
+    traffic = measured_traffic_kernel(a.config, kname)
     if path == "decode" and spec.tile_dtype != "f32":
         roof = {"bound": "mfma", "achieved": round(k_tflops, 3), "peak": PEAK_MFMA_F16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(k_tflops / PEAK_MFMA_F16_TFLOPS, 4), "traffic": traffic}
@@ -471,7 +666,9 @@ def main(argv=None):
     else:
         roof = {"bound": "hbm", "achieved": round(k_gbs, 3), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(k_gbs / PEAK_HBM_GBS, 4), "traffic": traffic}
-    roof["kernel_us"] = round(kms * 1e3, 3)
+    roof["kernel"] = kname
+    roof["kernel_avg_us"] = round(kms * 1e3, 3)
+    roof["timing"] = tmode
 
     out = {
         "metric": "dense-equivalent TFLOP/s of the AQ layer forward",
@@ -492,6 +689,7 @@ def main(argv=None):
         "algorithmic_bytes": algorithmic_bytes(spec),
         "dense_flops": flops,
         "roofline": roof,
+        "kernels": [{"kernel": n, "launches": c // 10, "avg_us": round(t / c, 3)} for n, t, c, _ in ktable],
     }
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(spec, inp)

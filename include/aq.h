@@ -220,6 +220,35 @@ typedef enum {
 aq_status aq_layer_set_option(aq_layer* layer, int32_t option, int64_t value);
 aq_status aq_layer_get_option(const aq_layer* layer, int32_t option, int64_t* value);
 
+/*
+ * Launch timing without a profiler.  After aq_layer_set_launch_events with n
+ * events (hipEvent_t handles created by the caller with timing enabled), each
+ * later aq_layer_forward or aq_layer_codebook_grad call on the layer records
+ * events[0] on its stream before its first kernel launch and events[k] right
+ * after its k-th launch (k < n; further launches are not bracketed).  Calls
+ * on a stream under graph capture record no events (the runtime has no
+ * external event nodes).  hipEventElapsedTime(events[k-1], events[k]) is then
+ * the duration of launch k (plus the gap before it).  n = 0 stops
+ * the recording; n is at most 64.  The events stay owned by the caller and
+ * must outlive their use.
+ * aq_layer_last_launches reports how many kernels the layer's last forward or
+ * gradient call launched and, in `names` (truncated to names_size - 1 bytes
+ * and terminated), their kernels one per line, as name<template arguments>
+ * with the arguments as integers (a code type as its bit width).
+ */
+aq_status aq_layer_set_launch_events(aq_layer* layer, void* const* events, int32_t n_events);
+aq_status aq_layer_last_launches(const aq_layer* layer, int32_t* n_launches, char* names, int64_t names_size);
+
+/*
+ * Text description of the route a forward over n tokens (linear) or images
+ * (conv) would take, as "key=value" pairs: the path and kernel route, and for
+ * the matrix-core kernels the weight source (in-loop decode or pre-decoded
+ * records, with the bytes the records write), tile, K split and workgroup
+ * order.  Pure host function; `buf` receives at most size - 1 characters and
+ * a terminating zero.
+ */
+aq_status aq_layer_describe(const aq_layer* layer, int64_t n, char* buf, int64_t size);
+
 /* The path a forward over `tokens` tokens would take (pure host function). */
 aq_status aq_layer_choose_path(const aq_layer* layer, int64_t tokens, aq_path* out);
 

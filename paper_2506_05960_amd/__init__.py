@@ -18,6 +18,9 @@ from .aq import (  # noqa: F401
     aq_layer_set_path,
     aq_layer_set_option,
     aq_layer_get_option,
+    aq_layer_set_launch_events,
+    aq_layer_last_launches,
+    aq_layer_describe,
     OPTION_CODES,
     aq_layer_choose_path,
     aq_layer_destroy,

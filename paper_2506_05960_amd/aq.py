@@ -30,8 +30,9 @@ OPTION_CODES = {"lut_max_tokens": 1, "weights": 2, "generic": 3, "record_product
 _TILE_OPTIONS = ("fused_tile", "dense_tile", "grad_tile")
 
 EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
-            "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_choose_path",
-            "aq_layer_destroy", "aq_last_error", "aq_version")
+            "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
+            "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy",
+            "aq_last_error", "aq_version")
 
 
 class AQError(RuntimeError):
@@ -79,11 +80,14 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_set_path.argtypes = [vp, i32]
     lib.aq_layer_set_option.argtypes = [vp, i32, i64]
     lib.aq_layer_get_option.argtypes = [vp, i32, ctypes.POINTER(ctypes.c_int64)]
+    lib.aq_layer_set_launch_events.argtypes = [vp, ctypes.POINTER(vp), i32]
+    lib.aq_layer_last_launches.argtypes = [vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_char_p, i64]
+    lib.aq_layer_describe.argtypes = [vp, i64, ctypes.c_char_p, i64]
     lib.aq_layer_choose_path.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_int)]
     lib.aq_layer_destroy.argtypes = [vp]
     for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
-              "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_choose_path",
-              "aq_layer_destroy"):
+              "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
+              "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy"):
         getattr(lib, f).restype = ctypes.c_int
     lib.aq_last_error.restype = ctypes.c_char_p
     lib.aq_last_error.argtypes = []
@@ -151,6 +155,32 @@ def aq_layer_get_option(handle: int, option: int) -> int:
     out = ctypes.c_int64()
     _check(load_library().aq_layer_get_option(handle, option, ctypes.byref(out)))
     return out.value
+
+
+def aq_layer_set_launch_events(handle: int, events) -> None:
+    """``events``: HIP event handles (ints), recorded around the layer's later kernel launches."""
+    arr = (ctypes.c_void_p * max(1, len(events)))(*events)
+    _check(load_library().aq_layer_set_launch_events(handle, arr, len(events)))
+
+
+def aq_layer_last_launches(handle: int):
+    """(number of kernel launches of the layer's last call, their kernel names)."""
+    n = ctypes.c_int32()
+    buf = ctypes.create_string_buffer(4096)
+    _check(load_library().aq_layer_last_launches(handle, ctypes.byref(n), buf, len(buf)))
+    names = buf.value.decode()
+    return n.value, (names.split("\n") if names else [])
+
+
+def aq_layer_describe(handle: int, n: int) -> dict:
+    """The route a forward over ``n`` tokens (linear) or images (conv) would take, as a dict."""
+    buf = ctypes.create_string_buffer(1024)
+    _check(load_library().aq_layer_describe(handle, n, buf, len(buf)))
+    out = {}
+    for kv in buf.value.decode().split(" "):
+        k, _, v = kv.partition("=")
+        out[k] = v
+    return out
 
 
 def aq_layer_choose_path(handle: int, tokens: int) -> str:
@@ -322,6 +352,19 @@ class AQLayer:
 
     def choose_path(self, tokens: int) -> str:
         return aq_layer_choose_path(self.handle, tokens)
+
+    def set_launch_events(self, events) -> None:
+        """torch.cuda.Event objects (timing enabled, recorded once so they exist) or raw handles."""
+        hs = [e if isinstance(e, int) else e.cuda_event for e in events]
+        if any(h == 0 for h in hs):
+            raise ValueError("events must exist: record each torch.cuda.Event once first")
+        aq_layer_set_launch_events(self.handle, hs)
+
+    def last_launches(self):
+        return aq_layer_last_launches(self.handle)
+
+    def describe(self, n: int) -> dict:
+        return aq_layer_describe(self.handle, n)
 
     def close(self) -> None:
         if getattr(self, "handle", None):

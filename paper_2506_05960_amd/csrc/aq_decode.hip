@@ -59,6 +59,7 @@ static hipError_t decode_dispatch_tile(const Geom& geo, const DeviceWeights& w, 
                                                                               geo.C_out, geo.G, geo.g, geo.M, geo.B);
         break;
     }
+    note_launch(st, "decode_to_global_kernel", {CBT, 8 * (int)sizeof(CodeT), tile});
     return hipGetLastError();
 }
 
@@ -245,6 +246,7 @@ static hipError_t records_dispatch(const Geom& geo, const FusedPlan& plan, const
             else AQ_REC16(false, 4);
         }
 #undef AQ_REC16
+        note_launch(st, "operand_records_f16_kernel", {8 * (int)sizeof(CodeT), plan.kind == 1, geo.M});
         return hipGetLastError();
     }
 #define AQ_REC(CBT)                                                                                             \
@@ -263,6 +265,7 @@ static hipError_t records_dispatch(const Geom& geo, const FusedPlan& plan, const
     case AQ_F16: AQ_REC(AQ_F16) break;
     default: AQ_REC(AQ_BF16) break;
     }
+    note_launch(st, "operand_records_kernel", {w.cb_dtype, 8 * (int)sizeof(CodeT), plan.kind == 1, geo.g});
 #undef AQ_REC
     return hipGetLastError();
 }

@@ -88,6 +88,7 @@ static hipError_t f32_launch_codes(const Geom& geo, const DeviceWeights& w, cons
     case AQ_BF16: f32_fwd_kernel<AQ_BF16, CodeT><<<grid, 256, 0, st>>>(geo, w.cb32, codes, w.scales, X, x_scales, Y, y_dtype); break;
     default: f32_fwd_kernel<AQ_I8, CodeT><<<grid, 256, 0, st>>>(geo, w.cb32, codes, w.scales, X, x_scales, Y, y_dtype); break;
     }
+    note_launch(st, "f32_fwd_kernel", {x_dtype, 8 * (int)sizeof(CodeT)});
     return hipGetLastError();
 }
 

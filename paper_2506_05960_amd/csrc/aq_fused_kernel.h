@@ -5,6 +5,12 @@
 // w, w+4, w+8, ... and accumulates the whole tile for them, so the main loop
 // needs no workgroup barrier.  At the end the four partial tiles meet in LDS
 // and each wave sums (in a fixed order) and stores a quarter of the tile.
+// With a K split over S workgroups (layers with too few tiles to fill the
+// chip), workgroup s of a tile takes chunks 4 s + w, 4 s + w + 4 S, ...;
+// each writes its fp32 partial tile to a workspace and bumps the tile's
+// arrival counter, and the last to arrive adds the S partials in split order
+// (so the result does not depend on arrival order), stores Y and resets the
+// counter for the next launch.
 //
 // Operands.  v_mfma_f32_32x32x16_f16 takes 8 fp16 values per lane for each
 // operand; lane l holds row (l % 32) and a k-slice of 8 chosen by (l / 32).
@@ -171,7 +177,7 @@ template <int KIND, int CM, int XT, int DEC, int MC, int BM, int BN, int UPL, in
 __global__ void __launch_bounds__(256, OCC)
 fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const uint8_t* __restrict__ crec,
                  const float* __restrict__ scales, const void* __restrict__ X, const float* __restrict__ x_scales,
-                 void* __restrict__ Y, int y_dtype) {
+                 void* __restrict__ Y, int y_dtype, float* __restrict__ part, uint32_t* __restrict__ arrivals) {
     constexpr bool CONV = KIND != 0;
     constexpr int KH = KIND == 1 ? 3 : 1;
     constexpr int NS = KIND == 1 ? 9 : CM;         // MFMA steps per chunk (= groups per lane)
@@ -192,7 +198,8 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                  "s"(plan.nmajor), "s"(plan.units), "s"(plan.tile_div), "s"(plan.rec_bytes), "s"(plan.inv_pr),
                  "s"(plan.inv_ow), "s"(plan.cb_bytes), "s"(plan.x_bytes), "s"(plan.total_rows), "s"(plan.inv_wp),
                  "s"(plan.inv_tile_div), "s"(plan.inv_oh), "s"(cb), "s"(crec), "s"(X), "s"(gridDim.x),
-                 "s"(plan.sr), "s"(plan.rpb), "s"(plan.inv_sr), "s"(plan.inv_rpb));
+                 "s"(plan.sr), "s"(plan.rpb), "s"(plan.inv_sr), "s"(plan.inv_rpb), "s"(plan.splitk),
+                 "s"(plan.ntiles), "s"(plan.inv_ntiles));
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     // uniform per wave: held in a scalar register, so chunk offsets are scalar arithmetic
@@ -203,12 +210,17 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     // so id h runs on XCD h % 8.  Giving each XCD a contiguous range of logical
     // tiles (output-channel tile fastest) keeps the input rows a token tile
     // shares with its neighbours, and with its other channel tiles, in one L2.
-    int tile_m, tile_n;
+    int tile_m, tile_n, tile_lin, ksplit;
     {
         const int nwg = (int)gridDim.x, h = (int)blockIdx.x;
         const int xcd = h & 7, j = h >> 3;
         const int per = nwg >> 3, rem = nwg & 7;
-        const int L = xcd * per + min(xcd, rem) + j;
+        const int Lg = xcd * per + min(xcd, rem) + j;
+        // K split slowest: an XCD's range of workgroups covers one split (the
+        // same K range) of neighbouring tiles
+        ksplit = __builtin_amdgcn_readfirstlane(fdiv(Lg, plan.ntiles, plan.inv_ntiles));
+        const int L = Lg - ksplit * plan.ntiles;
+        tile_lin = L;
         // plan.nmajor: channel tile slowest (an XCD's range then covers few
         // channel tiles, so the weight operands it streams stay in its L2);
         // else token tile slowest.  The host supplies the count of the fastest
@@ -218,6 +230,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         tile_n = plan.nmajor ? hi : lo;
         tile_m = plan.nmajor ? lo : hi;
     }
+    const int cstep = kWaves * plan.splitk;          // chunk stride of one wave
     const int T0 = tile_m * BM;                     // token and element counts fit in 31 bits (host check)
     const int N0 = tile_n * BN;
     const int tokens = (int)geo.tokens;
@@ -394,7 +407,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
 
     // Prologue, first part: the chunk's codes and activations go out right
     // after the codebook, before the remaining index arithmetic.
-    int chunk = wave;
+    int chunk = wave + kWaves * ksplit;
     codes_load(chunk);
     stage_load(chunk);
     __builtin_amdgcn_sched_barrier(0);   // issue them here, not next to their uses
@@ -522,11 +535,11 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
             constexpr int P = decltype(pc)::value;
             const uint8_t* cur = P ? pbuf1 : pbuf0;
             uint8_t* nxt = P ? pbuf0 : pbuf1;
-            stage_load(c + kWaves);
+            stage_load(c + cstep);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-                rec_step(rec[1 - P][s], c + kWaves, s);
+                rec_step(rec[1 - P][s], c + cstep, s);
                 if (s == NS / 2) {
                     wave_sync();
                     stage_store(nxt);
@@ -551,9 +564,9 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
-        for (; chunk + kWaves < plan.nchunk; chunk += 2 * kWaves) {
+        for (; chunk + cstep < plan.nchunk; chunk += 2 * cstep) {
             body(std::integral_constant<int, 0>{}, chunk);
-            body(std::integral_constant<int, 1>{}, chunk + kWaves);
+            body(std::integral_constant<int, 1>{}, chunk + cstep);
         }
         if (chunk < plan.nchunk) body(std::integral_constant<int, 0>{}, chunk);
     } else {
@@ -564,17 +577,17 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     wave_sync();
     load_af(pbuf0, af);
     int it = 0;
-    for (; chunk < plan.nchunk; chunk += kWaves, ++it) {
+    for (; chunk < plan.nchunk; chunk += cstep, ++it) {
         uint8_t* nxt = (it & 1) ? pbuf0 : pbuf1;
-        const bool more = chunk + kWaves < plan.nchunk;
+        const bool more = chunk + cstep < plan.nchunk;
         uint32_t crn[AN][REC_DW];
 #pragma unroll
         for (int b = 0; b < AN; ++b)
 #pragma unroll
             for (int d = 0; d < REC_DW; ++d) crn[b][d] = crg[b][d];
         if (more) {
-            stage_load(chunk + kWaves);   // next chunk's activations and codes
-            codes_load(chunk + kWaves);
+            stage_load(chunk + cstep);   // next chunk's activations and codes
+            codes_load(chunk + cstep);
         }
 #pragma unroll
         for (int b = 0; b < AN; ++b) {
@@ -586,7 +599,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
                     decode_block(crn[b + 1], chunk, b + 1, dnext);
                     have_next = true;
                 } else if (more) {
-                    decode_block(crg[0], chunk + kWaves, 0, dnext);   // block 0 of the next chunk
+                    decode_block(crg[0], chunk + cstep, 0, dnext);   // block 0 of the next chunk
                     have_next = true;
                 }
             } else {
@@ -694,6 +707,7 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     constexpr int TASKS = (ROWS / 4) * (COLS / 8);   // (4 rows, 8 columns) per task
     static_assert(TASKS <= 256, "one epilogue task per thread");
     const int task = tid;
+    floatx4 v[8];
     if (task < TASKS) {
         const int c8 = (task / (ROWS / 4)) * 8;
         const int rq = task - (task / (ROWS / 4)) * (ROWS / 4);
@@ -702,9 +716,57 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         for (int w = 0; w < kWaves; ++w)
 #pragma unroll
             for (int c = 0; c < 8; ++c) pv[w][c] = red[(w * (ROWS / 4) + rq) * COLSP + c8 + c];
-        floatx4 v[8];
 #pragma unroll
         for (int c = 0; c < 8; ++c) v[c] = ((pv[0][c] + pv[1][c]) + pv[2][c]) + pv[3][c];
+    }
+    if (plan.splitk > 1) {
+        // K split over workgroups: publish this split's partial tile, count the
+        // arrival; the last workgroup of the tile sums every split in order.
+        // The partial tiles are written and read with device-coherent accesses
+        // (agent-scope atomic stores and loads, which bypass the per-XCD L2's
+        // stale copies), so no cache-wide write-back or invalidation is needed:
+        // each thread's stores have completed (vmcnt 0) before the barrier that
+        // precedes the arrival count, and the loads are issued after it.
+        // Layout [tile][split][16][TASKS] of 8-byte pairs, task fastest: each
+        // store and load instruction covers 64 consecutive pairs (512 bytes).
+        const int S = plan.splitk;
+        uint64_t* mine = reinterpret_cast<uint64_t*>(part) + (size_t)(tile_lin * S + ksplit) * TASKS * 16 + task;
+        if (task < TASKS) {
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                __hip_atomic_store(mine + (2 * c) * TASKS,
+                                   (uint64_t)__float_as_uint(v[c][0]) | ((uint64_t)__float_as_uint(v[c][1]) << 32),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(mine + (2 * c + 1) * TASKS,
+                                   (uint64_t)__float_as_uint(v[c][2]) | ((uint64_t)__float_as_uint(v[c][3]) << 32),
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        wait_vmcnt<0>();
+        __syncthreads();                         // (every thread is also done reading the partial tiles in LDS)
+        uint32_t* arrived = reinterpret_cast<uint32_t*>(lds);
+        if (tid == 0) *arrived = __hip_atomic_fetch_add(arrivals + tile_lin, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        if (*arrived != (uint32_t)(S - 1)) return;   // not the last split of this tile (uniform)
+        if (task < TASKS) {
+            const uint64_t* p0 = reinterpret_cast<const uint64_t*>(part) + (size_t)(tile_lin * S) * TASKS * 16 + task;
+            for (int k = 0; k < S; ++k) {
+                const uint64_t* pk = p0 + (size_t)k * TASKS * 16;
+#pragma unroll
+                for (int c = 0; c < 8; ++c) {
+                    const uint64_t lo = __hip_atomic_load(pk + (2 * c) * TASKS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const uint64_t hi = __hip_atomic_load(pk + (2 * c + 1) * TASKS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const floatx4 q{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
+                                    __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
+                    v[c] = k == 0 ? q : v[c] + q;          // splits added in order 0, 1, ..., S - 1
+                }
+            }
+        }
+        if (tid == 0) __hip_atomic_store(arrivals + tile_lin, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (task < TASKS) {
+        const int c8 = (task / (ROWS / 4)) * 8;
+        const int rq = task - (task / (ROWS / 4)) * (ROWS / 4);
         // Columns are tokens (convolution: 8 consecutive tokens stay in one image
         // plane when the plane size is a multiple of 8) or output channels
         // (linear: 16-byte aligned when C_out is a multiple of 8).
@@ -778,9 +840,10 @@ static hipError_t fused_launch_cfg(const Geom& geo, const FusedPlan& plan, const
     auto kern = fused_fwd_kernel<KIND, CM, XT, DEC, MC, BM, BN, UPL, OCC>;
     hipError_t e = ensure_dynamic_lds((const void*)kern, plan.lds_bytes);
     if (e != hipSuccess) return e;
-    const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN)));
+    const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN) * plan.splitk));
     kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.cb, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y,
-                                                   fl.y_dtype);
+                                                   fl.y_dtype, fl.part, fl.arrivals);
+    note_launch(fl.stream, "fused_fwd_kernel", {KIND, CM, XT, DEC, MC, BM, BN, UPL, OCC});
     return hipGetLastError();
 }
 

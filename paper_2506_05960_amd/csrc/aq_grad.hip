@@ -689,6 +689,7 @@ hipError_t wgrad_launch(const Geom& geo, const GradArgs& ga, hipStream_t st) {
     const int total = ga.S * ga.tiles_m * ga.tiles_n;
     const unsigned grid = (unsigned)(8 * ((total + 7) / 8));
     wgrad_kernel<KIND, DT, BM, BN><<<grid, 256, 0, st>>>(geo, ga);
+    note_launch(st, "wgrad_kernel", {KIND, DT, BM, BN});
     return hipGetLastError();
 }
 
@@ -697,6 +698,7 @@ hipError_t wgrad_dma_launch(const Geom& geo, const GradArgs& ga, const uint8_t* 
     const int total = ga.S * ga.tiles_m * ga.tiles_n;
     const unsigned grid = (unsigned)(8 * ((total + 7) / 8));
     wgrad_conv_dma_kernel<KIND, DT, BM, BNP><<<grid, 256, 0, st>>>(geo, ga, zero);
+    note_launch(st, "wgrad_conv_dma_kernel", {KIND, DT, BM, BNP});
     return hipGetLastError();
 }
 
@@ -809,6 +811,7 @@ hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, 
             wgrad_linear_dma_kernel<AQ_BF16><<<grid, 256, 0, st>>>(geo, ga, z16);
         else
             wgrad_linear_dma_kernel<AQ_F16><<<grid, 256, 0, st>>>(geo, ga, z16);
+        note_launch(st, "wgrad_linear_dma_kernel", {dtype});
         e = hipGetLastError();
     } else if (gp.dma) {
         e = kind == 1 ? (dtype == AQ_BF16 ? wgrad_dma_dispatch<1, AQ_BF16>(geo, gp, ga, z16, st)
@@ -832,6 +835,7 @@ hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, 
         const int64_t n4 = std::max<int64_t>(1, slice / 4);
         const unsigned grid = (unsigned)std::min<int64_t>((n4 + 255) / 256, 4096);
         split_sum_kernel<<<grid, 256, 0, st>>>(P, slice, ga.S);
+        note_launch(st, "split_sum_kernel", {});
         e = hipGetLastError();
         if (e != hipSuccess) return e;
         S_gather = 1;
@@ -847,6 +851,7 @@ hipError_t launch_codebook_grad(const Geom& geo, const GradPlan& gp, int dtype, 
         cbgrad_gather_kernel<256><<<(unsigned)buckets, 256, 0, st>>>(P, slice, S_gather, offs, ent, nent, nk, geo.M,
                                                                      geo.g, dC);
     }
+    note_launch(st, "cbgrad_gather_kernel", {nent / nk < 64 ? 64 : 256});
     return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <initializer_list>
 #include <vector>
 
 #include "aq.h"
@@ -38,6 +39,11 @@ struct Options {
 };
 
 constexpr int kMaxSplitK = 8;   // most workgroups sharing one output tile along K
+
+// Launch trace of the entry point running on this thread (aq_layer_set_launch_events):
+// every launcher reports each kernel it puts on `st` right after the launch, by
+// name and template arguments, so that the caller's timing events bracket it.
+void note_launch(hipStream_t st, const char* kernel, std::initializer_list<int> template_args);
 
 // Raise a kernel's dynamic-LDS limit to at least `bytes` on the current
 // device (once per kernel and device; thread-safe).
@@ -102,6 +108,9 @@ struct FusedPlan {
     int64_t x_bytes;      // bytes of this forward's input X (the bound of the kernel's activation loads)
     int tile_div;         // tiles along the faster tile index (token tiles if nmajor, else channel tiles)
     float inv_tile_div;   // its fp32 reciprocal
+    int splitk;           // workgroups sharing one tile along K (1: no split)
+    int ntiles;           // output tiles (the grid is ntiles * splitk workgroups)
+    float inv_ntiles;     // its fp32 reciprocal
 };
 
 struct FusedLaunch {
@@ -114,6 +123,8 @@ struct FusedLaunch {
     int y_dtype;
     int x_dtype;
     hipStream_t stream;
+    float* part;          // K split: fp32 partial tiles [ntiles][splitk][BM * BN] (null without a split)
+    uint32_t* arrivals;   // K split: arrival counter per tile, zero between launches
 };
 
 hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);

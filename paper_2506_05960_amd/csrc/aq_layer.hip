@@ -1,6 +1,7 @@
 // C ABI entry points: argument validation (host only, before any HIP call),
 // device copies and repacking of the quantized weights, path dispatch.
 #include <algorithm>
+#include <cmath>
 #include <cstdio>
 #include <cstdint>
 #include <cstdlib>
@@ -34,6 +35,9 @@ struct aq_layer {
     void* d_wrec;             // fused-path operand records, decoded per forward in the pre-decoded mode
     void* d_xpack;            // dense product: activations repacked per forward
     void* d_zero;             // 256 zero bytes
+    float* d_part;            // fused kernel K split: fp32 partial tiles
+    size_t part_bytes;        // bytes at d_part
+    uint32_t* d_arrivals;     // fused kernel K split: one arrival counter per tile (zero between launches)
     // codebook gradient, prepared by the first gradient call
     bool grad_ready;
     aq::GradPlan gplan;
@@ -46,9 +50,48 @@ struct aq_layer {
     aq_path path;
     int64_t lut_max_tokens;   // the measured rule for this layer
     aq::Options opt;
+    std::vector<hipEvent_t> events;   // caller's timing events (aq_layer_set_launch_events)
+    int32_t last_launches;            // kernel launches of the last traced call
+    std::string last_names;           // and their kernels, one per line
 };
 
 namespace aq {
+
+namespace {
+
+struct LaunchTrace {
+    bool active = false;
+    const hipEvent_t* ev = nullptr;
+    int n_ev = 0;
+    int count = 0;
+    hipError_t err = hipSuccess;
+    std::string names;
+};
+thread_local LaunchTrace g_trace;
+
+}  // namespace
+
+void note_launch(hipStream_t st, const char* kernel, std::initializer_list<int> template_args) {
+    LaunchTrace& t = g_trace;
+    if (!t.active) return;
+    if (!t.names.empty()) t.names += '\n';
+    t.names += kernel;
+    if (template_args.size()) {
+        t.names += '<';
+        bool first = true;
+        for (int a : template_args) {
+            if (!first) t.names += ", ";
+            t.names += std::to_string(a);
+            first = false;
+        }
+        t.names += '>';
+    }
+    ++t.count;
+    if (t.ev && t.count < t.n_ev && t.err == hipSuccess) {
+        t.err = hipEventRecordWithFlags(t.ev[t.count], st, 0u);
+        if (t.err != hipSuccess) (void)hipGetLastError();
+    }
+}
 
 hipError_t ensure_dynamic_lds(const void* kernel, size_t bytes) {
     static std::mutex mu;
@@ -80,6 +123,37 @@ aq_status hip_fail(hipError_t e, const char* what) {
         return fail(AQ_ERR_OUT_OF_MEMORY, std::string(what) + ": " + hipGetErrorString(e));
     return fail(AQ_ERR_DEVICE, std::string(what) + ": " + hipGetErrorString(e));
 }
+
+// Starts the launch trace of one entry-point call: event 0 is recorded on the
+// call's stream before its first launch.  A stream under graph capture gets
+// no event records (this runtime has no external event nodes).  A failed
+// record is reported by the entry point and cleared from the runtime's
+// last-error state, which the launchers read.
+struct TraceScope {
+    aq_layer* L;
+    explicit TraceScope(aq_layer* layer, hipStream_t st) : L(layer) {
+        aq::LaunchTrace& t = aq::g_trace;
+        t = aq::LaunchTrace{};
+        t.active = true;
+        t.ev = L->events.empty() ? nullptr : L->events.data();
+        t.n_ev = (int)L->events.size();
+        if (t.ev) {
+            hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+            t.err = hipStreamIsCapturing(st, &cs);
+            if (t.err == hipSuccess && cs != hipStreamCaptureStatusNone) t.ev = nullptr;
+            if (t.err == hipSuccess && t.ev) t.err = hipEventRecordWithFlags(t.ev[0], st, 0u);
+            if (t.err != hipSuccess) (void)hipGetLastError();
+        }
+    }
+    hipError_t error() const { return aq::g_trace.err; }
+    ~TraceScope() {
+        aq::LaunchTrace& t = aq::g_trace;
+        L->last_launches = t.count;
+        L->last_names = t.names;
+        t.active = false;
+        t.ev = nullptr;
+    }
+};
 
 size_t dtype_bytes(int dt) {
     switch (dt) {
@@ -161,7 +235,7 @@ void free_layer(aq_layer* L) {
     if (!L) return;
     void* ptrs[] = {L->d_cb,     L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales,
                     L->d_ws,     L->d_crec, L->d_wrec,   L->d_xpack, L->d_zero, L->d_gidx_offs,
-                    L->d_gidx_ent, L->d_gpart};
+                    L->d_gidx_ent, L->d_gpart, L->d_part, L->d_arrivals};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete L;
@@ -283,7 +357,26 @@ struct TileCand {
 
 // Per-forward tile choice; fills the remaining plan fields.  Returns false when
 // no instantiated tile fits (the caller then uses the generic kernel).
-bool fused_plan_tile(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) {
+// K split over workgroups (fused kernel): a layer whose tiles do not fill one
+// round of the compute units may give each tile to S workgroups that share its
+// K chunks.  Cost per workgroup in chunk-time units: the chunks of one wave,
+// plus the fixed prologue and epilogue, plus one for publishing and summing the
+// partial tiles.  Layers that fill the chip keep the fitted model (fixed cost
+// about three chunks); for under-filled layers (fewer than 256 tiles of 64 x 64)
+// the fixed cost measured about twelve chunks on the U-Net's 512-token
+// convolutions, and the in-loop decode's codeword gathers (per output channel
+// and codebook) weigh against the products (per token and channel) by a factor
+// 1 + M 32 / BM (measured: M = 2 favours 64 x 64 tiles, M = 4 128 x 64).
+constexpr double kFixedChunks = 3.0;
+constexpr double kFixedChunksUnderfilled = 12.0;
+constexpr double kSplitChunks = 1.0;
+
+// Fewer than 256 tiles of 64 tokens x 64 channels: the layer cannot fill the chip.
+bool underfilled(const Geom& geo) {
+    return ((geo.tokens + 63) / 64) * (int64_t)((geo.C_out + 63) / 64) < 256;
+}
+
+bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, aq::FusedPlan* p) {
     static const TileCand conv3[] = {{64, 96, 3}, {64, 64, 3}, {128, 64, 3}, {128, 64, 6}, {64, 64, 6}};
     static const TileCand conv1[] = {{64, 96, 4}, {64, 64, 4}};
     static const TileCand lin[] = {{64, 96, 8}, {64, 64, 8}, {32, 128, 4}, {32, 64, 4}};
@@ -360,24 +453,43 @@ bool fused_plan_tile(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) 
         q.lds_bytes = (size_t)p->cb_bytes + std::max<size_t>((size_t)8 * q.pbuf_bytes, red);
         if (q.lds_bytes > kLdsBytes) continue;
         const int64_t nwg = ((geo.tokens + t.bm - 1) / t.bm) * (int64_t)((geo.C_out + t.bn - 1) / t.bn);
-        const int64_t rounds = (nwg + 255) / 256;
         // rounds of whole-chip work, weighted by a per-tile overhead term; linear
         // layers also weigh the staging units per lane (fitted to measured tiles)
-        double cost = (double)rounds * t.bm * t.bn * (1.0 + 48.0 / t.bm + 48.0 / t.bn);
-        if (p->kind == 0) cost *= t.upl / (t.upl + 2.0);
+        double tcost = (double)t.bm * t.bn * (1.0 + 48.0 / t.bm + 48.0 / t.bn);
+        if (p->kind == 0) tcost *= t.upl / (t.upl + 2.0);
         // pre-decoded operands of a linear layer: the 64 x 64 tile measured best
-        if (p->kind == 0 && p->dec == aq::FUSED_DEC_REC && !(t.bm == 64 && t.bn == 64)) cost *= 1.25;
-        if (narrow && !widen) cost *= 1.15;             // bank conflicts on the A-fragment reads (measured)
-        if (!found || cost < best) {
-            best = cost;
-            bestp = q;
-            found = true;
+        if (p->kind == 0 && p->dec == aq::FUSED_DEC_REC && !(t.bm == 64 && t.bn == 64)) tcost *= 1.25;
+        if (narrow && !widen) tcost *= 1.15;             // bank conflicts on the A-fragment reads (measured)
+        const bool under = underfilled(geo);
+        if (under && p->dec == aq::FUSED_DEC_PK16) tcost *= 1.0 + 32.0 * p->mc / t.bm;
+        for (int S = 1; S <= aq::kMaxSplitK; ++S) {
+            if (opt.split_k != 0 && S != opt.split_k && !(S == 1 && opt.split_k > 1)) continue;
+            if (S > 1) {
+                if (opt.split_k == 0 && (!under || nwg * S > 256)) continue;   // planner: one round, under-filled layers
+                if (4 * S > p->nchunk) continue;                                 // every wave keeps a chunk
+                if ((size_t)S * nwg * t.bm * t.bn * 4 > part_cap) continue;
+                if (nwg * S >= (int64_t(1) << 24)) continue;
+            }
+            const int64_t rounds = (nwg * S + 255) / 256;
+            const double cpw = std::ceil((double)p->nchunk / (4.0 * S));
+            double cost = (double)rounds * tcost *
+                          (cpw + (under ? kFixedChunksUnderfilled : kFixedChunks) + (S > 1 ? kSplitChunks : 0.0));
+            // a forced split wins over the unsplit fallback of the same tile
+            if (opt.split_k > 1 && S == 1) cost *= 1e6;
+            if (!found || cost < best) {
+                best = cost;
+                bestp = q;
+                bestp.splitk = S;
+                bestp.ntiles = (int)nwg;
+                bestp.inv_ntiles = 1.0f / (float)nwg;
+                found = true;
+            }
         }
     }
     if (!found && want_bm) {
         aq::Options o = opt;
         o.fused_bm = o.fused_bn = 0;      // the forced tile does not fit: the planner's choice
-        return fused_plan_tile(geo, o, p);
+        return fused_plan_tile(geo, o, part_cap, p);
     }
     if (found) *p = bestp;
     return found;
@@ -453,6 +565,11 @@ bool use_predecoded(const aq_layer* L, const Geom& geo) {
     // measured on the U-Net layer shapes: the in-loop decode is repeated for every
     // token tile, so the single decode pass wins once tokens x M is large enough
     const int64_t tm = geo.tokens * p.mc;
+    // under-filled convolutions with K to split: the in-loop decode with a K split
+    // over workgroups (no record pass) measured faster on the U-Net's 512-token
+    // 3x3 layers for M = 2 and 4 (8 x 8 level, K = 8640: 21.8 / 27.1 us against
+    // 29.5 in-loop unsplit and 32.8 with records)
+    if (p.kind != 0 && p.dec == aq::FUSED_DEC_PK16 && underfilled(geo) && p.nchunk >= 8) return false;
     if (p.kind == 1) {
         // 3x3 convolutions of the U-Net shapes (both routes timed per shape): with
         // M = 4 the pre-decoded route won on every shape from 512 tokens up; with
@@ -474,6 +591,67 @@ bool use_predecoded(const aq_layer* L, const Geom& geo) {
         return p.mc >= 4 && geo.C_out >= 1152 && geo.tokens >= 2048;
     }
     return p.mc >= 4 && geo.tokens >= 32768;
+}
+
+// The route of one forward, resolved on the host (shared by the forward and
+// aq_layer_describe).
+struct Route {
+    enum Kind { LUT = 0, F32 = 1, GENERIC = 2, DENSE = 3, FUSED = 4, REC_LINEAR = 5, NONE = 6 } kind;
+    aq::FusedPlan fp;
+};
+
+Route plan_route(const aq_layer* L, const Geom& geo) {
+    Route r{};
+    const aq_layer_desc& d = L->desc;
+    if (choose(L, geo.tokens) == AQ_PATH_LUT) {
+        r.kind = Route::LUT;
+        return r;
+    }
+    if (d.tile_dtype == AQ_F32) {
+        r.kind = Route::F32;
+        return r;
+    }
+    const aq::Options& opt = L->opt;
+    aq::FusedPlan fp = L->fplan;
+    // the fused kernel uses 32-bit element and byte offsets
+    const int64_t nimg = geo.conv ? geo.tokens / ((int64_t)geo.OH * geo.OW) : 0;
+    const bool fits31 = geo.tokens * (int64_t)std::max(geo.K, geo.C_out) * 4 < (int64_t(1) << 31) &&
+                        (!geo.conv || nimg * (int64_t)geo.cin * geo.H * geo.W * 2 < (int64_t(1) << 31));
+    if (L->fused_ok && use_predecoded(L, geo)) {
+        // pre-decoded mode: operands decoded once per forward, then read with plain loads
+        fp.dec = aq::FUSED_DEC_REC;
+        fp.mc = 1;
+        fp.cb_bytes = 0;
+    }
+    auto order = [&opt](aq::FusedPlan& q) {
+        // channel-major order for pre-decoded convolution operands; linear layers
+        // measured faster token-major (qkv 8192 x 576 -> 1728: 59.5 vs 61.8 us)
+        q.nmajor = q.dec == aq::FUSED_DEC_REC && q.kind != 0;
+        if (opt.tile_order != 0) q.nmajor = opt.tile_order == 2;
+    };
+    aq::FusedPlan gp = fp;
+    // dense product over the records: a comparator route (AQ_OPT_RECORD_PRODUCT = 2);
+    // measured slower than the fused kernel's pre-decoded mode on most layer shapes here
+    if (L->fused_ok && fits31 && fp.dec == aq::FUSED_DEC_REC && opt.rec_product == 2 && gemm_plan_tile(geo, opt, &gp)) {
+        order(gp);
+        r.kind = Route::DENSE;
+        r.fp = gp;
+        return r;
+    }
+    if (L->fused_ok && fits31 && opt.generic != 1 && fused_plan_tile(geo, opt, L->part_bytes, &fp)) {
+        order(fp);
+        fp.tile_div = fp.nmajor ? (int)((geo.tokens + fp.bm - 1) / fp.bm) : (geo.C_out + fp.bn - 1) / fp.bn;
+        fp.inv_tile_div = 1.0f / (float)fp.tile_div;
+        fp.rlin_var = aq::rec_linear_tile(geo, opt.rlin_tile);
+        // a linear layer's records feed the 2 x 2 wave-split product (AQ_OPT_RECORD_PRODUCT = 1:
+        // the fused kernel's own pre-decoded mode, whose partial-tile order matches its in-loop mode)
+        const bool rlin = fp.dec == aq::FUSED_DEC_REC && opt.rec_product != 1 && aq::rec_linear_supported(geo, fp, d.x_dtype);
+        r.kind = rlin ? Route::REC_LINEAR : Route::FUSED;
+        r.fp = fp;
+        return r;
+    }
+    r.kind = geo.g == 8 ? Route::GENERIC : Route::NONE;
+    return r;
 }
 
 }  // namespace
@@ -599,6 +777,39 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
             free_layer(L);
             return hip_fail(e, "zero block");
         }
+        // K-split workspace: what the planner takes for a forward of max_tokens
+        // tokens in either weight mode (fewer tokens may split further only
+        // within it), and one arrival counter per smallest tile
+        {
+            const int64_t per = g1.conv ? (int64_t)g1.OH * g1.OW : 1;
+            const Geom gmax = make_geom(L, std::max<int64_t>(1, desc->max_tokens / per));
+            size_t need = 0;
+            for (int mode = 0; mode < 2; ++mode) {
+                aq::FusedPlan q = L->fplan;
+                if (mode == 1 || q.rec_only) {
+                    q.dec = aq::FUSED_DEC_REC;
+                    q.mc = 1;
+                    q.cb_bytes = 0;
+                }
+                // room for every split count the planner allows on its tile, so a
+                // forced split (AQ_OPT_SPLIT_K) fits too
+                if (fused_plan_tile(gmax, aq::Options{}, SIZE_MAX, &q) && q.ntiles < 256) {
+                    const int smax = std::min<int>({aq::kMaxSplitK, 512 / q.ntiles, q.nchunk / 4});
+                    if (smax > 1) need = std::max(need, (size_t)smax * q.ntiles * q.bm * q.bn * 4);
+                }
+            }
+            if (need) {
+                AQ_TRY(dev_upload(&L->d_part, nullptr, need, "split partial tiles"));
+                L->part_bytes = need;
+            }
+            const size_t ncnt = (size_t)((desc->max_tokens + 31) / 32) * ((C_out + 63) / 64);
+            AQ_TRY(dev_upload(&L->d_arrivals, nullptr, ncnt * 4, "split arrival counters"));
+            e = hipMemset(L->d_arrivals, 0, ncnt * 4);
+            if (e != hipSuccess) {
+                free_layer(L);
+                return hip_fail(e, "split arrival counters");
+            }
+        }
     }
 
     e = aq::launch_codebook_prep(L->d_cb, desc->codebook_dtype, (int64_t)cb_elems, L->d_cb32, L->d_cbtile,
@@ -623,73 +834,80 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
     if (d.x_dtype == AQ_I8 && !x_scales) return fail(AQ_ERR_INVALID_ARGUMENT, "int8 activations need x_scales");
     if ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 15)
         return fail(AQ_ERR_INVALID_ARGUMENT, "X and Y must be 16-byte aligned");
+    const Route r = plan_route(L, geo);
+    if (r.kind == Route::NONE)
+        return fail(AQ_ERR_UNSUPPORTED, "g = 9 layers run on the fused kernel only (it was disabled or its "
+                                        "tiles do not fit this shape)");
     const float* xs = d.x_dtype == AQ_I8 ? x_scales : nullptr;
     const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, d.codebook_dtype};
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    if (choose(L, geo.tokens) == AQ_PATH_LUT)
+    TraceScope trace(L, st);
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
+    hipError_t e = hipSuccess;
+    aq::FusedPlan fp = r.fp;
+    switch (r.kind) {
+    case Route::LUT:
         e = aq::launch_lut_forward(geo, w, L->plan, X, d.x_dtype, xs, Y, d.y_dtype, L->d_ws, st);
-    else if (d.tile_dtype == AQ_F32)
+        break;
+    case Route::F32:
         e = aq::launch_f32_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, st);
-    else {
-        aq::FusedPlan fp = L->fplan;
-        // the fused kernel uses 32-bit element and byte offsets
-        const bool fits31 = geo.tokens * (int64_t)std::max(geo.K, geo.C_out) * 4 < (int64_t(1) << 31) &&
-                            (!geo.conv || n * (int64_t)geo.cin * geo.H * geo.W * 2 < (int64_t(1) << 31));
-        if (L->fused_ok && use_predecoded(L, geo)) {
-            // pre-decoded mode: operands decoded once per forward, then read with plain loads
-            fp.dec = aq::FUSED_DEC_REC;
-            fp.mc = 1;
-            fp.cb_bytes = 0;
+        break;
+    case Route::GENERIC:
+        e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
+        break;
+    case Route::DENSE: {
+        e = aq::launch_operand_records(geo, fp, w, L->d_wrec, st);
+        const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(L->d_wrec), L->d_scales, X, xs, Y,
+                                 d.y_dtype, d.x_dtype, st, nullptr, nullptr};
+        if (e == hipSuccess) e = aq::launch_rec_gemm(geo, fp, fl, L->d_xpack, L->d_zero);
+        break;
+    }
+    default: {   // FUSED, REC_LINEAR
+        const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
+                            : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
+                                                           : L->d_cbtile;
+        const uint8_t* recs = L->d_crec;
+        if (fp.dec == aq::FUSED_DEC_REC) {
+            e = aq::launch_operand_records(geo, fp, w, L->d_wrec, st);
+            recs = static_cast<const uint8_t*>(L->d_wrec);
         }
-        aq::FusedPlan gp = fp;
-        const aq::Options& opt = L->opt;
-        // dense product over the records: a comparator route (AQ_OPT_RECORD_PRODUCT = 2);
-        // measured slower than the fused kernel's pre-decoded mode on most layer shapes here
-        const bool gemm = L->fused_ok && fits31 && fp.dec == aq::FUSED_DEC_REC && opt.rec_product == 2 &&
-                          gemm_plan_tile(geo, opt, &gp);
-        auto order = [&opt](aq::FusedPlan& q) {
-            // channel-major order for pre-decoded convolution operands; linear layers
-            // measured faster token-major (qkv 8192 x 576 -> 1728: 59.5 vs 61.8 us)
-            q.nmajor = q.dec == aq::FUSED_DEC_REC && q.kind != 0;
-            if (opt.tile_order != 0) q.nmajor = opt.tile_order == 2;
-        };
-        order(fp);
-        order(gp);
-        if (gemm) {
-            e = aq::launch_operand_records(geo, gp, w, L->d_wrec, st);
-            const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(L->d_wrec), L->d_scales, X, xs, Y,
-                                     d.y_dtype, d.x_dtype, st};
-            if (e == hipSuccess) e = aq::launch_rec_gemm(geo, gp, fl, L->d_xpack, L->d_zero);
-        } else if (L->fused_ok && fits31 && opt.generic != 1 && fused_plan_tile(geo, opt, &fp)) {
-            const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
-                                : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
-                                                               : L->d_cbtile;
-            const uint8_t* recs = L->d_crec;
-            e = hipSuccess;
-            if (fp.dec == aq::FUSED_DEC_REC) {
-                e = aq::launch_operand_records(geo, fp, w, L->d_wrec, st);
-                recs = static_cast<const uint8_t*>(L->d_wrec);
-            }
-            fp.x_bytes = geo.conv ? n * (int64_t)geo.cin * geo.H * geo.W * 2
-                                  : geo.tokens * (int64_t)geo.K * (d.x_dtype == AQ_I8 ? 1 : 2);
-            fp.tile_div = fp.nmajor ? (int)((geo.tokens + fp.bm - 1) / fp.bm) : (geo.C_out + fp.bn - 1) / fp.bn;
-            fp.inv_tile_div = 1.0f / (float)fp.tile_div;
-            const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st};
-            // a linear layer's records feed the 2 x 2 wave-split product (AQ_OPT_RECORD_PRODUCT = 1:
-            // the fused kernel's own pre-decoded mode, whose partial-tile order matches its in-loop mode)
-            const bool rlin = fp.dec == aq::FUSED_DEC_REC && opt.rec_product != 1 &&
-                              aq::rec_linear_supported(geo, fp, d.x_dtype);
-            fp.rlin_var = aq::rec_linear_tile(geo, opt.rlin_tile);
-            if (e == hipSuccess) e = rlin ? aq::launch_rec_linear(geo, fp, fl) : aq::launch_fused_forward(geo, fp, fl);
-        } else if (geo.g == 8) {
-            e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
-        } else {
-            return fail(AQ_ERR_UNSUPPORTED, "g = 9 layers run on the fused kernel only (it was disabled or its "
-                                            "tiles do not fit this shape)");
-        }
+        fp.x_bytes = geo.conv ? n * (int64_t)geo.cin * geo.H * geo.W * 2
+                              : geo.tokens * (int64_t)geo.K * (d.x_dtype == AQ_I8 ? 1 : 2);
+        const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st, L->d_part,
+                                 L->d_arrivals};
+        if (e == hipSuccess)
+            e = r.kind == Route::REC_LINEAR ? aq::launch_rec_linear(geo, fp, fl) : aq::launch_fused_forward(geo, fp, fl);
+        break;
+    }
     }
     if (e != hipSuccess) return hip_fail(e, "forward launch");
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
+    return AQ_OK;
+}
+
+aq_status aq_layer_describe(const aq_layer* L, int64_t n, char* buf, int64_t size) {
+    if (!L || !buf || size < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument or empty buffer");
+    if (n < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "n must be >= 1");
+    const Geom geo = make_geom(L, n);
+    if (geo.tokens > L->desc.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens");
+    const Route r = plan_route(L, geo);
+    static const char* kinds[] = {"table", "fp32", "generic", "dense-records", "fused", "rec-linear", "none"};
+    static const char* decs[] = {"in-loop fp16 codebook in LDS", "in-loop fp32 codebook in LDS",
+                                 "in-loop fp16 codebook in LDS", "in-loop fp16 codebook in L2", "records"};
+    std::string t = std::string("path=") + (r.kind == Route::LUT ? "lut" : "decode") + " route=" + kinds[r.kind];
+    if (r.kind == Route::FUSED || r.kind == Route::REC_LINEAR || r.kind == Route::DENSE) {
+        const aq::FusedPlan& p = r.fp;
+        t += std::string(" weights=") + decs[p.dec] + " tile=" + std::to_string(p.bm) + "x" + std::to_string(p.bn);
+        if (r.kind == Route::FUSED)
+            t += " upl=" + std::to_string(p.upl) + " split_k=" + std::to_string(p.splitk) +
+                 " order=" + (p.nmajor ? "channel" : "token");
+        if (r.kind == Route::REC_LINEAR) t += " variant=" + std::to_string(p.rlin_var);
+        if (p.dec == aq::FUSED_DEC_REC)
+            t += " records_bytes=" + std::to_string(aq::operand_record_bytes(geo, p));
+    }
+    const size_t m = std::min<size_t>(t.size(), (size_t)size - 1);
+    std::memcpy(buf, t.data(), m);
+    buf[m] = '\0';
     return AQ_OK;
 }
 
@@ -770,10 +988,13 @@ aq_status aq_layer_codebook_grad(aq_layer* L, const void* X, const void* dY, int
         L->gplan = gp;
         L->grad_stale = false;
     }
+    TraceScope trace(L, static_cast<hipStream_t>(stream));
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
     const hipError_t e =
         aq::launch_codebook_grad(geo, L->gplan, dtype, X, dY, L->d_scales, L->d_gpart, L->d_gidx_offs, L->d_gidx_ent,
                                  dC, L->d_zero, L->opt.grad_splits, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "codebook gradient launch");
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
     return AQ_OK;
 }
 
@@ -890,6 +1111,27 @@ aq_status aq_layer_get_option(const aq_layer* L, int32_t option, int64_t* value)
     case AQ_OPT_GRAD_TILE: *value = o.grad_bm * 1000 + o.grad_bn; return AQ_OK;
     default: return fail(AQ_ERR_INVALID_ARGUMENT, "unknown option " + std::to_string(option));
     }
+}
+
+aq_status aq_layer_set_launch_events(aq_layer* L, void* const* events, int32_t n_events) {
+    if (!L) return fail(AQ_ERR_INVALID_ARGUMENT, "null layer");
+    if (n_events < 0 || n_events > 64 || (n_events > 0 && !events))
+        return fail(AQ_ERR_INVALID_ARGUMENT, "n_events must be in [0, 64] with a non-null array");
+    for (int i = 0; i < n_events; ++i)
+        if (!events[i]) return fail(AQ_ERR_INVALID_ARGUMENT, "null event at index " + std::to_string(i));
+    L->events.assign(reinterpret_cast<hipEvent_t const*>(events), reinterpret_cast<hipEvent_t const*>(events) + n_events);
+    return AQ_OK;
+}
+
+aq_status aq_layer_last_launches(const aq_layer* L, int32_t* n_launches, char* names, int64_t names_size) {
+    if (!L || !n_launches) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    *n_launches = L->last_launches;
+    if (names && names_size > 0) {
+        const size_t n = std::min<size_t>(L->last_names.size(), (size_t)names_size - 1);
+        std::memcpy(names, L->last_names.data(), n);
+        names[n] = '\0';
+    }
+    return AQ_OK;
 }
 
 aq_status aq_layer_choose_path(const aq_layer* L, int64_t tokens, aq_path* out) {

@@ -465,6 +465,7 @@ static hipError_t launch_table(const Geom& geo, const LutPlan& plan, const LutAr
     const dim3 grid((unsigned)((geo.C_out + rows_wg - 1) / rows_wg), (unsigned)((a.nchunk + a.cpw - 1) / a.cpw),
                     (unsigned)((a.ntok + NT - 1) / NT));
     lut_fwd_kernel<NT, MF, CBT, XT><<<grid, 256, lds, st>>>(geo, a);
+    note_launch(st, "lut_fwd_kernel", {NT, (int)MF, CBT, XT});
     return hipGetLastError();
 }
 
@@ -554,6 +555,7 @@ hipError_t launch_lut_forward(const Geom& geo, const DeviceWeights& w, const Lut
         else
             lut_reduce_kernel<AQ_F16><<<grid, 16 * kRedParts, 0, stream>>>(geo, ws, (int)cgs, plan.tok_block, tok0, ntok,
                                                                 w.scales, x_scales, Y);
+        note_launch(stream, "lut_reduce_kernel", {y_dtype == AQ_F32 ? AQ_F32 : AQ_F16});
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

@@ -301,6 +301,7 @@ static hipError_t launch_cfg(const Geom& geo, const DeviceWeights& w, const void
     const dim3 grid((unsigned)((geo.tokens + BM - 1) / BM), (unsigned)((geo.C_out + BN - 1) / BN));
     const int acc16 = w.cb_dtype == AQ_F16 && TILE == AQ_F16;
     kern<<<grid, kThreads, dyn, st>>>(geo, cbdev, w.codes, w.scales, X, x_scales, Y, y_dtype, acc16);
+    note_launch(st, "mfma_fwd_kernel", {MODE, XT, TILE, (int)CONV, BM, BN});
     return hipGetLastError();
 }
 

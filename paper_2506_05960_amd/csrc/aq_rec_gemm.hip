@@ -347,6 +347,7 @@ static hipError_t rec_gemm_cfg(const Geom& geo, const FusedPlan& plan, const Gem
     if (e != hipSuccess) return e;
     const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN)));
     kern<<<grid, 256, plan.lds_bytes, st>>>(geo, plan, ga);
+    note_launch(st, "rec_gemm_kernel", {KIND, XT, BM, BN});
     return hipGetLastError();
 }
 
@@ -404,12 +405,14 @@ hipError_t launch_rec_gemm(const Geom& geo, const FusedPlan& p, const FusedLaunc
         const int64_t total = (int64_t)nimg * (geo.cin / 8) * geo.H * geo.W;
         act_pack_conv_kernel<<<(unsigned)((total + 255) / 256), 256, 0, st>>>(
             static_cast<const uint16_t*>(fl.X), static_cast<u32x4*>(xpack), nimg, geo.cin, geo.H, geo.W);
+        note_launch(st, "act_pack_conv_kernel", {});
         ga.xa = static_cast<const uint8_t*>(xpack);
         ga.cstride = (uint32_t)((p.kind == 1 ? 2 : 8) * geo.H * geo.W * 16);   // the chunk's 8-channel planes
     } else if (fl.x_dtype == AQ_I8) {
         const int64_t n8 = geo.tokens * geo.K / 8;
         act_widen_i8_kernel<<<(unsigned)((n8 + 255) / 256), 256, 0, st>>>(static_cast<const uint64_t*>(fl.X),
                                                                            static_cast<u32x4*>(xpack), n8);
+        note_launch(st, "act_widen_i8_kernel", {});
         ga.xa = static_cast<const uint8_t*>(xpack);
         ga.cstride = 64 * 2;
     } else {

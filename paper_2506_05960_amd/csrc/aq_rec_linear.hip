@@ -360,6 +360,7 @@ hipError_t rec_linear_cfg(const RecLinArgs& ar, const FusedLaunch& fl) {
     const int64_t tm = (ar.tokens + BM - 1) / BM, tn = (ar.C_out + BN - 1) / BN;
     const dim3 grid((unsigned)(tm * tn));
     kern<<<grid, 256, lds, fl.stream>>>(ar, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y);
+    note_launch(fl.stream, "rec_linear_kernel", {XT, TM, TN, WGT});
     return hipGetLastError();
 }
 

@@ -162,6 +162,11 @@ def test_null_handles_are_rejected():
     out = ctypes.c_int()
     assert lib.aq_layer_choose_path(None, 4, ctypes.byref(out)) == A.AQ_ERR_INVALID_ARGUMENT
     assert lib.aq_layer_destroy(None) == A.AQ_OK
+    buf = ctypes.create_string_buffer(64)
+    assert lib.aq_layer_describe(None, 4, buf, 64) == A.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layer_set_launch_events(None, None, 0) == A.AQ_ERR_INVALID_ARGUMENT
+    n = ctypes.c_int32()
+    assert lib.aq_layer_last_launches(None, ctypes.byref(n), buf, 64) == A.AQ_ERR_INVALID_ARGUMENT
 
 
 def test_python_binding_raises_on_error():

@@ -14,6 +14,7 @@ import torch
 
 import oracle as O
 import workloads as W
+from parity_checks import check_against_oracle, edge_samples, sampled_outputs
 from workloads import ConvGeom, LayerSpec, generate
 
 pytestmark = pytest.mark.gpu
@@ -550,55 +551,6 @@ def _sweep_shape_cases():
     return cases
 
 
-def _edge_samples(spec, rng, n_tok=64, n_ch=48):
-    """Sampled output positions: first and last token and channel, the image
-    border pixels of the first and last image, token and channel tile edges,
-    then random positions."""
-    T, C = spec.tokens, spec.C_out
-    tok = [0, T - 1]
-    if spec.conv is not None:
-        OH, OW = spec.conv.OH, spec.conv.OW
-        for b in (0, spec.n - 1):
-            for oh, ow in ((0, 0), (0, OW - 1), (OH - 1, 0), (OH - 1, OW - 1), (0, OW // 2), (OH // 2, 0),
-                           (OH - 1, OW // 2), (OH // 2, OW - 1)):
-                tok.append((b * OH + oh) * OW + ow)
-    for e in (32, 64, 128, 256):
-        for t in (e - 1, e, T - e, T - e - 1):
-            tok.append(t)
-    ch = [0, C - 1]
-    for e in (32, 64, 96, 128, 192, 256):
-        ch += [e - 1, e, C - e]
-    tok = sorted(set(t for t in tok if 0 <= t < T))
-    ch = sorted(set(c for c in ch if 0 <= c < C))
-    while len(tok) < min(n_tok, T):
-        tok = sorted(set(tok) | {int(rng.integers(0, T))})
-    while len(ch) < min(n_ch, C):
-        ch = sorted(set(ch) | {int(rng.integers(0, C))})
-    return np.array(tok), np.array(ch)
-
-
-def _sampled_outputs(spec, y, tok, ch):
-    if spec.conv is None:
-        return y[np.ix_(tok, ch)]
-    flat = y.transpose(0, 2, 3, 1).reshape(spec.tokens, spec.C_out)
-    return flat[np.ix_(tok, ch)]
-
-
-def check_against_oracle(spec, inp, got, tok, ch, path, tol):
-    """The GPU outputs at (tok, ch) against the oracle: infinity-norm and RMS
-    relative errors within ``tol``, and every element within its rounding bound."""
-    ref = O.forward_sampled(spec, inp, tok, ch)
-    a_ref = O.forward_sampled(spec, O.abs_inputs(spec, inp), tok, ch)
-    bound = O.rounding_bound(spec, ref, a_ref, path)
-    e_inf, e_rms, e_el = O.rel_err_inf(got, ref), O.rel_err_rms(got, ref), O.rel_err_elem(got, ref)
-    over = np.argwhere(np.abs(got - ref) > bound)
-    _say(f"  inf={e_inf:.2e} rms={e_rms:.2e} elem(floor 1e-3 rms)={e_el:.2e} over_bound={len(over)}")
-    for i, j in over[:5]:
-        _say(f"    token {tok[i]} channel {ch[j]}: got {got[i, j]!r} ref {ref[i, j]!r} bound {bound[i, j]:.3e}")
-    assert e_inf <= tol and e_rms <= tol
-    assert len(over) == 0
-
-
 @pytest.mark.parametrize("layer,variant", _sweep_shape_cases(),
                          ids=[f"{l.name}-{v}" for l, v in _sweep_shape_cases()])
 def test_sweep_shape_parity(layer, variant):
@@ -615,8 +567,8 @@ def test_sweep_shape_parity(layer, variant):
     torch.cuda.synchronize()
     out = y.float().cpu().numpy().astype(np.float64)
     lay.close()
-    tok, ch = _edge_samples(spec, np.random.default_rng(17))
-    check_against_oracle(spec, inp, _sampled_outputs(spec, out, tok, ch), tok, ch, path, 2e-3)
+    tok, ch = edge_samples(spec, np.random.default_rng(17))
+    check_against_oracle(spec, inp, sampled_outputs(spec, out, tok, ch), tok, ch, path, 2e-3)
 
 
 def test_graph_replay_matches_eager():
@@ -646,3 +598,124 @@ def test_graph_replay_matches_eager():
             _ = layer.forward(x, xs)          # eager work between replays
             torch.cuda.synchronize()
         layer.close()
+
+
+def test_launch_events_and_names():
+    """Caller events bracket every launch of a forward (eager); under capture none are recorded and the
+    forward still succeeds; the names list the kernels launched."""
+    import paper_2506_05960_amd as P
+    spec = LayerSpec(name="ev", C_out=256, K=512, g=8, M=2, B=8, n=2048)
+    inp = generate(spec, 3)
+    layer = P.AQLayer(spec, inp)
+    layer.set_option("weights", 2)                     # records + product: two launches
+    x = _dev(inp["x"], "f16")
+    y = layer.forward(x)
+    torch.cuda.synchronize()
+    n, names = layer.last_launches()
+    assert n == 2 and names[0].startswith("operand_records") and names[1].startswith("rec_linear_kernel<")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for e in ev:
+        e.record()
+    torch.cuda.synchronize()
+    layer.set_launch_events(ev)
+    layer.forward(x, out=y)
+    torch.cuda.synchronize()
+    t = [ev[k].elapsed_time(ev[k + 1]) for k in range(2)]
+    assert all(v > 0 for v in t)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            layer.forward(x, out=y)
+    torch.cuda.current_stream().wait_stream(s)
+    g.replay()
+    torch.cuda.synchronize()
+    layer.set_launch_events([])
+    assert O.rel_err_inf(y.float().cpu().numpy(), O.forward(spec, inp)) <= 2e-3
+    layer.close()
+
+
+# ---------------------------------------------------------------------------
+# K split over workgroups (under-filled layers): the last workgroup of a tile
+# sums the splits' partial tiles in split order
+# ---------------------------------------------------------------------------
+
+SPLIT = [
+    # few tiles (512 tokens: eight 8x8 images, 16 tiles of 64x96) and 16 chunks along K
+    LayerSpec(name="s_conv3", C_out=192, K=256 * 9, g=8, M=2, B=8, n=8, conv=ConvGeom(256, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="s_conv3_m4", C_out=130, K=256 * 9, g=8, M=4, B=8, n=6, conv=ConvGeom(256, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="s_conv3_b16", C_out=96, K=256 * 9, g=8, M=1, B=16, n=4, conv=ConvGeom(256, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="s_conv3_s2", C_out=70, K=256 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(256, 3, 3, 2, 1, 16, 16)),
+    LayerSpec(name="s_kaq", C_out=96, K=256 * 9, g=9, M=2, B=8, n=4, conv=ConvGeom(256, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="s_conv1", C_out=200, K=1024, g=8, M=2, B=8, n=8, conv=ConvGeom(1024, 1, 1, 1, 0, 8, 8)),
+    LayerSpec(name="s_lin", C_out=136, K=1024, g=8, M=2, B=8, n=300),
+    LayerSpec(name="s_lin_i8", C_out=72, K=1536, g=8, M=4, B=8, n=100, x_dtype="i8"),
+    LayerSpec(name="s_lin_f32y", C_out=64, K=2048, g=8, M=2, B=8, n=65, y_dtype="f32"),
+]
+
+
+@pytest.mark.parametrize("weights", [1, 2])
+@pytest.mark.parametrize("spec", SPLIT, ids=lambda s: s.name)
+def test_split_k_matches_oracle_and_is_deterministic(spec, weights):
+    import paper_2506_05960_amd as P
+    if spec.g == 9 and weights == 1:
+        pytest.skip("g = 9 has no in-loop decode")
+    inp = generate(spec, 612)
+    y_ref = O.forward(spec, inp)
+    a_ref = O.forward(spec, O.abs_inputs(spec, inp))
+    layer = P.AQLayer(spec, inp)
+    layer.set_path("decode")
+    layer.set_option("weights", weights)
+    layer.set_option("record_product", 1)          # the fused kernel's own loop over records
+    x = _dev(inp["x"], spec.x_dtype)
+    xs = None if inp["x_scales"] is None else torch.from_numpy(inp["x_scales"]).cuda()
+    planned = int(layer.describe(spec.n)["split_k"])
+    _say(f"split {spec.name} weights={weights}: {layer.describe(spec.n)}")
+    assert planned > 1, "the planner splits an under-filled layer"
+    outs = {}
+    for S in sorted({1, 2, planned}):
+        layer.set_option("split_k", S)
+        assert int(layer.describe(spec.n)["split_k"]) == S
+        a = layer.forward(x, xs).float().cpu().numpy().astype(np.float64)
+        b = layer.forward(x, xs).float().cpu().numpy().astype(np.float64)
+        assert np.array_equal(a, b), f"split {S}: repeated forwards differ"
+        err = O.rel_err_inf(a, y_ref)
+        bound = O.rounding_bound(spec, y_ref, a_ref, "decode")
+        _say(f"  S={S} err={err:.3e} over_bound={int(np.sum(np.abs(a - y_ref) > bound))}")
+        assert err <= _tol(spec, "decode")
+        assert np.all(np.abs(a - y_ref) <= bound)
+        outs[S] = a
+    # the split changes only the summation order
+    assert not np.array_equal(outs[1], outs[2])
+    layer.close()
+
+
+def test_split_k_graph_replays():
+    """The arrival counters reset themselves: graph replays with eager split forwards in between agree bitwise."""
+    import paper_2506_05960_amd as P
+    spec = SPLIT[0]
+    inp = generate(spec, 613)
+    layer = P.AQLayer(spec, inp)
+    assert int(layer.describe(spec.n)["split_k"]) > 1
+    x = _dev(inp["x"], "f16")
+    eager = layer.forward(x).clone()
+    torch.cuda.synchronize()
+    y = torch.zeros_like(eager)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            for _ in range(3):
+                layer.forward(x, out=y)
+    torch.cuda.current_stream().wait_stream(s)
+    for rep in range(4):
+        y.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager), rep
+        assert torch.equal(layer.forward(x), eager)
+        torch.cuda.synchronize()
+    layer.close()

@@ -15,6 +15,9 @@ from .layers import (  # noqa: F401
     config_inputs,
     sweep_layers,
     sweep_spec,
+    sweep_io_elems,
+    chain_sources,
+    chain_codebook_std,
     lut_regime_specs,
     SEED_BASE,
 )

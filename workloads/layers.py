@@ -341,18 +341,59 @@ def unet_unquantized_conv_macs(batch: int, latent_ch: int = 3) -> int:
     return batch * 2 * 64 * 64 * 9 * latent_ch * 192
 
 
-def sweep_spec(layer: SweepLayer, M: int, batch: int = 8, B: int = 8, g: int = 8) -> LayerSpec:
-    """AQ layer spec of one sweep layer (fp16 activations, fp16 codebooks)."""
+def sweep_spec(layer: SweepLayer, M: int, batch: int = 8, B: int = 8, g: int = 8,
+               codebook_std: Optional[float] = None) -> LayerSpec:
+    """AQ layer spec of one sweep layer (fp16 activations, fp16 codebooks).
+
+    ``codebook_std`` defaults to 0.05; ``"chain"`` selects the unit-scale
+    value of ``chain_codebook_std``."""
     variant = f"W{M * B // g}"
     if layer.kind == "linear":
         t = layer.tokens_per_image if layer.tokens_per_image is not None else layer.res * layer.res
-        return LayerSpec(name=f"{layer.name}.{variant}", C_out=layer.cout, K=layer.cin, g=g, M=M, B=B,
-                         n=batch * t, note=layer.role)
-    k = 3 if layer.kind == "conv3x3" else 1
-    geom = ConvGeom(cin=layer.cin, kh=k, kw=k, stride=layer.stride, pad=(k - 1) // 2,
-                    H=layer.res, W=layer.res)
-    return LayerSpec(name=f"{layer.name}.{variant}", C_out=layer.cout, K=geom.K, g=g, M=M, B=B,
-                     n=batch, conv=geom, note=layer.role)
+        K = layer.cin
+        geom = None
+        n = batch * t
+    else:
+        k = 3 if layer.kind == "conv3x3" else 1
+        geom = ConvGeom(cin=layer.cin, kh=k, kw=k, stride=layer.stride, pad=(k - 1) // 2,
+                        H=layer.res, W=layer.res)
+        K = geom.K
+        n = batch
+    std = 0.05 if codebook_std is None else (chain_codebook_std(M, K) if codebook_std == "chain" else codebook_std)
+    return LayerSpec(name=f"{layer.name}.{variant}", C_out=layer.cout, K=K, g=g, M=M, B=B, n=n, conv=geom,
+                     note=layer.role, codebook_std=float(std))
+
+
+def sweep_io_elems(layer: SweepLayer, batch: int):
+    """(input elements, output elements) of one sweep layer at ``batch``."""
+    if layer.kind == "linear":
+        t = batch * (layer.tokens_per_image if layer.tokens_per_image is not None else layer.res * layer.res)
+        return t * layer.cin, t * layer.cout
+    o = layer.res // layer.stride
+    return batch * layer.cin * layer.res * layer.res, batch * layer.cout * o * o
+
+
+def chain_sources(layers: List[SweepLayer], batch: int = 8) -> List[Optional[int]]:
+    """For a chained pass over ``layers``: entry i is i - 1 when the previous
+    layer's output buffer can serve as layer i's input (same element count:
+    a convolution output [n, C, R, R] is read as the [n*R*R, C] tokens of a
+    following linear layer and back), else None (layer i reads a buffer of
+    its own).  The U-Net's glue between layers (normalisation, attention,
+    up-sampling, skip concatenation) is not part of the pass."""
+    src: List[Optional[int]] = []
+    for i, lay in enumerate(layers):
+        if i > 0 and sweep_io_elems(layers[i - 1], batch)[1] == sweep_io_elems(lay, batch)[0]:
+            src.append(i - 1)
+        else:
+            src.append(None)
+    return src
+
+
+def chain_codebook_std(M: int, K: int) -> float:
+    """Codebook standard deviation that keeps a chained layer's output at unit
+    scale for unit-scale input: with scales U(0.5, 1.5) (mean square 13/12),
+    M codewords per group and K inputs, var(y) = (13/12) K M sigma^2."""
+    return 1.0 / np.sqrt(13.0 / 12.0 * M * K)
 
 
 def lut_regime_specs(n_list=(1, 2, 4, 8, 16, 32, 64)) -> List[LayerSpec]:
