@@ -197,6 +197,12 @@ aq_status aq_layer_set_path(aq_layer* layer, aq_path path);
  *   AQ_OPT_GRAD_REGS        codebook gradient: 1 = register-staged kernels
  *                           (0: direct-to-LDS kernels where they apply)
  *   AQ_OPT_GRAD_TILE        codebook gradient tile BM * 1000 + BN (0 = planner)
+ *   AQ_OPT_TABLE_ONE_LAUNCH table path: 1 = the table kernel also adds the
+ *                           chunk groups' partial sums (the last workgroup of
+ *                           each row slice to arrive does, in chunk-group
+ *                           order); 0 = a second, reduction kernel (measured
+ *                           faster).  Both orders are fixed: repeated runs
+ *                           are bitwise identical
  * The gradient options take effect at the next gradient call; if they need a
  * larger partial-gradient workspace, that call reallocates it (synchronous).
  * Unknown options or out-of-range values return AQ_ERR_INVALID_ARGUMENT.
@@ -214,7 +220,8 @@ typedef enum {
     AQ_OPT_SPLIT_K = 10,
     AQ_OPT_GRAD_SPLITS = 11,
     AQ_OPT_GRAD_REGS = 12,
-    AQ_OPT_GRAD_TILE = 13
+    AQ_OPT_GRAD_TILE = 13,
+    AQ_OPT_TABLE_ONE_LAUNCH = 14
 } aq_option;
 
 aq_status aq_layer_set_option(aq_layer* layer, int32_t option, int64_t value);

@@ -26,7 +26,7 @@ STATUS_NAMES = {0: "AQ_OK", 1: "AQ_ERR_INVALID_ARGUMENT", 2: "AQ_ERR_UNSUPPORTED
 # aq_option (include/aq.h)
 OPTION_CODES = {"lut_max_tokens": 1, "weights": 2, "generic": 3, "record_product": 4, "fused_tile": 5,
                 "dense_tile": 6, "rec_linear_tile": 7, "tile_order": 8, "stage_rows": 9, "split_k": 10,
-                "grad_splits": 11, "grad_regs": 12, "grad_tile": 13}
+                "grad_splits": 11, "grad_regs": 12, "grad_tile": 13, "table_one_launch": 14}
 _TILE_OPTIONS = ("fused_tile", "dense_tile", "grad_tile")
 
 EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",

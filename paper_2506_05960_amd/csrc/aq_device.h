@@ -23,6 +23,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* p, uin
 }
 constexpr uint32_t kOutOfRange = 0x80000000u;   // byte offset past every buffer the kernels read
 
+// Cache policy of a buffer access that is coherent across the whole device
+// (the SC1 bit): it reads and writes memory past this XCD's L2, which may
+// hold stale copies of lines another XCD wrote.  Used for the partial sums
+// that one workgroup publishes and another, possibly on another XCD, reads.
+constexpr int kCoherent = 16;
+
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 
 // Two IEEE fp16 additions (round to nearest even) on packed halves.

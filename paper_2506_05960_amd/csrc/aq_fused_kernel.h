@@ -722,25 +722,21 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
     if (plan.splitk > 1) {
         // K split over workgroups: publish this split's partial tile, count the
         // arrival; the last workgroup of the tile sums every split in order.
-        // The partial tiles are written and read with device-coherent accesses
-        // (agent-scope atomic stores and loads, which bypass the per-XCD L2's
-        // stale copies), so no cache-wide write-back or invalidation is needed:
-        // each thread's stores have completed (vmcnt 0) before the barrier that
-        // precedes the arrival count, and the loads are issued after it.
-        // Layout [tile][split][16][TASKS] of 8-byte pairs, task fastest: each
-        // store and load instruction covers 64 consecutive pairs (512 bytes).
+        // The partial tiles are written and read with device-coherent buffer
+        // accesses (past the per-XCD L2, which may hold stale copies), so no
+        // cache-wide write-back or invalidation is needed: each thread's stores
+        // have completed (vmcnt 0) before the barrier that precedes the
+        // arrival count, and the loads are issued after it.  Layout
+        // [tile][split][8][TASKS] of 16-byte pieces, task fastest: one store or
+        // load instruction of a wave covers 1 KB.
         const int S = plan.splitk;
-        uint64_t* mine = reinterpret_cast<uint64_t*>(part) + (size_t)(tile_lin * S + ksplit) * TASKS * 16 + task;
+        const __amdgpu_buffer_rsrc_t pr = buffer_rsrc(part, (uint64_t)plan.ntiles * S * TASKS * 8 * 16);
+        const uint32_t mine = (uint32_t)(((tile_lin * S + ksplit) * 8 * TASKS + task) * 16);
         if (task < TASKS) {
 #pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                __hip_atomic_store(mine + (2 * c) * TASKS,
-                                   (uint64_t)__float_as_uint(v[c][0]) | ((uint64_t)__float_as_uint(v[c][1]) << 32),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(mine + (2 * c + 1) * TASKS,
-                                   (uint64_t)__float_as_uint(v[c][2]) | ((uint64_t)__float_as_uint(v[c][3]) << 32),
-                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
+            for (int c = 0; c < 8; ++c)
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v[c]), pr, mine + (uint32_t)(c * TASKS * 16),
+                                                       0, kCoherent);
         }
         wait_vmcnt<0>();
         __syncthreads();                         // (every thread is also done reading the partial tiles in LDS)
@@ -749,16 +745,17 @@ fused_fwd_kernel(Geom geo, FusedPlan plan, const void* __restrict__ cb, const ui
         __syncthreads();
         if (*arrived != (uint32_t)(S - 1)) return;   // not the last split of this tile (uniform)
         if (task < TASKS) {
-            const uint64_t* p0 = reinterpret_cast<const uint64_t*>(part) + (size_t)(tile_lin * S) * TASKS * 16 + task;
+            const uint32_t base = (uint32_t)((tile_lin * S * 8 * TASKS + task) * 16);
             for (int k = 0; k < S; ++k) {
-                const uint64_t* pk = p0 + (size_t)k * TASKS * 16;
+                u32x4 q[8];
+#pragma unroll
+                for (int c = 0; c < 8; ++c)
+                    q[c] = __builtin_amdgcn_raw_buffer_load_b128(pr, base + (uint32_t)((k * 8 + c) * TASKS * 16), 0,
+                                                                 kCoherent);
 #pragma unroll
                 for (int c = 0; c < 8; ++c) {
-                    const uint64_t lo = __hip_atomic_load(pk + (2 * c) * TASKS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    const uint64_t hi = __hip_atomic_load(pk + (2 * c + 1) * TASKS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    const floatx4 q{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
-                                    __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
-                    v[c] = k == 0 ? q : v[c] + q;          // splits added in order 0, 1, ..., S - 1
+                    const floatx4 f = __builtin_bit_cast(floatx4, q[c]);
+                    v[c] = k == 0 ? f : v[c] + f;      // splits added in order 0, 1, ..., S - 1
                 }
             }
         }

@@ -36,6 +36,7 @@ struct Options {
     int grad_splits;          // codebook gradient token splits (0: planner)
     int grad_regs;            // 1: register-staged weight-gradient kernels
     int grad_bm, grad_bn;     // forced weight-gradient tile (0: planner)
+    int table_one_launch;     // 1: table path reduces in its own kernel (last-arriving workgroup)
 };
 
 constexpr int kMaxSplitK = 8;   // most workgroups sharing one output tile along K
@@ -155,9 +156,12 @@ hipError_t launch_fused_linear(const Geom& geo, const FusedPlan& plan, const Fus
 hipError_t launch_decode_to_global(const Geom& geo, const DeviceWeights& w, int tile_dtype, void* W,
                                    hipStream_t stream);
 
+// ws: [chunk groups][tok_block][C_out] fp32 partial sums; arrivals: lut_arrival_count(geo) counters, zero
+// between launches (the last workgroup of each row slice and token pass resets its own)
 hipError_t launch_lut_forward(const Geom& geo, const DeviceWeights& w, const LutPlan& plan, const void* X,
                               int x_dtype, const float* x_scales, void* Y, int y_dtype, float* ws,
-                              hipStream_t stream);
+                              uint32_t* arrivals, bool one_launch, hipStream_t stream);
+size_t lut_arrival_count(int C_out);
 
 hipError_t launch_mfma_forward(const Geom& geo, const DeviceWeights& w, const void* X, int x_dtype,
                                const float* x_scales, void* Y, int y_dtype, int tile_dtype,

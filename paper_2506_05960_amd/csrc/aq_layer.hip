@@ -29,6 +29,7 @@ struct aq_layer {
     uint8_t* d_codes_lut;
     float* d_scales;
     float* d_ws;
+    uint32_t* d_lut_arrivals; // table path: arrival counters (zero between launches)
     LutPlan plan;
     aq::FusedPlan fplan;
     uint8_t* d_crec;          // fused-path code records (null when the fused path does not apply)
@@ -235,7 +236,7 @@ void free_layer(aq_layer* L) {
     if (!L) return;
     void* ptrs[] = {L->d_cb,     L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales,
                     L->d_ws,     L->d_crec, L->d_wrec,   L->d_xpack, L->d_zero, L->d_gidx_offs,
-                    L->d_gidx_ent, L->d_gpart, L->d_part, L->d_arrivals};
+                    L->d_gidx_ent, L->d_gpart, L->d_part, L->d_arrivals, L->d_lut_arrivals};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete L;
@@ -279,8 +280,9 @@ bool lut_plan_create(const aq_layer_desc& d, int g, int M, int G, LutPlan* p) {
     p->mfma_table = d.codebook_dtype == AQ_F16 && (d.x_dtype == AQ_F16 || d.x_dtype == AQ_I8) && g == 8;
     int64_t tb = std::min<int64_t>(d.max_tokens, 32);   // the table path serves few tokens per launch
     p->tok_block = (int)((tb + 3) / 4 * 4);
-    // 32-bit code offsets in the kernel
-    return (int64_t)p->nchunk * d.out_features * jc * M < (int64_t(1) << 31);
+    // 32-bit code and partial-sum offsets in the kernel
+    return (int64_t)p->nchunk * d.out_features * jc * M < (int64_t(1) << 31) &&
+           (int64_t)p->nchunk * p->tok_block * d.out_features * 4 < (int64_t(1) << 31);
 }
 
 bool fused_plan_create(const aq_layer_desc& d, int g, int M, int B, aq::FusedPlan* p) {
@@ -654,6 +656,83 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
     return r;
 }
 
+// Where a forward's per-call scratch lives: the layer's workspace, or the
+// static array of the allocation-free entry point.
+struct Workspace {
+    float* lut_ws;            // table path: [chunk groups][tok_block][C_out] partial sums
+    uint32_t* lut_arrivals;   // table path: arrival counters
+    void* wrec;               // pre-decoded operand records
+    float* part;              // fused kernel K split: partial tiles
+    uint32_t* arrivals;       // fused kernel K split: arrival counters
+    void* xpack;              // dense product: repacked activations
+};
+
+aq_status check_forward(const aq_layer* L, const void* X, const float* x_scales, const void* Y, int64_t n, Geom* geo,
+                        Route* r) {
+    if (!L || !X || !Y) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
+    if (n < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "n must be >= 1");
+    const aq_layer_desc& d = L->desc;
+    *geo = make_geom(L, n);
+    if (geo->tokens > d.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens");
+    if (d.x_dtype == AQ_I8 && !x_scales) return fail(AQ_ERR_INVALID_ARGUMENT, "int8 activations need x_scales");
+    if ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 15)
+        return fail(AQ_ERR_INVALID_ARGUMENT, "X and Y must be 16-byte aligned");
+    *r = plan_route(L, *geo);
+    if (r->kind == Route::NONE)
+        return fail(AQ_ERR_UNSUPPORTED, "g = 9 layers run on the fused kernel only (it was disabled or its "
+                                        "tiles do not fit this shape)");
+    return AQ_OK;
+}
+
+aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X, const float* x_scales, void* Y,
+                    int64_t n, hipStream_t st, const Workspace& wk) {
+    const aq_layer_desc& d = L->desc;
+    const float* xs = d.x_dtype == AQ_I8 ? x_scales : nullptr;
+    const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, d.codebook_dtype};
+    TraceScope trace(L, st);
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
+    hipError_t e = hipSuccess;
+    aq::FusedPlan fp = r.fp;
+    switch (r.kind) {
+    case Route::LUT:
+        e = aq::launch_lut_forward(geo, w, L->plan, X, d.x_dtype, xs, Y, d.y_dtype, wk.lut_ws, wk.lut_arrivals,
+                                   L->opt.table_one_launch != 0, st);
+        break;
+    case Route::F32:
+        e = aq::launch_f32_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, st);
+        break;
+    case Route::GENERIC:
+        e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
+        break;
+    case Route::DENSE: {
+        e = aq::launch_operand_records(geo, fp, w, wk.wrec, st);
+        const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(wk.wrec), L->d_scales, X, xs, Y,
+                                 d.y_dtype, d.x_dtype, st, nullptr, nullptr};
+        if (e == hipSuccess) e = aq::launch_rec_gemm(geo, fp, fl, wk.xpack, L->d_zero);
+        break;
+    }
+    default: {   // FUSED, REC_LINEAR
+        const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
+                            : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
+                                                           : L->d_cbtile;
+        const uint8_t* recs = L->d_crec;
+        if (fp.dec == aq::FUSED_DEC_REC) {
+            e = aq::launch_operand_records(geo, fp, w, wk.wrec, st);
+            recs = static_cast<const uint8_t*>(wk.wrec);
+        }
+        fp.x_bytes = geo.conv ? n * (int64_t)geo.cin * geo.H * geo.W * 2
+                              : geo.tokens * (int64_t)geo.K * (d.x_dtype == AQ_I8 ? 1 : 2);
+        const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st, wk.part, wk.arrivals};
+        if (e == hipSuccess)
+            e = r.kind == Route::REC_LINEAR ? aq::launch_rec_linear(geo, fp, fl) : aq::launch_fused_forward(geo, fp, fl);
+        break;
+    }
+    }
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
+    return AQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -706,10 +785,12 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
     L->lut_ok = lut_ok;
     L->dec_ok = dec_ok;
     L->path = AQ_PATH_AUTO;
-    // Measured crossover on MI355X (fp16 layers with 256-entry codebooks): the
-    // table path beats the matrix-core path only when K is large enough that
-    // the latter's few workgroups each walk a long reduction, up to 16 tokens.
-    L->lut_max_tokens = desc->in_features >= 4096 ? 16 : 0;
+    // Measured crossover on MI355X (fp16 layers with 256-entry codebooks, codes
+    // read from HBM): the table path beats the matrix-core path (which splits
+    // such under-filled layers along K) only for long reductions and the
+    // fewest tokens: up to 4 tokens with M <= 2, one token with more codebooks
+    // (K = 8640 and 17280 to 960 outputs).
+    L->lut_max_tokens = desc->in_features >= 4096 ? (M <= 2 ? 4 : 1) : 0;
     e = hipGetDevice(&L->device);
     if (e != hipSuccess) {
         free_layer(L);
@@ -751,6 +832,13 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
             }
         AQ_TRY(dev_upload(&L->d_codes_lut, rep.data(), rep.size(), "LUT codes"));
         AQ_TRY(dev_upload(&L->d_ws, nullptr, (size_t)p.nchunk * p.tok_block * C_out * sizeof(float), "workspace"));
+        const size_t ncnt = aq::lut_arrival_count(C_out) * sizeof(uint32_t);
+        AQ_TRY(dev_upload(&L->d_lut_arrivals, nullptr, ncnt, "table arrival counters"));
+        e = hipMemset(L->d_lut_arrivals, 0, ncnt);
+        if (e != hipSuccess) {
+            free_layer(L);
+            return hip_fail(e, "table arrival counters");
+        }
     }
 
     L->fused_ok = fused_ok;
@@ -826,63 +914,12 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
 }
 
 aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, void* Y, int64_t n, void* stream) {
-    if (!L || !X || !Y) return fail(AQ_ERR_INVALID_ARGUMENT, "null pointer argument");
-    if (n < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "n must be >= 1");
-    const aq_layer_desc& d = L->desc;
-    const Geom geo = make_geom(L, n);
-    if (geo.tokens > d.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens");
-    if (d.x_dtype == AQ_I8 && !x_scales) return fail(AQ_ERR_INVALID_ARGUMENT, "int8 activations need x_scales");
-    if ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 15)
-        return fail(AQ_ERR_INVALID_ARGUMENT, "X and Y must be 16-byte aligned");
-    const Route r = plan_route(L, geo);
-    if (r.kind == Route::NONE)
-        return fail(AQ_ERR_UNSUPPORTED, "g = 9 layers run on the fused kernel only (it was disabled or its "
-                                        "tiles do not fit this shape)");
-    const float* xs = d.x_dtype == AQ_I8 ? x_scales : nullptr;
-    const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, d.codebook_dtype};
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    TraceScope trace(L, st);
-    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
-    hipError_t e = hipSuccess;
-    aq::FusedPlan fp = r.fp;
-    switch (r.kind) {
-    case Route::LUT:
-        e = aq::launch_lut_forward(geo, w, L->plan, X, d.x_dtype, xs, Y, d.y_dtype, L->d_ws, st);
-        break;
-    case Route::F32:
-        e = aq::launch_f32_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, st);
-        break;
-    case Route::GENERIC:
-        e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
-        break;
-    case Route::DENSE: {
-        e = aq::launch_operand_records(geo, fp, w, L->d_wrec, st);
-        const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(L->d_wrec), L->d_scales, X, xs, Y,
-                                 d.y_dtype, d.x_dtype, st, nullptr, nullptr};
-        if (e == hipSuccess) e = aq::launch_rec_gemm(geo, fp, fl, L->d_xpack, L->d_zero);
-        break;
-    }
-    default: {   // FUSED, REC_LINEAR
-        const void* cbsrc = fp.dec == aq::FUSED_DEC_PK16   ? L->d_cb
-                            : fp.dec == aq::FUSED_DEC_F32L ? static_cast<const void*>(L->d_cb32)
-                                                           : L->d_cbtile;
-        const uint8_t* recs = L->d_crec;
-        if (fp.dec == aq::FUSED_DEC_REC) {
-            e = aq::launch_operand_records(geo, fp, w, L->d_wrec, st);
-            recs = static_cast<const uint8_t*>(L->d_wrec);
-        }
-        fp.x_bytes = geo.conv ? n * (int64_t)geo.cin * geo.H * geo.W * 2
-                              : geo.tokens * (int64_t)geo.K * (d.x_dtype == AQ_I8 ? 1 : 2);
-        const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st, L->d_part,
-                                 L->d_arrivals};
-        if (e == hipSuccess)
-            e = r.kind == Route::REC_LINEAR ? aq::launch_rec_linear(geo, fp, fl) : aq::launch_fused_forward(geo, fp, fl);
-        break;
-    }
-    }
-    if (e != hipSuccess) return hip_fail(e, "forward launch");
-    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
-    return AQ_OK;
+    Route r;
+    Geom geo;
+    const aq_status s = check_forward(L, X, x_scales, Y, n, &geo, &r);
+    if (s != AQ_OK) return s;
+    const Workspace wk{L->d_ws, L->d_lut_arrivals, L->d_wrec, L->d_part, L->d_arrivals, L->d_xpack};
+    return run_route(L, geo, r, X, x_scales, Y, n, static_cast<hipStream_t>(stream), wk);
 }
 
 aq_status aq_layer_describe(const aq_layer* L, int64_t n, char* buf, int64_t size) {
@@ -892,8 +929,8 @@ aq_status aq_layer_describe(const aq_layer* L, int64_t n, char* buf, int64_t siz
     if (geo.tokens > L->desc.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens");
     const Route r = plan_route(L, geo);
     static const char* kinds[] = {"table", "fp32", "generic", "dense-records", "fused", "rec-linear", "none"};
-    static const char* decs[] = {"in-loop fp16 codebook in LDS", "in-loop fp32 codebook in LDS",
-                                 "in-loop fp16 codebook in LDS", "in-loop fp16 codebook in L2", "records"};
+    static const char* decs[] = {"in-loop-lds-fp16", "in-loop-lds-fp32", "in-loop-lds-fp16", "in-loop-l2-fp16",
+                                 "records"};
     std::string t = std::string("path=") + (r.kind == Route::LUT ? "lut" : "decode") + " route=" + kinds[r.kind];
     if (r.kind == Route::FUSED || r.kind == Route::REC_LINEAR || r.kind == Route::DENSE) {
         const aq::FusedPlan& p = r.fp;
@@ -1087,6 +1124,10 @@ aq_status aq_layer_set_option(aq_layer* L, int32_t option, int64_t value) {
         if (!tile(&o.grad_bm, &o.grad_bn)) return bad();
         L->grad_stale = true;
         return AQ_OK;
+    case AQ_OPT_TABLE_ONE_LAUNCH:
+        if (!in(0, 1)) return bad();
+        o.table_one_launch = (int)value;
+        return AQ_OK;
     default:
         return fail(AQ_ERR_INVALID_ARGUMENT, "unknown option " + std::to_string(option));
     }
@@ -1109,6 +1150,7 @@ aq_status aq_layer_get_option(const aq_layer* L, int32_t option, int64_t* value)
     case AQ_OPT_GRAD_SPLITS: *value = o.grad_splits; return AQ_OK;
     case AQ_OPT_GRAD_REGS: *value = o.grad_regs; return AQ_OK;
     case AQ_OPT_GRAD_TILE: *value = o.grad_bm * 1000 + o.grad_bn; return AQ_OK;
+    case AQ_OPT_TABLE_ONE_LAUNCH: *value = o.table_one_launch; return AQ_OK;
     default: return fail(AQ_ERR_INVALID_ARGUMENT, "unknown option " + std::to_string(option));
     }
 }

@@ -17,9 +17,17 @@
 //     combine their sums with cross-lane reductions.
 //
 // A workgroup walks a few consecutive chunks, keeping its rows' sums in
-// registers, and writes one partial sum per row and token to a workspace; a
-// second kernel adds the partial sums in a fixed order, applies the
-// per-channel (and per-token) scales and stores Y.
+// registers, and writes one partial sum per row and token to a workspace.
+// The partial sums are then added in a fixed order, the per-channel (and
+// per-token) scales applied and Y stored, in one of two ways:
+//  * a second kernel (the default): 64 threads per output each add every
+//    64th chunk group's partial, then one adds the 64 results in order;
+//  * in this kernel: the workgroups of one row slice and token pass (one per
+//    chunk group) count their arrivals, and the last to arrive adds every
+//    chunk group's partial in chunk-group order and resets the counter (one
+//    launch, no memset).  Measured slower: the last workgroup of each slice
+//    reduces its whole slice alone, a latency chain longer than the launch
+//    it saves.
 //
 // Table layout: slot s = (group jj, codebook m) = jj*M + m, entry s*256 + code,
 // NT consecutive floats per entry (one 4/8/16-byte LDS read).  Every slot has
@@ -62,6 +70,14 @@ struct LutArgs {
     int rpl;                 // row steps per workgroup, 1 .. kLutMaxSteps
     int tok_block;           // workspace rows per chunk group
     float* ws;               // [chunk groups][tok_block][C_out]
+    uint32_t* arrivals;      // [row slices][token passes] arrival counters, zero between launches
+    int ncg;                 // chunk groups (gridDim.y)
+    const float* scales;     // [C_out]
+    const float* x_scales;   // [tokens] per-token scales (int8 input), else null
+    void* Y;                 // the whole output
+    int64_t tok_out0;        // first token of this launch in Y (and x_scales)
+    int y_dtype;
+    int one_launch;          // reduce in this kernel (last-arriving workgroup) instead of a second kernel
 };
 
 constexpr int kLutMaxSteps = 4;      // chunks per workgroup, and row steps per workgroup
@@ -391,6 +407,7 @@ lut_fwd_kernel(Geom geo, LutArgs a) {
     }
 
     // ---- combine the LPR lanes of a row (adjacent lanes) and store this chunk group's partial sums ----
+    const __amdgpu_buffer_rsrc_t wsr = buffer_rsrc(a.ws, (uint64_t)a.ncg * a.tok_block * geo.C_out * 4);
 #pragma unroll
     for (int r = 0; r < kLutMaxSteps; ++r) {
         if (r >= a.rpl) break;
@@ -413,11 +430,54 @@ lut_fwd_kernel(Geom geo, LutArgs a) {
                     float e;
                     if constexpr (NT == 1) e = v;
                     else e = v[n];
-                    a.ws[((int64_t)cgrp * a.tok_block + tok) * geo.C_out + row] = e;
+                    const uint32_t off = (uint32_t)(((cgrp * a.tok_block + tok) * geo.C_out + row) * 4);
+                    // device-coherent when this kernel reduces (the last workgroup may run on another XCD)
+                    if (a.one_launch) __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e), wsr, off, 0, kCoherent);
+                    else __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(e), wsr, off, 0, 0);
                 }
             }
         }
     }
+
+    if (!a.one_launch) return;       // the reduction kernel follows
+    // ---- arrival of this chunk group; the last one of the (row slice, token
+    // pass) adds every chunk group's partial sums in order and stores Y ----
+    wait_vmcnt<0>();                 // this thread's partial sums have reached memory
+    __syncthreads();                 // (and every thread is done with the table in LDS)
+    uint32_t* arrived = reinterpret_cast<uint32_t*>(lds);
+    uint32_t* cnt = a.arrivals + (size_t)slice * gridDim.z + blockIdx.z;
+    if (threadIdx.x == 0) *arrived = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (*arrived != (uint32_t)(a.ncg - 1)) return;    // uniform over the workgroup
+    const int nrows = rows_step * a.rpl;
+    const int rbase = slice * nrows;
+    for (int e = threadIdx.x; e < nrows * NT; e += 256) {
+        const int n = e / nrows;
+        const int row = rbase + (e - n * nrows);
+        const int tok = tok_first + n;
+        if (row >= geo.C_out || tok >= a.ntok) continue;
+        // every chunk group's partial sum, 16 device-coherent loads in flight at
+        // a time (past the end: zeros), added in chunk-group order
+        const uint32_t src = (uint32_t)((tok * geo.C_out + row) * 4);
+        const uint32_t cstride = (uint32_t)(a.tok_block * geo.C_out * 4);
+        float t = 0.0f;
+        for (int c0 = 0; c0 < a.ncg; c0 += 16) {
+            uint32_t q[16];
+#pragma unroll
+            for (int c = 0; c < 16; ++c)
+                q[c] = __builtin_amdgcn_raw_buffer_load_b32(wsr, c0 + c < a.ncg ? src + (uint32_t)(c0 + c) * cstride
+                                                                              : kOutOfRange, 0, kCoherent);
+#pragma unroll
+            for (int c = 0; c < 16; ++c)
+                if (c0 + c < a.ncg) t = (c0 + c == 0) ? __uint_as_float(q[c]) : t + __uint_as_float(q[c]);
+        }
+        float y = t * a.scales[row];
+        if (a.x_scales) y *= a.x_scales[a.tok_out0 + tok];
+        const int64_t yi = y_index(geo, a.tok_out0 + tok, row);
+        if (a.y_dtype == AQ_F32) static_cast<float*>(a.Y)[yi] = y;
+        else static_cast<uint16_t*>(a.Y)[yi] = f32_to_f16(y);
+    }
+    if (threadIdx.x == 0) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Fixed-order reduction over chunk groups, scales, dtype cast and store.
@@ -491,6 +551,11 @@ static hipError_t launch_table_nt(const Geom& geo, const LutPlan& plan, int cb_d
 #undef AQ_LUT_X
 }
 
+// Arrival counters of one launch: one per (row slice, token pass).  A table
+// has at most 144 slots (144 KB of LDS), so a row takes at most 9 lanes and a
+// row step (four waves) at least 28 rows; a launch covers at most 32 tokens.
+size_t lut_arrival_count(int C_out) { return (size_t)((C_out + 15) / 16) * 32; }
+
 int lut_tokens_per_entry(const LutPlan& plan, int ntok) {
     int nt = ntok >= 3 ? 4 : ntok;
     while (nt > plan.nt_max) nt >>= 1;
@@ -499,7 +564,7 @@ int lut_tokens_per_entry(const LutPlan& plan, int ntok) {
 
 hipError_t launch_lut_forward(const Geom& geo, const DeviceWeights& w, const LutPlan& plan, const void* X,
                               int x_dtype, const float* x_scales, void* Y, int y_dtype, float* ws,
-                              hipStream_t stream) {
+                              uint32_t* arrivals, bool one_launch, hipStream_t stream) {
     for (int64_t tok0 = 0; tok0 < geo.tokens; tok0 += plan.tok_block) {
         const int ntok = (int)((geo.tokens - tok0 < plan.tok_block) ? geo.tokens - tok0 : plan.tok_block);
         const int nt = lut_tokens_per_entry(plan, ntok);
@@ -538,8 +603,17 @@ hipError_t launch_lut_forward(const Geom& geo, const DeviceWeights& w, const Lut
         a.cpw = cpw;
         a.rpl = rpl;
         const int64_t cgs = (plan.nchunk + cpw - 1) / cpw;
+        if ((size_t)(slices * passes) > lut_arrival_count(geo.C_out)) return hipErrorInvalidValue;
         a.tok_block = plan.tok_block;
         a.ws = ws;
+        a.arrivals = arrivals;
+        a.ncg = (int)cgs;
+        a.scales = w.scales;
+        a.x_scales = x_scales;
+        a.Y = Y;
+        a.tok_out0 = tok0;
+        a.y_dtype = y_dtype;
+        a.one_launch = one_launch ? 1 : 0;
         hipError_t e;
         switch (nt) {
         case 4: e = launch_table_nt<4>(geo, plan, w.cb_dtype, x_dtype, a, stream); break;
@@ -547,6 +621,7 @@ hipError_t launch_lut_forward(const Geom& geo, const DeviceWeights& w, const Lut
         default: e = launch_table_nt<1>(geo, plan, w.cb_dtype, x_dtype, a, stream); break;
         }
         if (e != hipSuccess) return e;
+        if (one_launch) continue;
         const int64_t nout = (int64_t)ntok * geo.C_out;
         const dim3 grid((unsigned)((nout + 15) / 16));
         if (y_dtype == AQ_F32)

@@ -208,15 +208,52 @@ LUT_CASES = [
 
 
 @pytest.mark.parametrize("case", LUT_CASES, ids=lambda c: c[0])
-def test_lut_kernel(case):
+@pytest.mark.parametrize("one_launch", [0, 1])
+def test_lut_kernel(case, one_launch):
     name, C_out, K, M, B, n, xd, cbd, yd = case
     spec = LayerSpec(name=name, C_out=C_out, K=K, g=8, M=M, B=B, n=n, x_dtype=xd, codebook_dtype=cbd, y_dtype=yd)
     inp = generate(spec, 4321)
-    _say(f"lut {name}")
-    y = _run(spec, inp, "lut")
-    err = O.rel_err_inf(y, O.forward(spec, inp))
+    _say(f"lut {name} one_launch={one_launch}")
+    y = _run(spec, inp, "lut", opts={"table_one_launch": one_launch})
+    y_ref = O.forward(spec, inp)
+    err = O.rel_err_inf(y, y_ref)
     _say(f"  rel_err_inf={err:.3e}")
     assert err <= (1e-5 if yd == "f32" else 2e-3)
+    bound = O.rounding_bound(spec, y_ref, O.forward(spec, O.abs_inputs(spec, inp)), "lut")
+    assert np.all(np.abs(y - y_ref) <= bound)
+
+
+def test_lut_one_launch_graph_replays_and_repeats():
+    """The in-kernel reduction's arrival counters reset themselves: repeated forwards and graph
+    replays (several token blocks per forward) agree bit for bit."""
+    import paper_2506_05960_amd as P
+    spec = LayerSpec(name="lut1", C_out=300, K=4096, g=8, M=2, B=8, n=70)
+    inp = generate(spec, 5)
+    layer = P.AQLayer(spec, inp)
+    layer.set_path("lut")
+    layer.set_option("table_one_launch", 1)
+    x = _dev(inp["x"], "f16")
+    eager = layer.forward(x).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(layer.forward(x), eager)
+    assert O.rel_err_inf(eager.float().cpu().numpy(), O.forward(spec, inp)) <= 2e-3
+    y = torch.zeros_like(eager)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            layer.forward(x, out=y)
+            layer.forward(x, out=y)
+    torch.cuda.current_stream().wait_stream(s)
+    for rep in range(3):
+        y.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager), rep
+        assert torch.equal(layer.forward(x), eager)
+    layer.close()
 
 
 def test_lut_g9_conv_partial_chunk():
@@ -490,8 +527,12 @@ def test_dispatch_choice():
     spec_k = LayerSpec(name="disp_k", C_out=64, K=8192, g=8, M=2, B=8, n=64)
     layer = P.AQLayer(spec_k, generate(spec_k, 1))
     assert layer.choose_path(1) == "lut"             # long reduction, few tokens: the table path
-    assert layer.choose_path(16) == "lut"
-    assert layer.choose_path(17) == "decode"
+    assert layer.choose_path(4) == "lut"
+    assert layer.choose_path(5) == "decode"
+    layer.close()
+    spec_k4 = LayerSpec(name="disp_k4", C_out=64, K=8192, g=8, M=4, B=8, n=64)
+    layer = P.AQLayer(spec_k4, generate(spec_k4, 1))
+    assert layer.choose_path(1) == "lut" and layer.choose_path(2) == "decode"
     layer.set_path("decode")
     assert layer.choose_path(1) == "decode"
     layer.close()
