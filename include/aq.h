@@ -115,6 +115,26 @@ aq_status aq_layer_forward(aq_layer* layer, const void* X, const float* x_scales
                            void* stream);
 
 /*
+ * Allocation-free forward, for callers that cannot allocate device memory
+ * during the call or keep per-layer workspace (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation).  Arguments,
+ * validation, route, kernels and results (bit for bit) are those of
+ * aq_layer_forward; the per-call scratch of the kernels -- the table path's
+ * partial sums and arrival counters, the fused kernel's K-split partial tiles
+ * and arrival counters, the pre-decoded operand records and the dense
+ * product's repacked activations -- lives in one static device array of the
+ * library (64 MiB per GPU, 256 KiB of it counters) instead of the layer's
+ * workspace.  It calls no hipMalloc, hipFree or allocating library routine.
+ * A call whose scratch would exceed the array returns AQ_ERR_UNSUPPORTED
+ * before launching anything.  The first call on a device resolves the
+ * array's address and clears its counters with a small kernel on `stream`.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (other streams, other threads) race; serialise them.
+ */
+aq_status aq_layer_forward_static(aq_layer* layer, const void* X, const float* x_scales, void* Y, int64_t n,
+                                  void* stream);
+
+/*
  * Decoded weights W [C_out][K] in desc->tile_dtype (device, caller-owned),
  * computed as the decode path does (eq. (4) with the per-channel scale): the
  * M codewords summed in ascending m -- in fp16, rounding each partial sum,

@@ -13,6 +13,7 @@ from .aq import (  # noqa: F401
     make_desc,
     aq_layer_create,
     aq_layer_forward,
+    aq_layer_forward_static,
     aq_layer_decode,
     aq_layer_codebook_grad,
     aq_layer_set_path,

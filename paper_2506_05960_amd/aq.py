@@ -29,7 +29,7 @@ OPTION_CODES = {"lut_max_tokens": 1, "weights": 2, "generic": 3, "record_product
                 "grad_splits": 11, "grad_regs": 12, "grad_tile": 13, "table_one_launch": 14}
 _TILE_OPTIONS = ("fused_tile", "dense_tile", "grad_tile")
 
-EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
+EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_decode", "aq_layer_codebook_grad",
             "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
             "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy",
             "aq_last_error", "aq_version")
@@ -75,6 +75,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
     lib.aq_layer_create.argtypes = [ctypes.POINTER(aq_layer_desc), vp, vp, vp, i32, i32, i32, ctypes.POINTER(vp)]
     lib.aq_layer_forward.argtypes = [vp, vp, vp, vp, i64, vp]
+    lib.aq_layer_forward_static.argtypes = [vp, vp, vp, vp, i64, vp]
     lib.aq_layer_decode.argtypes = [vp, vp, vp]
     lib.aq_layer_codebook_grad.argtypes = [vp, vp, vp, i32, vp, i64, vp]
     lib.aq_layer_set_path.argtypes = [vp, i32]
@@ -85,7 +86,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_describe.argtypes = [vp, i64, ctypes.c_char_p, i64]
     lib.aq_layer_choose_path.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_int)]
     lib.aq_layer_destroy.argtypes = [vp]
-    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_decode", "aq_layer_codebook_grad",
+    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_decode", "aq_layer_codebook_grad",
               "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
               "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy"):
         getattr(lib, f).restype = ctypes.c_int
@@ -133,6 +134,10 @@ def aq_layer_create(desc: aq_layer_desc, codebooks: np.ndarray, codes: np.ndarra
 
 def aq_layer_forward(handle: int, X: int, x_scales: int, Y: int, n: int, stream: int) -> None:
     _check(load_library().aq_layer_forward(handle, X, x_scales, Y, n, stream))
+
+
+def aq_layer_forward_static(handle: int, X: int, x_scales: int, Y: int, n: int, stream: int) -> None:
+    _check(load_library().aq_layer_forward_static(handle, X, x_scales, Y, n, stream))
 
 
 def aq_layer_decode(handle: int, W: int, stream: int) -> None:
@@ -279,8 +284,11 @@ class AQLayer:
         s = self.spec
         return n if s.conv is None else n * s.conv.OH * s.conv.OW
 
-    def forward(self, x, x_scales=None, out=None, stream=None):
-        """Y for device tensor ``x`` (token-major [n, K] or NCHW); returns ``out``."""
+    def forward(self, x, x_scales=None, out=None, stream=None, static=False):
+        """Y for device tensor ``x`` (token-major [n, K] or NCHW); returns ``out``.
+
+        ``static=True`` calls the allocation-free entry point (scratch in the
+        library's static device array instead of the layer's workspace)."""
         import torch
         s = self.spec
         if not isinstance(x, torch.Tensor) or x.dim() < 1 or x.shape[0] < 1:
@@ -298,7 +306,7 @@ class AQLayer:
         _check_tensor("out", out, _torch_dtypes(s.y_dtype), self.out_shape(n), self.device)
         st = stream if stream is not None else torch.cuda.current_stream(x.device).cuda_stream
         xs = 0 if x_scales is None else x_scales.data_ptr()
-        aq_layer_forward(self.handle, x.data_ptr(), xs, out.data_ptr(), n, st)
+        (aq_layer_forward_static if static else aq_layer_forward)(self.handle, x.data_ptr(), xs, out.data_ptr(), n, st)
         return out
 
     __call__ = forward

@@ -733,6 +733,99 @@ aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X,
     return AQ_OK;
 }
 
+// ---- allocation-free forward: scratch in a static device array ----
+
+constexpr size_t kScratchBytes = size_t(64) << 20;             // per GPU
+constexpr size_t kScratchCounterBytes = size_t(256) << 10;     // arrival counters first (table, then K split)
+constexpr size_t kScratchLutCounters = 0;
+constexpr size_t kScratchSplitCounters = size_t(128) << 10;
+constexpr int kScratchMaxDevices = 64;
+
+}  // namespace
+
+// The scratch of aq_layer_forward_static.  Every GPU the library runs on holds
+// its own copy until the process ends.  Host code never uses this name as an
+// address: the per-device address comes from hipGetSymbolAddress.
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+
+__global__ void scratch_clear_kernel(uint32_t* p, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+struct ScratchDev {
+    uint8_t* ptr = nullptr;
+};
+std::mutex g_scratch_mu;
+ScratchDev g_scratch[kScratchMaxDevices];
+
+// The current device's scratch address; the first call on a device resolves it
+// and clears the counter area with a fill kernel on `st` (a memset could not
+// be captured into a graph safely).  The counters return to zero at the end of
+// every launch that uses them.
+aq_status scratch_for_current_device(hipStream_t st, uint8_t** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kScratchMaxDevices) return fail(AQ_ERR_UNSUPPORTED, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    ScratchDev& sd = g_scratch[dev];
+    if (!sd.ptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "scratch address");
+        const int n = (int)(kScratchCounterBytes / 4);
+        scratch_clear_kernel<<<(n + 255) / 256, 256, 0, st>>>(static_cast<uint32_t*>(p), n);
+        e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "scratch counter clear");
+        sd.ptr = static_cast<uint8_t*>(p);
+    }
+    *out = sd.ptr;
+    return AQ_OK;
+}
+
+size_t align256(size_t b) { return (b + 255) / 256 * 256; }
+
+// Lay the route's scratch out in the static array, or refuse.
+aq_status static_workspace(const aq_layer* L, const Geom& geo, const Route& r, uint8_t* base, Workspace* wk) {
+    *wk = Workspace{};
+    uint8_t* data = base + kScratchCounterBytes;
+    const size_t cap = kScratchBytes - kScratchCounterBytes;
+    size_t used = 0;
+    auto take = [&](size_t bytes) {
+        uint8_t* p = data + used;
+        used += align256(bytes);
+        return p;
+    };
+    if (r.kind == Route::LUT) {
+        const LutPlan& p = L->plan;
+        if (aq::lut_arrival_count(geo.C_out) * 4 > kScratchSplitCounters - kScratchLutCounters)
+            return fail(AQ_ERR_UNSUPPORTED, "static forward: too many table arrival counters (C_out > 16384)");
+        wk->lut_arrivals = reinterpret_cast<uint32_t*>(base + kScratchLutCounters);
+        wk->lut_ws = reinterpret_cast<float*>(take((size_t)p.nchunk * p.tok_block * geo.C_out * 4));
+    } else if (r.kind == Route::FUSED || r.kind == Route::REC_LINEAR || r.kind == Route::DENSE) {
+        const aq::FusedPlan& fp = r.fp;
+        if (fp.dec == aq::FUSED_DEC_REC) wk->wrec = take(aq::operand_record_bytes(geo, fp));
+        if (r.kind == Route::FUSED && fp.splitk > 1) {
+            if ((size_t)fp.ntiles * 4 > kScratchCounterBytes - kScratchSplitCounters)
+                return fail(AQ_ERR_UNSUPPORTED, "static forward: too many split arrival counters");
+            wk->arrivals = reinterpret_cast<uint32_t*>(base + kScratchSplitCounters);
+            wk->part = reinterpret_cast<float*>(take((size_t)fp.splitk * fp.ntiles * fp.bm * fp.bn * 4));
+        }
+        if (r.kind == Route::DENSE) {
+            const size_t xp = geo.conv ? (size_t)(geo.tokens / ((int64_t)geo.OH * geo.OW)) * geo.cin * geo.H * geo.W * 2
+                                       : L->desc.x_dtype == AQ_I8 ? (size_t)geo.tokens * geo.K * 2 : 0;
+            wk->xpack = take(xp);
+        }
+    }
+    if (used > cap)
+        return fail(AQ_ERR_UNSUPPORTED, "static forward: needs " + std::to_string(used) + " bytes of scratch, above the " +
+                                             std::to_string(cap) + " the static array holds");
+    return AQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -920,6 +1013,25 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
     if (s != AQ_OK) return s;
     const Workspace wk{L->d_ws, L->d_lut_arrivals, L->d_wrec, L->d_part, L->d_arrivals, L->d_xpack};
     return run_route(L, geo, r, X, x_scales, Y, n, static_cast<hipStream_t>(stream), wk);
+}
+
+aq_status aq_layer_forward_static(aq_layer* L, const void* X, const float* x_scales, void* Y, int64_t n,
+                                  void* stream) {
+    Route r;
+    Geom geo;
+    aq_status s = check_forward(L, X, x_scales, Y, n, &geo, &r);
+    if (s != AQ_OK) return s;
+    uint8_t* base = nullptr;
+    Workspace wk;
+    // sizes first, so a refused call launches nothing
+    s = static_workspace(L, geo, r, reinterpret_cast<uint8_t*>(uintptr_t(256)), &wk);
+    if (s != AQ_OK) return s;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    s = scratch_for_current_device(st, &base);
+    if (s != AQ_OK) return s;
+    s = static_workspace(L, geo, r, base, &wk);
+    if (s != AQ_OK) return s;
+    return run_route(L, geo, r, X, x_scales, Y, n, st, wk);
 }
 
 aq_status aq_layer_describe(const aq_layer* L, int64_t n, char* buf, int64_t size) {
