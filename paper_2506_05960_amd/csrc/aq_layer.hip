@@ -1046,7 +1046,9 @@ aq_status aq_layer_describe(const aq_layer* L, int64_t n, char* buf, int64_t siz
     std::string t = std::string("path=") + (r.kind == Route::LUT ? "lut" : "decode") + " route=" + kinds[r.kind];
     if (r.kind == Route::FUSED || r.kind == Route::REC_LINEAR || r.kind == Route::DENSE) {
         const aq::FusedPlan& p = r.fp;
-        t += std::string(" weights=") + decs[p.dec] + " tile=" + std::to_string(p.bm) + "x" + std::to_string(p.bn);
+        const bool rl = r.kind == Route::REC_LINEAR;
+        const int bm = rl ? (p.rlin_var == 1 ? 256 : 128) : p.bm, bn = rl ? 128 : p.bn;
+        t += std::string(" weights=") + decs[p.dec] + " tile=" + std::to_string(bm) + "x" + std::to_string(bn);
         if (r.kind == Route::FUSED)
             t += " upl=" + std::to_string(p.upl) + " split_k=" + std::to_string(p.splitk) +
                  " order=" + (p.nmajor ? "channel" : "token");
