@@ -408,6 +408,10 @@ def sweep_bench(a, torch, P, W):
         "kernels": [{"kernel": n, "launches": c, "total_us": round(t, 2)} for n, t, c, _ in ktable[:6]],
         "activation_rms": [round(min(rms), 4), round(max(rms), 4)],
     }
+    if a.copy_bytes > 0:
+        src_b = torch.empty(a.copy_bytes, dtype=torch.uint8, device="cuda")
+        torch.empty_like(src_b).copy_(src_b)
+        torch.cuda.synchronize()
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = sweep_cpu_baseline(specs, seeds)
     for layer, _, _ in objs:
@@ -429,8 +433,10 @@ def lut_regime_bench(a, torch, P, W):
     """
     import numpy as np
 
-    ns = (1, 2, 4, 8, 16, 32)
+    ns = tuple(int(v) for v in a.lut_ns.split(",")) if a.lut_ns else (1, 2, 4, 8, 16, 32)
     shapes = sorted(set((s.K, s.C_out, s.M) for s in W.lut_regime_specs()))
+    if a.lut_k:
+        shapes = [sh for sh in shapes if sh[0] == a.lut_k]
     tiny = torch.zeros(1, device="cuda")
     floor_us = _graph_time_us(torch, lambda: tiny.add_(1.0), reps=20)
     rows = []
@@ -590,6 +596,8 @@ def main(argv=None):
                     help="sweep: M = 2 or 4 codebooks of 256 (K: 3x3 convolutions with g = 9, one group per filter)")
     ap.add_argument("--full", action="store_true", help="sweep: every linear of the transformer blocks")
     ap.add_argument("--table", default="", help="sweep: write the per-layer table (markdown) here")
+    ap.add_argument("--lut-ns", default="", help="lutregime: token counts, comma separated (default 1..32)")
+    ap.add_argument("--lut-k", type=int, default=0, help="lutregime: only the shapes with this K")
     ap.add_argument("--op", default="forward", choices=["forward", "grad"],
                     help="grad: the codebook gradient of the named layer instead of its forward")
     a = ap.parse_args(argv)
