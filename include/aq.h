@@ -270,9 +270,10 @@ aq_status aq_layer_last_launches(const aq_layer* layer, int32_t* n_launches, cha
  * Text description of the route a forward over n tokens (linear) or images
  * (conv) would take, as "key=value" pairs: the path and kernel route, and for
  * the matrix-core kernels the weight source (in-loop decode or pre-decoded
- * records, with the bytes the records write), tile, K split and workgroup
- * order.  Pure host function; `buf` receives at most size - 1 characters and
- * a terminating zero.
+ * records, with the bytes the records write), tile, K split, workgroup
+ * order and workgroups per compute unit.  Host function: it launches nothing
+ * and queries only kernel occupancy on the current device; `buf` receives at
+ * most size - 1 characters and a terminating zero.
  */
 aq_status aq_layer_describe(const aq_layer* layer, int64_t n, char* buf, int64_t size);
 

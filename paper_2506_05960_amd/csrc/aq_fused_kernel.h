@@ -837,6 +837,7 @@ static hipError_t fused_launch_cfg(const Geom& geo, const FusedPlan& plan, const
     auto kern = fused_fwd_kernel<KIND, CM, XT, DEC, MC, BM, BN, UPL, OCC>;
     hipError_t e = ensure_dynamic_lds((const void*)kern, plan.lds_bytes);
     if (e != hipSuccess) return e;
+    if (fl.occupancy) return hipOccupancyMaxActiveBlocksPerMultiprocessor(fl.occupancy, kern, 256, plan.lds_bytes);
     const dim3 grid((unsigned)(((geo.tokens + BM - 1) / BM) * ((geo.C_out + BN - 1) / BN) * plan.splitk));
     kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.cb, fl.crec, fl.scales, fl.X, fl.x_scales, fl.Y,
                                                    fl.y_dtype, fl.part, fl.arrivals);

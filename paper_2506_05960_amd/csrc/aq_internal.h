@@ -126,6 +126,8 @@ struct FusedLaunch {
     hipStream_t stream;
     float* part;          // K split: fp32 partial tiles [ntiles][splitk][BM * BN] (null without a split)
     uint32_t* arrivals;   // K split: arrival counter per tile, zero between launches
+    int* occupancy;       // non-null: store the instantiation's workgroups per compute unit
+                          // at plan.lds_bytes and launch nothing
 };
 
 hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);

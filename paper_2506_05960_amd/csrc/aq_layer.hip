@@ -1,6 +1,7 @@
 // C ABI entry points: argument validation (host only, before any HIP call),
 // device copies and repacking of the quantized weights, path dispatch.
 #include <algorithm>
+#include <array>
 #include <cmath>
 #include <cstdio>
 #include <cstdint>
@@ -378,7 +379,51 @@ bool underfilled(const Geom& geo) {
     return ((geo.tokens + 63) / 64) * (int64_t)((geo.C_out + 63) / 64) < 256;
 }
 
-bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, aq::FusedPlan* p) {
+// Workgroups of one fused-kernel instantiation that a compute unit holds at once
+// (registers and LDS), as the runtime reports it; cached per device and
+// instantiation, 1 where the query fails.
+int fused_occupancy(const Geom& geo, const aq::FusedPlan& q, int x_dtype) {
+    static std::mutex mu;
+    static std::map<std::array<int64_t, 10>, int> cache;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return 1;
+    const std::array<int64_t, 10> key{dev, q.kind, q.cm, x_dtype, q.dec, q.mc, q.bm, q.bn, q.upl, (int64_t)q.lds_bytes};
+    {
+        std::lock_guard<std::mutex> lock(mu);
+        auto it = cache.find(key);
+        if (it != cache.end()) return it->second;
+    }
+    int occ = 0;
+    aq::FusedLaunch fl{};
+    fl.x_dtype = x_dtype;
+    fl.occupancy = &occ;
+    if (aq::launch_fused_forward(geo, q, fl) != hipSuccess || occ < 1) {
+        (void)hipGetLastError();
+        occ = 1;
+    }
+    std::lock_guard<std::mutex> lock(mu);
+    cache[key] = occ;
+    return occ;
+}
+
+// Time of `n` workgroups on one compute unit that holds `occ` at once, each
+// with `loop` units of main-loop work and `fixed` of prologue and epilogue:
+// workgroups sharing a compute unit share its matrix and LDS throughput in the
+// main loop (each one more adds 0.9 of its loop time) and hide each other's
+// fixed costs (fitted to forced-tile timings of the U-Net's convolutions at
+// 512 to 32768 tokens, both weight modes, M = 2 and 4).
+constexpr double kShareLoop = 0.9;
+constexpr double kShareFixed = 0.0;
+
+double cu_time(int64_t n, int occ, double loop, double fixed) {
+    auto together = [&](int64_t k) {
+        return k > 0 ? loop * (1.0 + kShareLoop * (double)(k - 1)) + fixed * (1.0 + kShareFixed * (double)(k - 1))
+                     : 0.0;
+    };
+    return (double)(n / occ) * together(occ) + together(n % occ);
+}
+
+bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, int x_dtype, aq::FusedPlan* p) {
     static const TileCand conv3[] = {{64, 96, 3}, {64, 64, 3}, {128, 64, 3}, {128, 64, 6}, {64, 64, 6}};
     static const TileCand conv1[] = {{64, 96, 4}, {64, 64, 4}};
     static const TileCand lin[] = {{64, 96, 8}, {64, 64, 8}, {32, 128, 4}, {32, 64, 4}};
@@ -455,8 +500,12 @@ bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, a
         q.lds_bytes = (size_t)p->cb_bytes + std::max<size_t>((size_t)8 * q.pbuf_bytes, red);
         if (q.lds_bytes > kLdsBytes) continue;
         const int64_t nwg = ((geo.tokens + t.bm - 1) / t.bm) * (int64_t)((geo.C_out + t.bn - 1) / t.bn);
-        // rounds of whole-chip work, weighted by a per-tile overhead term; linear
-        // layers also weigh the staging units per lane (fitted to measured tiles)
+        // convolutions: workgroups per compute unit (the grid spread over 256) timed
+        // by cu_time; linear layers' tile costs were fitted with one workgroup per
+        // compute unit and keep that model
+        const int occ = p->kind != 0 ? fused_occupancy(geo, q, x_dtype) : 1;
+        // each workgroup weighted by a per-tile overhead term; linear layers also
+        // weigh the staging units per lane (fitted to measured tiles)
         double tcost = (double)t.bm * t.bn * (1.0 + 48.0 / t.bm + 48.0 / t.bn);
         if (p->kind == 0) tcost *= t.upl / (t.upl + 2.0);
         // pre-decoded operands of a linear layer: the 64 x 64 tile measured best
@@ -472,10 +521,9 @@ bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, a
                 if ((size_t)S * nwg * t.bm * t.bn * 4 > part_cap) continue;
                 if (nwg * S >= (int64_t(1) << 24)) continue;
             }
-            const int64_t rounds = (nwg * S + 255) / 256;
-            const double cpw = std::ceil((double)p->nchunk / (4.0 * S));
-            double cost = (double)rounds * tcost *
-                          (cpw + (under ? kFixedChunksUnderfilled : kFixedChunks) + (S > 1 ? kSplitChunks : 0.0));
+            const double cpw = std::ceil((double)p->nchunk / (4.0 * S)) + (S > 1 ? kSplitChunks : 0.0);
+            double cost = tcost * cu_time((nwg * S + 255) / 256, occ, cpw,
+                                          under ? kFixedChunksUnderfilled : kFixedChunks);
             // a forced split wins over the unsplit fallback of the same tile
             if (opt.split_k > 1 && S == 1) cost *= 1e6;
             if (!found || cost < best) {
@@ -491,7 +539,7 @@ bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, a
     if (!found && want_bm) {
         aq::Options o = opt;
         o.fused_bm = o.fused_bn = 0;      // the forced tile does not fit: the planner's choice
-        return fused_plan_tile(geo, o, part_cap, p);
+        return fused_plan_tile(geo, o, part_cap, x_dtype, p);
     }
     if (found) *p = bestp;
     return found;
@@ -640,7 +688,7 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
         r.fp = gp;
         return r;
     }
-    if (L->fused_ok && fits31 && opt.generic != 1 && fused_plan_tile(geo, opt, L->part_bytes, &fp)) {
+    if (L->fused_ok && fits31 && opt.generic != 1 && fused_plan_tile(geo, opt, L->part_bytes, d.x_dtype, &fp)) {
         order(fp);
         fp.tile_div = fp.nmajor ? (int)((geo.tokens + fp.bm - 1) / fp.bm) : (geo.C_out + fp.bn - 1) / fp.bn;
         fp.inv_tile_div = 1.0f / (float)fp.tile_div;
@@ -974,7 +1022,7 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
                 }
                 // room for every split count the planner allows on its tile, so a
                 // forced split (AQ_OPT_SPLIT_K) fits too
-                if (fused_plan_tile(gmax, aq::Options{}, SIZE_MAX, &q) && q.ntiles < 256) {
+                if (fused_plan_tile(gmax, aq::Options{}, SIZE_MAX, desc->x_dtype, &q) && q.ntiles < 256) {
                     const int smax = std::min<int>({aq::kMaxSplitK, 512 / q.ntiles, q.nchunk / 4});
                     if (smax > 1) need = std::max(need, (size_t)smax * q.ntiles * q.bm * q.bn * 4);
                 }
@@ -1051,7 +1099,8 @@ aq_status aq_layer_describe(const aq_layer* L, int64_t n, char* buf, int64_t siz
         t += std::string(" weights=") + decs[p.dec] + " tile=" + std::to_string(bm) + "x" + std::to_string(bn);
         if (r.kind == Route::FUSED)
             t += " upl=" + std::to_string(p.upl) + " split_k=" + std::to_string(p.splitk) +
-                 " order=" + (p.nmajor ? "channel" : "token");
+                 " order=" + (p.nmajor ? "channel" : "token") +
+                 " wg_per_cu=" + std::to_string(fused_occupancy(geo, p, L->desc.x_dtype));
         if (r.kind == Route::REC_LINEAR) t += " variant=" + std::to_string(p.rlin_var);
         if (p.dec == aq::FUSED_DEC_REC)
             t += " records_bytes=" + std::to_string(aq::operand_record_bytes(geo, p));
