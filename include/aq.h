@@ -197,7 +197,10 @@ aq_status aq_layer_set_path(aq_layer* layer, aq_path path);
  *                           layers: the wave-split linear kernel), 1 the
  *                           fused kernel's own pre-decoded loop (outputs
  *                           bit-identical to its in-loop decode), 2 the
- *                           dense product with both operands staged in LDS
+ *                           dense product with both operands staged in LDS,
+ *                           3 the wave-split 3x3 convolution kernel where it
+ *                           applies (128-token tiles, image planes a multiple
+ *                           of 4 pixels)
  *   AQ_OPT_FUSED_TILE       fused kernel tile BM * 1000 + BN (0 = planner);
  *                           a tile that does not fit falls back to the planner
  *   AQ_OPT_DENSE_TILE       dense product tile BM * 1000 + BN (0 = planner)

@@ -384,10 +384,11 @@ bool underfilled(const Geom& geo) {
 // instantiation, 1 where the query fails.
 int fused_occupancy(const Geom& geo, const aq::FusedPlan& q, int x_dtype) {
     static std::mutex mu;
-    static std::map<std::array<int64_t, 10>, int> cache;
+    static std::map<std::array<int64_t, 11>, int> cache;
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 1;
-    const std::array<int64_t, 10> key{dev, q.kind, q.cm, x_dtype, q.dec, q.mc, q.bm, q.bn, q.upl, (int64_t)q.lds_bytes};
+    const std::array<int64_t, 11> key{dev,  q.kind, q.cm, x_dtype, q.dec, q.mc, q.bm, q.bn, q.upl, (int64_t)q.lds_bytes,
+                                      q.wsplit * 16 + q.rdepth};
     {
         std::lock_guard<std::mutex> lock(mu);
         auto it = cache.find(key);
@@ -397,7 +398,8 @@ int fused_occupancy(const Geom& geo, const aq::FusedPlan& q, int x_dtype) {
     aq::FusedLaunch fl{};
     fl.x_dtype = x_dtype;
     fl.occupancy = &occ;
-    if (aq::launch_fused_forward(geo, q, fl) != hipSuccess || occ < 1) {
+    const hipError_t e = q.wsplit ? aq::launch_rec_conv3(geo, q, fl) : aq::launch_fused_forward(geo, q, fl);
+    if (e != hipSuccess || occ < 1) {
         (void)hipGetLastError();
         occ = 1;
     }
@@ -421,6 +423,51 @@ double cu_time(int64_t n, int occ, double loop, double fixed) {
                      : 0.0;
     };
     return (double)(n / occ) * together(occ) + together(n % occ);
+}
+
+// Staging geometry of a convolution tile of `bm` output pixels: the input
+// rows it reads (each input row once per block of output rows of one image: a
+// tile of whole images, or of consecutive rows of one image; kh rows per output
+// row when that stages fewer rows or AQ_OPT_STAGE_ROWS = 1), their padded width,
+// and the staging units (plane of 8 channels, staged row, pixel pair).  With
+// `widen`, a staged row is widened until consecutive output rows start OW
+// 16-byte slots apart (mod 64 banks), which makes A-fragment reads of rows
+// shorter than 16 tokens conflict free.  False when bm and OW do not tile
+// each other.
+bool conv_staging(const Geom& geo, const aq::Options& opt, int kind, int cm, int bm, bool widen, aq::FusedPlan* q) {
+    if (!(bm % geo.OW == 0 || geo.OW % bm == 0)) return false;
+    const int tr = bm >= geo.OW ? bm / geo.OW : 1;
+    const int kh = kind == 1 ? 3 : 1;
+    const int img = geo.OH * geo.OW;
+    int rpb = 1;
+    if (opt.stage_rows != 1) {
+        if (bm % img == 0) rpb = geo.OH;
+        else if (img % bm == 0 && tr > 1) rpb = tr;
+    }
+    int sr = (rpb - 1) * geo.stride + kh;
+    if (rpb > 1 && (tr / rpb) * sr >= tr * kh) {
+        rpb = 1;
+        sr = kh;
+    }
+    q->rpb = rpb;
+    q->sr = sr;
+    q->inv_rpb = 1.0f / (float)rpb;
+    q->inv_sr = 1.0f / (float)sr;
+    q->pr = (tr / rpb) * sr;
+    q->pw = geo.W + 2 * geo.pad;
+    // consecutive output rows of a block are `stride` staged rows apart (kh
+    // apart with one output row per block)
+    const int rstep = rpb > 1 ? geo.stride : kh;
+    if (widen)
+        while ((rstep * q->pw - geo.OW) % 16 != 0) ++q->pw;
+    q->ps = q->pr * q->pw * 16;                    // one plane of 8 channels
+    q->units = 2 * cm * q->pr * (geo.W / 2);       // (plane, row, pixel pair)
+    q->total_rows = (int)(geo.tokens / geo.OW);
+    q->inv_ow = 1.0f / (float)geo.OW;
+    q->inv_oh = 1.0f / (float)geo.OH;
+    q->inv_pr = 1.0f / (float)q->pr;
+    q->inv_wp = 1.0f / (float)(geo.W / 2);
+    return true;
 }
 
 bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, int x_dtype, aq::FusedPlan* p) {
@@ -449,42 +496,7 @@ bool fused_plan_tile(const Geom& geo, const aq::Options& opt, size_t part_cap, i
         q.bn = t.bn;
         q.upl = t.upl;
         if (p->kind != 0) {
-            if (!(t.bm % geo.OW == 0 || geo.OW % t.bm == 0)) continue;
-            const int tr = t.bm >= geo.OW ? t.bm / geo.OW : 1;
-            const int kh = p->kind == 1 ? 3 : 1;
-            // Staged rows: each input row once per block of output rows of one image
-            // (a tile of whole images, or of consecutive rows of one image), instead
-            // of kh rows per output row, when that stages fewer rows (option
-            // AQ_OPT_STAGE_ROWS = 1 keeps kh rows per output row).
-            const int img = geo.OH * geo.OW;
-            int rpb = 1;
-            if (opt.stage_rows != 1) {
-                if (t.bm % img == 0) rpb = geo.OH;
-                else if (img % t.bm == 0 && tr > 1) rpb = tr;
-            }
-            int sr = (rpb - 1) * geo.stride + kh;
-            if (rpb > 1 && (tr / rpb) * sr >= tr * kh) {
-                rpb = 1;
-                sr = kh;
-            }
-            q.rpb = rpb;
-            q.sr = sr;
-            q.inv_rpb = 1.0f / (float)rpb;
-            q.inv_sr = 1.0f / (float)sr;
-            q.pr = (tr / rpb) * sr;
-            q.pw = geo.W + 2 * geo.pad;
-            // consecutive output rows of a block are `stride` staged rows apart (kh
-            // apart with one output row per block)
-            const int rstep = rpb > 1 ? geo.stride : kh;
-            if (widen)
-                while ((rstep * q.pw - geo.OW) % 16 != 0) ++q.pw;
-            q.ps = q.pr * q.pw * 16;                    // one plane of 8 channels
-            q.units = 2 * p->cm * q.pr * (geo.W / 2);   // (plane, row, pixel pair)
-            q.total_rows = (int)(geo.tokens / geo.OW);
-            q.inv_ow = 1.0f / (float)geo.OW;
-            q.inv_oh = 1.0f / (float)geo.OH;
-            q.inv_pr = 1.0f / (float)q.pr;
-            q.inv_wp = 1.0f / (float)(geo.W / 2);
+            if (!conv_staging(geo, opt, p->kind, p->cm, t.bm, widen, &q)) continue;
         } else {
             q.pr = q.pw = 0;
             q.sr = q.rpb = 1;
@@ -645,6 +657,35 @@ bool use_predecoded(const aq_layer* L, const Geom& geo) {
 
 // The route of one forward, resolved on the host (shared by the forward and
 // aq_layer_describe).
+// The 2 x 2 wave-split records kernel for a 3x3 convolution: a 128-token tile,
+// 192 channels where C_out is a multiple of 192 (else 128), and its staging.
+// False where the kernel does not apply (tile rows, image planes not a
+// multiple of 4 tokens, more than 768 staging units).
+bool wsplit_plan(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) {
+    if (p->kind != 1 || p->dec != aq::FUSED_DEC_REC) return false;
+    if ((geo.OH * geo.OW) % 4 != 0 || geo.W % 2 != 0) return false;
+    aq::FusedPlan q = *p;
+    if (!conv_staging(geo, opt, 1, 1, 128, false, &q)) return false;
+    q.upl = (q.units + 255) / 256;
+    if (q.upl > 3) return false;
+    int bn = geo.C_out % 192 == 0 ? 192 : 128;
+    if (opt.fused_bm == 128 && (opt.fused_bn == 128 || opt.fused_bn == 192)) bn = opt.fused_bn;
+    q.bm = 128;
+    q.bn = bn;
+    q.wsplit = 1;
+    q.rdepth = 3;
+    q.splitk = 1;
+    q.pbuf_bytes = 2 * q.ps + 32;                // two planes and a spare slot
+    q.lds_bytes = (size_t)2 * q.pbuf_bytes;
+    if (q.lds_bytes > kLdsBytes) return false;
+    const int64_t nt = ((geo.tokens + 127) / 128) * (int64_t)((geo.C_out + bn - 1) / bn);
+    if (nt >= (int64_t(1) << 24)) return false;
+    q.ntiles = (int)nt;
+    q.inv_ntiles = 1.0f / (float)nt;
+    *p = q;
+    return true;
+}
+
 struct Route {
     enum Kind { LUT = 0, F32 = 1, GENERIC = 2, DENSE = 3, FUSED = 4, REC_LINEAR = 5, NONE = 6 } kind;
     aq::FusedPlan fp;
@@ -688,7 +729,23 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
         r.fp = gp;
         return r;
     }
-    if (L->fused_ok && fits31 && opt.generic != 1 && fused_plan_tile(geo, opt, L->part_bytes, d.x_dtype, &fp)) {
+    // Pre-decoded 3x3 convolutions: the wave-split records kernel where its
+    // 128-token tiles number at least 192 (measured on the U-Net shapes: 20-25 %
+    // faster than the fused kernel's best tile at 32768 tokens, 256-512 tiles;
+    // slower with 128 tiles or fewer, which leave compute units idle).
+    // AQ_OPT_RECORD_PRODUCT = 3 forces it where it applies, 1 and 2 exclude it.
+    bool planned = false;
+    if (L->fused_ok && fits31 && opt.generic != 1 && fp.dec == aq::FUSED_DEC_REC && fp.kind == 1 &&
+        (opt.rec_product == 3 || opt.rec_product == 0)) {
+        aq::FusedPlan wp = fp;
+        if (wsplit_plan(geo, opt, &wp) && (opt.rec_product == 3 || wp.ntiles >= 192)) {
+            fp = wp;
+            planned = true;
+        }
+    }
+    if (!planned && L->fused_ok && fits31 && opt.generic != 1)
+        planned = fused_plan_tile(geo, opt, L->part_bytes, d.x_dtype, &fp);
+    if (planned) {
         order(fp);
         fp.tile_div = fp.nmajor ? (int)((geo.tokens + fp.bm - 1) / fp.bm) : (geo.C_out + fp.bn - 1) / fp.bn;
         fp.inv_tile_div = 1.0f / (float)fp.tile_div;
@@ -772,7 +829,9 @@ aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X,
                               : geo.tokens * (int64_t)geo.K * (d.x_dtype == AQ_I8 ? 1 : 2);
         const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st, wk.part, wk.arrivals};
         if (e == hipSuccess)
-            e = r.kind == Route::REC_LINEAR ? aq::launch_rec_linear(geo, fp, fl) : aq::launch_fused_forward(geo, fp, fl);
+            e = r.kind == Route::REC_LINEAR ? aq::launch_rec_linear(geo, fp, fl)
+                : fp.wsplit                  ? aq::launch_rec_conv3(geo, fp, fl)
+                                             : aq::launch_fused_forward(geo, fp, fl);
         break;
     }
     }
@@ -1091,12 +1150,14 @@ aq_status aq_layer_describe(const aq_layer* L, int64_t n, char* buf, int64_t siz
     static const char* kinds[] = {"table", "fp32", "generic", "dense-records", "fused", "rec-linear", "none"};
     static const char* decs[] = {"in-loop-lds-fp16", "in-loop-lds-fp32", "in-loop-lds-fp16", "in-loop-l2-fp16",
                                  "records"};
-    std::string t = std::string("path=") + (r.kind == Route::LUT ? "lut" : "decode") + " route=" + kinds[r.kind];
+    const char* route = r.kind == Route::FUSED && r.fp.wsplit ? "rec-conv" : kinds[r.kind];
+    std::string t = std::string("path=") + (r.kind == Route::LUT ? "lut" : "decode") + " route=" + route;
     if (r.kind == Route::FUSED || r.kind == Route::REC_LINEAR || r.kind == Route::DENSE) {
         const aq::FusedPlan& p = r.fp;
         const bool rl = r.kind == Route::REC_LINEAR;
         const int bm = rl ? (p.rlin_var == 1 ? 256 : 128) : p.bm, bn = rl ? 128 : p.bn;
         t += std::string(" weights=") + decs[p.dec] + " tile=" + std::to_string(bm) + "x" + std::to_string(bn);
+        if (r.kind == Route::FUSED && p.wsplit) t += " depth=" + std::to_string(p.rdepth);
         if (r.kind == Route::FUSED)
             t += " upl=" + std::to_string(p.upl) + " split_k=" + std::to_string(p.splitk) +
                  " order=" + (p.nmajor ? "channel" : "token") +
@@ -1250,7 +1311,7 @@ aq_status aq_layer_set_option(aq_layer* L, int32_t option, int64_t value) {
         o.generic = (int)value;
         return AQ_OK;
     case AQ_OPT_RECORD_PRODUCT:
-        if (!in(0, 2)) return bad();
+        if (!in(0, 3)) return bad();
         o.rec_product = (int)value;
         return AQ_OK;
     case AQ_OPT_FUSED_TILE:

@@ -317,6 +317,65 @@ def test_predecoded_operands_match_in_loop_decode(spec):
     assert err <= 2e-3 and err_g <= 2e-3
 
 
+# The wave-split records kernel for 3x3 convolutions (128-token tiles, four
+# waves splitting the tile 2 x 2): tile rows of 1 to 16 output rows, whole
+# images per tile, partial last tiles, stride 2, ragged channel tiles
+# (C_out not a multiple of the 128 / 192 tile), M = 1, 4 and g = 9 records,
+# fp32 outputs.
+WSPLIT = [
+    LayerSpec(name="ws_c192_16x16", C_out=192, K=64 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(64, 3, 3, 1, 1, 16, 16)),
+    LayerSpec(name="ws_c100_8x32", C_out=100, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 8, 32)),
+    LayerSpec(name="ws_s2_32x32", C_out=128, K=48 * 9, g=8, M=2, B=8, n=2, conv=ConvGeom(48, 3, 3, 2, 1, 32, 32)),
+    LayerSpec(name="ws_64x64", C_out=384, K=16 * 9, g=8, M=4, B=8, n=1, conv=ConvGeom(16, 3, 3, 1, 1, 64, 64)),
+    LayerSpec(name="ws_8x8_imgs", C_out=200, K=32 * 9, g=8, M=1, B=8, n=5, conv=ConvGeom(32, 3, 3, 1, 1, 8, 8)),
+    LayerSpec(name="ws_g9", C_out=64, K=32 * 9, g=9, M=2, B=8, n=2, conv=ConvGeom(32, 3, 3, 1, 1, 16, 16)),
+    LayerSpec(name="ws_f32out_w256", C_out=128, K=16 * 9, g=8, M=2, B=8, n=1, y_dtype="f32",
+              conv=ConvGeom(16, 3, 3, 1, 1, 4, 256)),
+    LayerSpec(name="ws_long_k", C_out=192, K=320 * 9, g=8, M=2, B=8, n=1, conv=ConvGeom(320, 3, 3, 1, 1, 16, 16)),
+]
+
+
+@pytest.mark.parametrize("spec", WSPLIT, ids=lambda s: s.name)
+def test_wave_split_conv_matches_oracle(spec):
+    import paper_2506_05960_amd as P
+    inp = generate(spec, 606)
+    layer = P.AQLayer(spec, inp)
+    layer.set_option("weights", 2)
+    layer.set_option("record_product", 3)
+    d = layer.describe(spec.n)
+    _say(f"wave split {spec.name} tokens={spec.tokens} {d}")
+    assert d["route"] == "rec-conv"
+    x = _dev(inp["x"], spec.x_dtype)
+    y1 = layer.forward(x).float().cpu().numpy().astype(np.float64)
+    y2 = layer.forward(x).float().cpu().numpy().astype(np.float64)
+    layer.close()
+    assert np.array_equal(y1, y2)
+    tok = np.arange(spec.tokens)
+    ch = np.arange(spec.C_out)
+    check_against_oracle(spec, inp, sampled_outputs(spec, y1, tok, ch), tok, ch, "decode", TOL[spec.tile_dtype])
+
+
+def test_wave_split_conv_staging_and_fallback():
+    """Input rows staged once per image block or kh rows per output row give identical outputs; shapes the
+    kernel does not take (output rows that do not tile 128 tokens) keep the fused kernel."""
+    spec = WSPLIT[0]
+    inp = generate(spec, 61)
+    a = _run(spec, inp, "decode", opts={"weights": 2, "record_product": 3})
+    b = _run(spec, inp, "decode", opts={"weights": 2, "record_product": 3, "stage_rows": 1})
+    assert np.array_equal(a, b)
+    import paper_2506_05960_amd as P
+    for odd in (LayerSpec(name="ws_no_6x6", C_out=64, K=16 * 9, g=8, M=2, B=8, n=2, conv=ConvGeom(16, 3, 3, 1, 1, 6, 6)),
+                LayerSpec(name="ws_no_12", C_out=64, K=16 * 9, g=8, M=2, B=8, n=2, conv=ConvGeom(16, 3, 3, 1, 1, 8, 12))):
+        inp = generate(odd, 62)
+        layer = P.AQLayer(odd, inp)
+        layer.set_option("weights", 2)
+        layer.set_option("record_product", 3)
+        assert layer.describe(odd.n)["route"] in ("fused", "generic")
+        y = layer.forward(_dev(inp["x"], odd.x_dtype)).float().cpu().numpy().astype(np.float64)
+        layer.close()
+        assert O.rel_err_inf(y, O.forward(odd, inp)) <= 2e-3
+
+
 GEMM_CASES = [
     LayerSpec(name="g_conv3", C_out=200, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 24, 16)),
     LayerSpec(name="g_conv3_img8", C_out=150, K=48 * 9, g=8, M=1, B=16, n=5, conv=ConvGeom(48, 3, 3, 1, 1, 8, 8)),
