@@ -145,8 +145,8 @@ def _graph_time_us(torch, fn, reps: int, trials: int = 5) -> float:
     return statistics.median(times)
 
 
-PRODUCT_KERNELS = ("fused_fwd_kernel", "rec_linear_kernel", "rec_gemm_kernel", "mfma_fwd_kernel", "f32_fwd_kernel",
-                   "lut_fwd_kernel")
+PRODUCT_KERNELS = ("fused_fwd_kernel", "rec_conv3_kernel", "rec_linear_kernel", "rec_gemm_kernel", "mfma_fwd_kernel",
+                   "f32_fwd_kernel", "lut_fwd_kernel")
 
 
 def launch_times(torch, items, replays: int = 5, graph_reps: int = 10):
