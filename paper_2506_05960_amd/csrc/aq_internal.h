@@ -135,7 +135,7 @@ struct FusedLaunch {
 hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 // 3x3 convolution over pre-decoded operand records (fl.crec) with the four waves
 // splitting a 128 x bn tile 2 x 2 (plan.wsplit; bn 128 or 192, plan.upl staging
-// units per thread, plan.rdepth 3 or 9).
+// units per thread, plan.rdepth 3 or 6).
 hipError_t launch_rec_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 // Dense matrix-core product over pre-decoded operand records (fl.crec), tile plan.bm x plan.bn;
 // for a convolution plan.pr / plan.ps / plan.pw are the staging's image slots, rows per

@@ -673,7 +673,8 @@ bool wsplit_plan(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) {
     q.bm = 128;
     q.bn = bn;
     q.wsplit = 1;
-    q.rdepth = 3;
+    // records five steps ahead (six register sets) where the registers allow
+    q.rdepth = bn == 192 && q.upl > 1 ? 3 : 6;
     q.splitk = 1;
     q.pbuf_bytes = 2 * q.ps + 32;                // two planes and a spare slot
     q.lds_bytes = (size_t)2 * q.pbuf_bytes;

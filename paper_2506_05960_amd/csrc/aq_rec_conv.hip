@@ -68,13 +68,14 @@ __device__ __forceinline__ uint32_t halves(uint32_t xlo, int hlo, uint32_t xhi, 
 
 // TM / TN: 32-wide token / channel blocks per wave (tile 64 TM x 64 TN);
 // UPL: staging units (plane, staged row, pixel pair) per thread; D: record
-// register sets (records are loaded D - 1 steps ahead; D divides 9).
+// register sets (records are loaded D - 1 steps ahead; D divides 18, the
+// steps of the two chunks one loop iteration covers).
 template <int TM, int TN, int UPL, int D>
 __global__ void __launch_bounds__(256, 2)
 rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const float* __restrict__ scales,
                  const void* __restrict__ X, void* __restrict__ Y, int y_dtype) {
     constexpr int NS = 9;
-    static_assert(NS % D == 0, "the record ring must divide a chunk");
+    static_assert((2 * NS) % D == 0, "the record ring must divide two chunks");
     constexpr int BM = 64 * TM, BN = 64 * TN;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     asm volatile("" ::"s"(geo.tokens), "s"(geo.C_out), "s"(geo.H), "s"(geo.W), "s"(geo.cin), "s"(geo.OW),
@@ -239,7 +240,7 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
     frag(af[0], buf0, 0);
 
     // One chunk c of parity P: step s uses fragment set (s + P) & 1 (the sets
-    // alternate across chunk boundaries) and record set s % D.
+    // alternate across chunk boundaries) and record set (s + P NS) % D.
     auto body = [&](auto pc, int c) {
         constexpr int P = decltype(pc)::value;
         const uint8_t* cur = P ? buf1 : buf0;
@@ -248,18 +249,21 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            // records D - 1 steps ahead, into the set the previous step used
-            rec_load(rc[(s + D - 1) % D], c + (s + D - 1) / NS, (s + D - 1) % NS);
+            // the next step's fragments first (the step's products cover their
+            // latency), then the records D - 1 steps ahead into the set the
+            // previous step used
             if (s + 1 < NS) frag(af[(s + 1 + P) & 1], cur, s + 1);
+            rec_load(rc[(s + P * NS + D - 1) % D], c + (s + D - 1) / NS, (s + D - 1) % NS);
 #pragma unroll
             for (int b = 0; b < TN; ++b)
 #pragma unroll
-                for (int a = 0; a < TM; ++a) acc[a][b] = mfma_16(af[(s + P) & 1][a], rc[s % D][b], acc[a][b]);
+                for (int a = 0; a < TM; ++a)
+                    acc[a][b] = mfma_16(af[(s + P) & 1][a], rc[(s + P * NS) % D][b], acc[a][b]);
 #pragma unroll
             for (int i = 0; i < TN * TM; ++i) {
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // MFMA
-                if (i < TN) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);              // VMEM read
-                if (i >= TN * TM - TM && s + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+                if (i < TM && s + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                             // MFMA
+                if (i < TN) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);                // VMEM read
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -330,18 +334,24 @@ hipError_t rec_conv3_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaun
 template <int TN, int D>
 hipError_t rec_conv3_upl(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
     if (plan.upl == 1) return rec_conv3_cfg<2, TN, 1, D>(geo, plan, fl);
-    if (plan.upl == 2) return rec_conv3_cfg<2, TN, 2, D>(geo, plan, fl);
-    if (plan.upl == 3) return rec_conv3_cfg<2, TN, 3, D>(geo, plan, fl);
-    return hipErrorInvalidConfiguration;
+    if constexpr (TN == 3 && D == 6) {
+        // 192 channels with six record sets: only one staging unit per thread
+        // fits 256 registers per lane
+        return hipErrorInvalidConfiguration;
+    } else {
+        if (plan.upl == 2) return rec_conv3_cfg<2, TN, 2, D>(geo, plan, fl);
+        if (plan.upl == 3) return rec_conv3_cfg<2, TN, 3, D>(geo, plan, fl);
+        return hipErrorInvalidConfiguration;
+    }
 }
 
 }  // namespace
 
 hipError_t launch_rec_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
     if (plan.kind != 1 || plan.bm != 128 || plan.dec != FUSED_DEC_REC) return hipErrorInvalidConfiguration;
-    // 192 channels: nine record sets would not fit 256 registers per lane
-    if (plan.bn == 192) return plan.rdepth == 3 ? rec_conv3_upl<3, 3>(geo, plan, fl) : hipErrorInvalidConfiguration;
-    if (plan.bn == 128) return plan.rdepth == 9 ? rec_conv3_upl<2, 9>(geo, plan, fl) : rec_conv3_upl<2, 3>(geo, plan, fl);
+    if (plan.rdepth != 3 && plan.rdepth != 6) return hipErrorInvalidConfiguration;
+    if (plan.bn == 192) return plan.rdepth == 6 ? rec_conv3_upl<3, 6>(geo, plan, fl) : rec_conv3_upl<3, 3>(geo, plan, fl);
+    if (plan.bn == 128) return plan.rdepth == 6 ? rec_conv3_upl<2, 6>(geo, plan, fl) : rec_conv3_upl<2, 3>(geo, plan, fl);
     return hipErrorInvalidConfiguration;
 }
 
