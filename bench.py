@@ -145,7 +145,7 @@ def _graph_time_us(torch, fn, reps: int, trials: int = 5) -> float:
     return statistics.median(times)
 
 
-PRODUCT_KERNELS = ("fused_fwd_kernel", "rec_conv3_kernel", "rec_linear_kernel", "rec_gemm_kernel", "mfma_fwd_kernel",
+PRODUCT_KERNELS = ("fused_fwd_kernel", "rec_conv_kernel", "rec_linear_kernel", "rec_gemm_kernel", "mfma_fwd_kernel",
                    "f32_fwd_kernel", "lut_fwd_kernel")
 
 

@@ -109,7 +109,7 @@ struct FusedPlan {
     int64_t x_bytes;      // bytes of this forward's input X (the bound of the kernel's activation loads)
     int tile_div;         // tiles along the faster tile index (token tiles if nmajor, else channel tiles)
     float inv_tile_div;   // its fp32 reciprocal
-    int wsplit;           // 1: 3x3 convolution on the 2 x 2 wave-split records kernel (tile bm x bn)
+    int wsplit;           // 1: convolution on the 2 x 2 wave-split records kernel (tile bm x bn)
     int rdepth;           // wave-split kernel: record register sets (loads run rdepth - 1 steps ahead)
     int splitk;           // workgroups sharing one tile along K (1: no split)
     int ntiles;           // output tiles (the grid is ntiles * splitk workgroups)
@@ -133,10 +133,10 @@ struct FusedLaunch {
 };
 
 hipError_t launch_fused_forward(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
-// 3x3 convolution over pre-decoded operand records (fl.crec) with the four waves
-// splitting a 128 x bn tile 2 x 2 (plan.wsplit; bn 128 or 192, plan.upl staging
-// units per thread, plan.rdepth 3 or 6).
-hipError_t launch_rec_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
+// 3x3 or 1x1 convolution over pre-decoded operand records (fl.crec) with the
+// four waves splitting a 128 x bn tile 2 x 2 (plan.wsplit; bn 128 or 192,
+// plan.upl staging units per thread; plan.rdepth 3 or 6 for 3x3, 4 for 1x1).
+hipError_t launch_rec_conv(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl);
 // Dense matrix-core product over pre-decoded operand records (fl.crec), tile plan.bm x plan.bn;
 // for a convolution plan.pr / plan.ps / plan.pw are the staging's image slots, rows per
 // slot and padded row width.  `xpack` receives the repacked activations (convolution, int8

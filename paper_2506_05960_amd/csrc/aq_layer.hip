@@ -398,7 +398,7 @@ int fused_occupancy(const Geom& geo, const aq::FusedPlan& q, int x_dtype) {
     aq::FusedLaunch fl{};
     fl.x_dtype = x_dtype;
     fl.occupancy = &occ;
-    const hipError_t e = q.wsplit ? aq::launch_rec_conv3(geo, q, fl) : aq::launch_fused_forward(geo, q, fl);
+    const hipError_t e = q.wsplit ? aq::launch_rec_conv(geo, q, fl) : aq::launch_fused_forward(geo, q, fl);
     if (e != hipSuccess || occ < 1) {
         (void)hipGetLastError();
         occ = 1;
@@ -657,26 +657,27 @@ bool use_predecoded(const aq_layer* L, const Geom& geo) {
 
 // The route of one forward, resolved on the host (shared by the forward and
 // aq_layer_describe).
-// The 2 x 2 wave-split records kernel for a 3x3 convolution: a 128-token tile,
-// 192 channels where C_out is a multiple of 192 (else 128), and its staging.
-// False where the kernel does not apply (tile rows, image planes not a
-// multiple of 4 tokens, more than 768 staging units).
+// The 2 x 2 wave-split records kernel for a 3x3 or 1x1 convolution: a
+// 128-token tile, 192 channels where C_out is a multiple of 192 (else 128),
+// and its staging.  False where the kernel does not apply (tile rows, image
+// planes not a multiple of 4 tokens, more staging units than instantiated).
 bool wsplit_plan(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) {
-    if (p->kind != 1 || p->dec != aq::FUSED_DEC_REC) return false;
+    if (p->dec != aq::FUSED_DEC_REC || !(p->kind == 1 || (p->kind == 2 && p->cm == 4))) return false;
     if ((geo.OH * geo.OW) % 4 != 0 || geo.W % 2 != 0) return false;
     aq::FusedPlan q = *p;
-    if (!conv_staging(geo, opt, 1, 1, 128, false, &q)) return false;
+    if (!conv_staging(geo, opt, p->kind, p->cm, 128, false, &q)) return false;
     q.upl = (q.units + 255) / 256;
-    if (q.upl > 3) return false;
+    if (p->kind == 1 ? q.upl > 3 : q.upl != 2) return false;
     int bn = geo.C_out % 192 == 0 ? 192 : 128;
     if (opt.fused_bm == 128 && (opt.fused_bn == 128 || opt.fused_bn == 192)) bn = opt.fused_bn;
     q.bm = 128;
     q.bn = bn;
     q.wsplit = 1;
-    // records five steps ahead (six register sets) where the registers allow
-    q.rdepth = bn == 192 && q.upl > 1 ? 3 : 6;
+    // 3x3: records five steps ahead (six register sets) where the registers
+    // allow; 1x1: three steps ahead
+    q.rdepth = p->kind == 2 ? 4 : bn == 192 && q.upl > 1 ? 3 : 6;
     q.splitk = 1;
-    q.pbuf_bytes = 2 * q.ps + 32;                // two planes and a spare slot
+    q.pbuf_bytes = 2 * p->cm * q.ps + 32;        // the chunk's planes and a spare slot
     q.lds_bytes = (size_t)2 * q.pbuf_bytes;
     if (q.lds_bytes > kLdsBytes) return false;
     const int64_t nt = ((geo.tokens + 127) / 128) * (int64_t)((geo.C_out + bn - 1) / bn);
@@ -730,16 +731,28 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
         r.fp = gp;
         return r;
     }
-    // Pre-decoded 3x3 convolutions: the wave-split records kernel where its
-    // 128-token tiles number at least 192 (measured on the U-Net shapes: 20-25 %
-    // faster than the fused kernel's best tile at 32768 tokens, 256-512 tiles;
-    // slower with 128 tiles or fewer, which leave compute units idle).
-    // AQ_OPT_RECORD_PRODUCT = 3 forces it where it applies, 1 and 2 exclude it.
+    // Convolutions on the wave-split records kernel, where its 128-token tiles
+    // fill the chip (measured on the U-Net shapes):
+    //  * 3x3 with pre-decoded operands and at least 192 tiles: 20-25 % faster
+    //    than the fused kernel's best tile at 32768 tokens (256-512 tiles),
+    //    slower with 128 tiles or fewer, which leave compute units idle;
+    //  * 1x1 with at least 256 tiles (128 for M >= 4), records decoded for it
+    //    even where the in-loop decode was chosen: 24.0 -> 17.6 us at 32768
+    //    tokens x 384 -> 192 channels, M = 2 (records included); with fewer
+    //    tiles the fused kernel's in-loop decode stays ahead for M = 2.
+    // AQ_OPT_RECORD_PRODUCT = 3 forces it where it applies, 1 and 2 exclude it;
+    // AQ_OPT_WEIGHTS = 1 keeps a 1x1 layer on the in-loop decode.
     bool planned = false;
-    if (L->fused_ok && fits31 && opt.generic != 1 && fp.dec == aq::FUSED_DEC_REC && fp.kind == 1 &&
+    const bool ws_1x1 = fp.kind == 2 && fp.dec != aq::FUSED_DEC_REC && opt.weights == 0;
+    if (L->fused_ok && fits31 && opt.generic != 1 && fp.kind != 0 && (fp.dec == aq::FUSED_DEC_REC || ws_1x1) &&
         (opt.rec_product == 3 || opt.rec_product == 0)) {
         aq::FusedPlan wp = fp;
-        if (wsplit_plan(geo, opt, &wp) && (opt.rec_product == 3 || wp.ntiles >= 192)) {
+        wp.dec = aq::FUSED_DEC_REC;
+        wp.mc = 1;
+        wp.cb_bytes = 0;
+        const bool ok = wsplit_plan(geo, opt, &wp);
+        const bool take = fp.kind == 1 ? wp.ntiles >= 192 : wp.ntiles * (geo.M >= 4 ? 2 : 1) >= 256;
+        if (ok && (ws_1x1 ? opt.rec_product == 0 && take : opt.rec_product == 3 || take)) {
             fp = wp;
             planned = true;
         }
@@ -831,7 +844,7 @@ aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X,
         const aq::FusedLaunch fl{cbsrc, recs, L->d_scales, X, xs, Y, d.y_dtype, d.x_dtype, st, wk.part, wk.arrivals};
         if (e == hipSuccess)
             e = r.kind == Route::REC_LINEAR ? aq::launch_rec_linear(geo, fp, fl)
-                : fp.wsplit                  ? aq::launch_rec_conv3(geo, fp, fl)
+                : fp.wsplit                  ? aq::launch_rec_conv(geo, fp, fl)
                                              : aq::launch_fused_forward(geo, fp, fl);
         break;
     }

@@ -1,6 +1,6 @@
-// Matrix-core product of a 3x3 convolution over its pre-decoded operand
-// records, gfx950 (Y = conv(X, W) with W decoded once per forward, Sec. 2.4
-// eq. (4); the convolution as an implicit im2col product, K ordered
+// Matrix-core product of a 3x3 or 1x1 convolution over its pre-decoded
+// operand records, gfx950 (Y = conv(X, W) with W decoded once per forward,
+// Sec. 2.4 eq. (4); the convolution as an implicit im2col product, K ordered
 // (input channel, kernel row, kernel column)).
 //
 // Work split.  A workgroup owns a BM (tokens) x BN (output channels) tile and
@@ -13,17 +13,18 @@
 // epilogue are paid once per tile, and the input rows are staged once per
 // workgroup for both token halves' four waves.
 //
-// Operands, per chunk of 16 input channels (9 matrix-core steps, one per
-// kernel position (kh, kw)):
+// Operands, per chunk (3x3: 16 input channels, 9 matrix-core steps, one per
+// kernel position (kh, kw); 1x1: 64 input channels, 4 steps of 16):
 //  * Activations (A operand, rows = tokens): the input rows the token tile
-//    touches, 16 channels as two planes of 8, are loaded two pixels of one
-//    channel per 32-bit load, transposed with byte permutes to 16 bytes per
-//    pixel (8 channels) and stored to one of two LDS buffers, whose zero
-//    padding columns are written once.  A lane's 8 operand values for step
-//    (kh, kw) are one 16-byte LDS read at its output pixel's input position.
+//    touches, the chunk's channels as planes of 8, are loaded two pixels of
+//    one channel per 32-bit load, transposed with byte permutes to 16 bytes
+//    per pixel (8 channels) and stored to one of two LDS buffers, whose zero
+//    padding columns are written once.  A lane's 8 operand values for a step
+//    are one 16-byte LDS read at its output pixel's input position.
 //  * Weights (B operand, columns = output channels): record (chunk, step,
-//    channel, lane half) holds the lane's 8 fp16 weights (channels 8 half +
-//    0..7 of the chunk at kernel position step).  They are read straight into
+//    channel, lane half) holds the lane's 8 fp16 weights (3x3: channels
+//    8 half + 0..7 of the chunk at kernel position step; 1x1: channels
+//    16 step + 8 half + 0..7).  They are read straight into
 //    registers, D - 1 steps ahead of their products, through a ring of D
 //    register sets; the two waves of a channel half read the same records,
 //    the second read hitting the L1 cache.
@@ -66,15 +67,16 @@ __device__ __forceinline__ uint32_t halves(uint32_t xlo, int hlo, uint32_t xhi, 
     return __builtin_amdgcn_perm(xhi, xlo, sel);
 }
 
-// TM / TN: 32-wide token / channel blocks per wave (tile 64 TM x 64 TN);
-// UPL: staging units (plane, staged row, pixel pair) per thread; D: record
-// register sets (records are loaded D - 1 steps ahead; D divides 18, the
-// steps of the two chunks one loop iteration covers).
-template <int TM, int TN, int UPL, int D>
+// KIND: 1 for 3x3, 2 for 1x1; TM / TN: 32-wide token / channel blocks per
+// wave (tile 64 TM x 64 TN); UPL: staging units (plane, staged row, pixel
+// pair) per thread; D: record register sets (records are loaded D - 1 steps
+// ahead; D divides the steps of the two chunks one loop iteration covers).
+template <int KIND, int TM, int TN, int UPL, int D>
 __global__ void __launch_bounds__(256, 2)
-rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const float* __restrict__ scales,
-                 const void* __restrict__ X, void* __restrict__ Y, int y_dtype) {
-    constexpr int NS = 9;
+rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const float* __restrict__ scales,
+                const void* __restrict__ X, void* __restrict__ Y, int y_dtype) {
+    constexpr int NS = KIND == 1 ? 9 : 4;           // steps per chunk
+    constexpr int CM = KIND == 1 ? 1 : 4;           // 16-channel slices per chunk (2 CM planes of 8)
     static_assert((2 * NS) % D == 0, "the record ring must divide two chunks");
     constexpr int BM = 64 * TM, BN = 64 * TN;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -145,7 +147,7 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
         const bool cv = c < plan.nchunk;
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
-            const uint32_t base = g_ok[j] & cv ? (g_off[j] + (uint32_t)(c * 16) * (uint32_t)HW) * 2u : kOutOfRange;
+            const uint32_t base = g_ok[j] & cv ? (g_off[j] + (uint32_t)(c * 16 * CM) * (uint32_t)HW) * 2u : kOutOfRange;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 stg[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, 0);
@@ -180,7 +182,9 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
         a_base[a] = (uint32_t)(q * plan.ps + (__umul24(R0, plan.pw) + __umul24(ow, geo.stride)) * 16);
     }
     auto frag = [&](u32x4 (&dst)[TM], const uint8_t* buf, int s) {
-        const uint32_t soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);
+        uint32_t soff;
+        if constexpr (KIND == 1) soff = (uint32_t)(((s / 3) * plan.pw + (s % 3)) * 16);   // kernel position
+        else soff = (uint32_t)(2 * s * plan.ps);                                           // planes 2 s, 2 s + 1
 #pragma unroll
         for (int a = 0; a < TM; ++a) dst[a] = *reinterpret_cast<const u32x4*>(buf + a_base[a] + soff);
     };
@@ -224,7 +228,7 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
     {
         // zero padding columns of both buffers: (buffer, plane, staged row, pad column)
         const int padc = plan.pw - geo.W;
-        const int nrow = 2 * 2 * plan.pr;
+        const int nrow = 2 * 2 * CM * plan.pr;
         for (int i = tid; i < nrow * padc; i += 256) {
             const int row = i / padc, pcx = i - row * padc;
             const int bsel = row & 1, rest = row >> 1;
@@ -239,8 +243,9 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
     u32x4 af[2][TM];
     frag(af[0], buf0, 0);
 
-    // One chunk c of parity P: step s uses fragment set (s + P) & 1 (the sets
-    // alternate across chunk boundaries) and record set (s + P NS) % D.
+    // One chunk c of parity P: step s uses fragment set (s + P NS) & 1 (the
+    // sets alternate across chunk boundaries for odd NS too) and record set
+    // (s + P NS) % D.
     auto body = [&](auto pc, int c) {
         constexpr int P = decltype(pc)::value;
         const uint8_t* cur = P ? buf1 : buf0;
@@ -252,13 +257,13 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
             // the next step's fragments first (the step's products cover their
             // latency), then the records D - 1 steps ahead into the set the
             // previous step used
-            if (s + 1 < NS) frag(af[(s + 1 + P) & 1], cur, s + 1);
+            if (s + 1 < NS) frag(af[(s + 1 + P * NS) & 1], cur, s + 1);
             rec_load(rc[(s + P * NS + D - 1) % D], c + (s + D - 1) / NS, (s + D - 1) % NS);
 #pragma unroll
             for (int b = 0; b < TN; ++b)
 #pragma unroll
                 for (int a = 0; a < TM; ++a)
-                    acc[a][b] = mfma_16(af[(s + P) & 1][a], rc[(s + P * NS) % D][b], acc[a][b]);
+                    acc[a][b] = mfma_16(af[(s + P * NS) & 1][a], rc[(s + P * NS) % D][b], acc[a][b]);
 #pragma unroll
             for (int i = 0; i < TN * TM; ++i) {
                 if (i < TM && s + 1 < NS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
@@ -271,7 +276,7 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
         // were issued before the previous barrier), then its first fragments
         stage_store(nxt);
         lds_barrier();
-        frag(af[(NS + P) & 1], nxt, 0);
+        frag(af[(NS + P * NS) & 1], nxt, 0);
     };
     int c = 0;
     for (; c + 1 < plan.nchunk; c += 2) {
@@ -319,40 +324,46 @@ rec_conv3_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, cons
         }
 }
 
-template <int TM, int TN, int UPL, int D>
-hipError_t rec_conv3_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
-    auto kern = rec_conv3_kernel<TM, TN, UPL, D>;
+template <int KIND, int TM, int TN, int UPL, int D>
+hipError_t rec_conv_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
+    auto kern = rec_conv_kernel<KIND, TM, TN, UPL, D>;
     hipError_t e = ensure_dynamic_lds((const void*)kern, plan.lds_bytes);
     if (e != hipSuccess) return e;
     if (fl.occupancy) return hipOccupancyMaxActiveBlocksPerMultiprocessor(fl.occupancy, kern, 256, plan.lds_bytes);
     const dim3 grid((unsigned)plan.ntiles);
     kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.crec, fl.scales, fl.X, fl.Y, fl.y_dtype);
-    note_launch(fl.stream, "rec_conv3_kernel", {TM, TN, UPL, D});
+    note_launch(fl.stream, "rec_conv_kernel", {KIND, TM, TN, UPL, D});
     return hipGetLastError();
 }
 
 template <int TN, int D>
 hipError_t rec_conv3_upl(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
-    if (plan.upl == 1) return rec_conv3_cfg<2, TN, 1, D>(geo, plan, fl);
+    if (plan.upl == 1) return rec_conv_cfg<1, 2, TN, 1, D>(geo, plan, fl);
     if constexpr (TN == 3 && D == 6) {
         // 192 channels with six record sets: only one staging unit per thread
         // fits 256 registers per lane
         return hipErrorInvalidConfiguration;
     } else {
-        if (plan.upl == 2) return rec_conv3_cfg<2, TN, 2, D>(geo, plan, fl);
-        if (plan.upl == 3) return rec_conv3_cfg<2, TN, 3, D>(geo, plan, fl);
+        if (plan.upl == 2) return rec_conv_cfg<1, 2, TN, 2, D>(geo, plan, fl);
+        if (plan.upl == 3) return rec_conv_cfg<1, 2, TN, 3, D>(geo, plan, fl);
         return hipErrorInvalidConfiguration;
     }
 }
 
 }  // namespace
 
-hipError_t launch_rec_conv3(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
-    if (plan.kind != 1 || plan.bm != 128 || plan.dec != FUSED_DEC_REC) return hipErrorInvalidConfiguration;
-    if (plan.rdepth != 3 && plan.rdepth != 6) return hipErrorInvalidConfiguration;
+hipError_t launch_rec_conv(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
+    if (plan.bm != 128 || plan.dec != FUSED_DEC_REC || (plan.bn != 128 && plan.bn != 192))
+        return hipErrorInvalidConfiguration;
+    if (plan.kind == 2) {
+        // 1x1: 128 tokens stage 8 planes x 128 pixels, two units per thread;
+        // records three steps ahead (four sets)
+        if (plan.upl != 2 || plan.rdepth != 4) return hipErrorInvalidConfiguration;
+        return plan.bn == 192 ? rec_conv_cfg<2, 2, 3, 2, 4>(geo, plan, fl) : rec_conv_cfg<2, 2, 2, 2, 4>(geo, plan, fl);
+    }
+    if (plan.kind != 1 || (plan.rdepth != 3 && plan.rdepth != 6)) return hipErrorInvalidConfiguration;
     if (plan.bn == 192) return plan.rdepth == 6 ? rec_conv3_upl<3, 6>(geo, plan, fl) : rec_conv3_upl<3, 3>(geo, plan, fl);
-    if (plan.bn == 128) return plan.rdepth == 6 ? rec_conv3_upl<2, 6>(geo, plan, fl) : rec_conv3_upl<2, 3>(geo, plan, fl);
-    return hipErrorInvalidConfiguration;
+    return plan.rdepth == 6 ? rec_conv3_upl<2, 6>(geo, plan, fl) : rec_conv3_upl<2, 3>(geo, plan, fl);
 }
 
 }  // namespace aq

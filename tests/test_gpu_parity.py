@@ -317,11 +317,11 @@ def test_predecoded_operands_match_in_loop_decode(spec):
     assert err <= 2e-3 and err_g <= 2e-3
 
 
-# The wave-split records kernel for 3x3 convolutions (128-token tiles, four
-# waves splitting the tile 2 x 2): tile rows of 1 to 16 output rows, whole
-# images per tile, partial last tiles, stride 2, ragged channel tiles
-# (C_out not a multiple of the 128 / 192 tile), M = 1, 4 and g = 9 records,
-# fp32 outputs.
+# The wave-split records kernel for 3x3 and 1x1 convolutions (128-token tiles,
+# four waves splitting the tile 2 x 2): tile rows of 1 to 16 output rows, whole
+# images per tile, partial last tiles, stride 2, ragged channel tiles (C_out
+# not a multiple of the 128 / 192 tile), M = 1, 4 and g = 9 records, fp32
+# outputs.
 WSPLIT = [
     LayerSpec(name="ws_c192_16x16", C_out=192, K=64 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(64, 3, 3, 1, 1, 16, 16)),
     LayerSpec(name="ws_c100_8x32", C_out=100, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 8, 32)),
@@ -332,6 +332,12 @@ WSPLIT = [
     LayerSpec(name="ws_f32out_w256", C_out=128, K=16 * 9, g=8, M=2, B=8, n=1, y_dtype="f32",
               conv=ConvGeom(16, 3, 3, 1, 1, 4, 256)),
     LayerSpec(name="ws_long_k", C_out=192, K=320 * 9, g=8, M=2, B=8, n=1, conv=ConvGeom(320, 3, 3, 1, 1, 16, 16)),
+    # 1x1: 64-channel chunks (odd and even counts), ragged channel tiles, whole-image tiles
+    LayerSpec(name="ws1_c192_32x32", C_out=192, K=64, g=8, M=2, B=8, n=2, conv=ConvGeom(64, 1, 1, 1, 0, 32, 32)),
+    LayerSpec(name="ws1_c100_16x16", C_out=100, K=192, g=8, M=4, B=8, n=3, conv=ConvGeom(192, 1, 1, 1, 0, 16, 16)),
+    LayerSpec(name="ws1_k576_64x64", C_out=192, K=576, g=8, M=2, B=8, n=1, conv=ConvGeom(576, 1, 1, 1, 0, 64, 64)),
+    LayerSpec(name="ws1_8x8_imgs", C_out=128, K=128, g=8, M=2, B=8, n=5, y_dtype="f32",
+              conv=ConvGeom(128, 1, 1, 1, 0, 8, 8)),
 ]
 
 
