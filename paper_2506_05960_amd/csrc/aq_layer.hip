@@ -657,30 +657,38 @@ bool use_predecoded(const aq_layer* L, const Geom& geo) {
 
 // The route of one forward, resolved on the host (shared by the forward and
 // aq_layer_describe).
-// The 2 x 2 wave-split records kernel for a 3x3 or 1x1 convolution: a
-// 128-token tile, 192 channels where C_out is a multiple of 192 (else 128),
-// and its staging.  False where the kernel does not apply (tile rows, image
-// planes not a multiple of 4 tokens, more staging units than instantiated).
-bool wsplit_plan(const Geom& geo, const aq::Options& opt, aq::FusedPlan* p) {
+// The 2 x 2 wave-split records kernel for a 3x3 or 1x1 convolution, `wk`
+// waves per reduction: a 128-token tile (wk = 1) or a 64-token tile whose
+// two channel halves each take every other chunk in two waves (wk = 2); 192
+// channels where C_out is a multiple of 192 (else 128); and its staging.
+// AQ_OPT_FUSED_TILE picks 128 or 192 channels when its token count matches.
+// False where the kernel does not apply (tile rows, image planes not a
+// multiple of 4 tokens, more staging units than instantiated).
+bool wsplit_plan(const Geom& geo, const aq::Options& opt, int wk, aq::FusedPlan* p) {
     if (p->dec != aq::FUSED_DEC_REC || !(p->kind == 1 || (p->kind == 2 && p->cm == 4))) return false;
     if ((geo.OH * geo.OW) % 4 != 0 || geo.W % 2 != 0) return false;
+    const int bm = wk == 1 ? 128 : 64;
     aq::FusedPlan q = *p;
-    if (!conv_staging(geo, opt, p->kind, p->cm, 128, false, &q)) return false;
-    q.upl = (q.units + 255) / 256;
+    if (!conv_staging(geo, opt, p->kind, p->cm, bm, false, &q)) return false;
+    q.upl = (wk * q.units + 255) / 256;
     if (p->kind == 1 ? q.upl > 3 : q.upl != 2) return false;
     int bn = geo.C_out % 192 == 0 ? 192 : 128;
-    if (opt.fused_bm == 128 && (opt.fused_bn == 128 || opt.fused_bn == 192)) bn = opt.fused_bn;
-    q.bm = 128;
+    if (opt.fused_bm == bm && (opt.fused_bn == 128 || opt.fused_bn == 192)) bn = opt.fused_bn;
+    if (p->kind == 1 && wk == 2 && bn == 192 && q.upl > 2) bn = 128;   // registers (see the launcher)
+    q.bm = bm;
     q.bn = bn;
     q.wsplit = 1;
     // 3x3: records five steps ahead (six register sets) where the registers
-    // allow; 1x1: three steps ahead
-    q.rdepth = p->kind == 2 ? 4 : bn == 192 && q.upl > 1 ? 3 : 6;
+    // allow (not with the two-wave reduction); 1x1: three steps ahead
+    q.rdepth = p->kind == 2 ? 4 : wk == 2 || (bn == 192 && q.upl > 1) ? 3 : 6;
     q.splitk = 1;
     q.pbuf_bytes = 2 * p->cm * q.ps + 32;        // the chunk's planes and a spare slot
-    q.lds_bytes = (size_t)2 * q.pbuf_bytes;
+    // staging: two buffers per chunk of an iteration; wk = 2: then the partial
+    // tiles of the second reduction half (4 KB per 32 x 32 block)
+    const size_t red = wk == 2 ? (size_t)2 * 2 * (bn / 64) * 4 * 64 * 16 : 0;
+    q.lds_bytes = std::max((size_t)2 * wk * q.pbuf_bytes, red);
     if (q.lds_bytes > kLdsBytes) return false;
-    const int64_t nt = ((geo.tokens + 127) / 128) * (int64_t)((geo.C_out + bn - 1) / bn);
+    const int64_t nt = ((geo.tokens + bm - 1) / bm) * (int64_t)((geo.C_out + bn - 1) / bn);
     if (nt >= (int64_t(1) << 24)) return false;
     q.ntiles = (int)nt;
     q.inv_ntiles = 1.0f / (float)nt;
@@ -731,29 +739,42 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
         r.fp = gp;
         return r;
     }
-    // Convolutions on the wave-split records kernel, where its 128-token tiles
-    // fill the chip (measured on the U-Net shapes):
-    //  * 3x3 with pre-decoded operands and at least 192 tiles: 20-25 % faster
-    //    than the fused kernel's best tile at 32768 tokens (256-512 tiles),
-    //    slower with 128 tiles or fewer, which leave compute units idle;
-    //  * 1x1 with at least 256 tiles (128 for M >= 4), records decoded for it
-    //    even where the in-loop decode was chosen: 24.0 -> 17.6 us at 32768
-    //    tokens x 384 -> 192 channels, M = 2 (records included); with fewer
-    //    tiles the fused kernel's in-loop decode stays ahead for M = 2.
-    // AQ_OPT_RECORD_PRODUCT = 3 forces it where it applies, 1 and 2 exclude it;
-    // AQ_OPT_WEIGHTS = 1 keeps a 1x1 layer on the in-loop decode.
+    // Convolutions on the wave-split records kernel where its tiles fill the
+    // chip (measured on the U-Net shapes, records included):
+    //  * 128-token tiles (one wave per reduction) for 3x3 layers with at least
+    //    192 of them (20-25 % faster than the fused kernel's best tile at 32768
+    //    tokens) and 1x1 layers with at least 256 (24.0 -> 17.6 us at 32768
+    //    tokens x 384 -> 192 channels, M = 2);
+    //  * else 64-token tiles with two waves per reduction where there are at
+    //    least 256 of them and every wave keeps 4 chunks or more (8192 tokens
+    //    x 384 channels: 3-8 % faster than the fused kernel, 3x3 and 1x1);
+    //  * else, for 1x1 layers with M >= 4, 128-token tiles from 128 of them
+    //    (the in-loop decode gathers 4 codewords per group).
+    // Fewer tiles leave compute units idle: the fused kernel stays ahead.  1x1
+    // layers switch to records for it even where the in-loop decode was
+    // chosen.  AQ_OPT_RECORD_PRODUCT = 3 forces the kernel where it applies
+    // (a forced 64-token AQ_OPT_FUSED_TILE selects the two-wave reduction), 1
+    // and 2 exclude it; AQ_OPT_WEIGHTS = 1 keeps a 1x1 layer on the in-loop decode.
     bool planned = false;
     const bool ws_1x1 = fp.kind == 2 && fp.dec != aq::FUSED_DEC_REC && opt.weights == 0;
     if (L->fused_ok && fits31 && opt.generic != 1 && fp.kind != 0 && (fp.dec == aq::FUSED_DEC_REC || ws_1x1) &&
         (opt.rec_product == 3 || opt.rec_product == 0)) {
-        aq::FusedPlan wp = fp;
-        wp.dec = aq::FUSED_DEC_REC;
-        wp.mc = 1;
-        wp.cb_bytes = 0;
-        const bool ok = wsplit_plan(geo, opt, &wp);
-        const bool take = fp.kind == 1 ? wp.ntiles >= 192 : wp.ntiles * (geo.M >= 4 ? 2 : 1) >= 256;
-        if (ok && (ws_1x1 ? opt.rec_product == 0 && take : opt.rec_product == 3 || take)) {
-            fp = wp;
+        aq::FusedPlan rp = fp;
+        rp.dec = aq::FUSED_DEC_REC;
+        rp.mc = 1;
+        rp.cb_bytes = 0;
+        aq::FusedPlan w1 = rp, w2 = rp;
+        const bool ok1 = wsplit_plan(geo, opt, 1, &w1), ok2 = wsplit_plan(geo, opt, 2, &w2);
+        const aq::FusedPlan* pick = nullptr;
+        if (opt.rec_product == 3 && !ws_1x1) {
+            if (opt.fused_bm == 64 ? ok2 : ok1) pick = opt.fused_bm == 64 ? &w2 : &w1;
+        } else if (opt.rec_product == 0) {
+            if (ok1 && w1.ntiles >= (fp.kind == 1 ? 192 : 256)) pick = &w1;
+            else if (ok2 && w2.ntiles >= 256 && fp.nchunk >= 8) pick = &w2;
+            else if (ok1 && fp.kind == 2 && geo.M >= 4 && w1.ntiles >= 128) pick = &w1;
+        }
+        if (pick) {
+            fp = *pick;
             planned = true;
         }
     }

@@ -5,7 +5,10 @@
 //
 // Work split.  A workgroup owns a BM (tokens) x BN (output channels) tile and
 // its four waves split it 2 x 2: wave w covers token half (w & 1) and channel
-// half (w >> 1) over the whole reduction dimension.  The fused decode kernel
+// half (w >> 1) over the whole reduction dimension (WK = 1), or, for layers
+// with too few such tiles to fill the chip, channel half (w & 1) of a tile
+// half as tall over every other chunk (WK = 2; the two partial tiles are
+// summed in LDS at the end, in a fixed order).  The fused decode kernel
 // splits K between its waves instead (so that each wave decodes its own
 // weights), which leaves each wave a quarter of the reduction and makes the
 // workgroup reduce four partial tiles at the end; with the weights already
@@ -67,18 +70,20 @@ __device__ __forceinline__ uint32_t halves(uint32_t xlo, int hlo, uint32_t xhi, 
     return __builtin_amdgcn_perm(xhi, xlo, sel);
 }
 
-// KIND: 1 for 3x3, 2 for 1x1; TM / TN: 32-wide token / channel blocks per
-// wave (tile 64 TM x 64 TN); UPL: staging units (plane, staged row, pixel
+// KIND: 1 for 3x3, 2 for 1x1; WK: waves sharing the reduction (1 or 2);
+// TM / TN: 32-wide token / channel blocks per wave (tile 32 TM (3 - WK) x
+// 64 TN); UPL: staging units (chunk of the iteration, plane, staged row, pixel
 // pair) per thread; D: record register sets (records are loaded D - 1 steps
-// ahead; D divides the steps of the two chunks one loop iteration covers).
-template <int KIND, int TM, int TN, int UPL, int D>
+// ahead; D divides the steps of the two iterations the loop body covers).
+template <int KIND, int WK, int TM, int TN, int UPL, int D>
 __global__ void __launch_bounds__(256, 2)
 rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const float* __restrict__ scales,
                 const void* __restrict__ X, void* __restrict__ Y, int y_dtype) {
     constexpr int NS = KIND == 1 ? 9 : 4;           // steps per chunk
     constexpr int CM = KIND == 1 ? 1 : 4;           // 16-channel slices per chunk (2 CM planes of 8)
     static_assert((2 * NS) % D == 0, "the record ring must divide two chunks");
-    constexpr int BM = 64 * TM, BN = 64 * TN;
+    static_assert(WK == 1 || WK == 2, "one or two waves per reduction");
+    constexpr int BM = 32 * TM * (3 - WK), BN = 64 * TN;
     extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
     asm volatile("" ::"s"(geo.tokens), "s"(geo.C_out), "s"(geo.H), "s"(geo.W), "s"(geo.cin), "s"(geo.OW),
                  "s"(geo.OH), "s"(geo.stride), "s"(geo.pad));
@@ -105,23 +110,28 @@ rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const
         tile_m = plan.nmajor ? lo : hi;
     }
     const int T0 = tile_m * BM, N0 = tile_n * BN;
-    const int WT = (wave & 1) * 32 * TM;   // the wave's token offset in the tile
-    const int WN = (wave >> 1) * 32 * TN;  // the wave's channel offset in the tile
+    const int WT = WK == 1 ? (wave & 1) * 32 * TM : 0;          // the wave's token offset in the tile
+    const int WN = (WK == 1 ? wave >> 1 : wave & 1) * 32 * TN;  // the wave's channel offset in the tile
+    const int wk = WK == 1 ? 0 : wave >> 1;                      // the wave's chunks: wk, wk + WK, ...
     const int tokens = (int)geo.tokens;
     const int HW = geo.H * geo.W;
-    uint8_t* buf0 = lds;
-    uint8_t* buf1 = lds + plan.pbuf_bytes;
+    // staging buffer (chunk g of an iteration, parity p) at lds + (2 g + p) pbuf_bytes
 
-    // ---- staging units of this thread: unit u = tid + 256 j is (plane o, staged row, pixel pair) ----
+    // ---- staging units of this thread: unit tid + 256 j is (chunk g of the
+    // iteration, plane o, staged row, pixel pair) ----
     const int gr0 = qdiv_rc(T0, geo.OW, plan.inv_ow);   // first output row of the tile
-    uint32_t g_off[UPL];   // element offset of the unit's first value for chunk 0
-    uint32_t l_off[UPL];   // byte offset of the unit's destination in a staging buffer
+    uint32_t g_off[UPL];   // element offset of the unit's first value for iteration 0
+    uint32_t l_off[UPL];   // byte offset of the unit's destination from its parity's buffer of chunk 0
+    int u_chunk[UPL];      // the unit's chunk within an iteration
     bool g_ok[UPL];
     {
         const int wp = geo.W >> 1;
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
-            const int u = tid + 256 * j;
+            const int uu = tid + 256 * j;
+            const int g = WK == 2 && uu >= plan.units ? 1 : 0;
+            const int u = uu - g * plan.units;
+            u_chunk[j] = g;
             const int t = qdiv_rc(u, wp, plan.inv_wp);
             const int pp = u - __umul24(t, wp);
             const int o = qdiv_rc(t, plan.pr, plan.inv_pr);
@@ -134,26 +144,30 @@ rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const
             const int ih = __umul24(oh, geo.stride) - geo.pad + jr;
             const bool l_ok = u < plan.units;
             g_ok[j] = l_ok & (gr < plan.total_rows) & (ih >= 0) & (ih < geo.H);
-            g_off[j] = g_ok[j] ? (uint32_t)(__umul24(__umul24(b, geo.cin) + 8 * o, geo.H) + ih) * (uint32_t)geo.W + 2u * pp
+            g_off[j] = g_ok[j] ? (uint32_t)(__umul24(__umul24(b, geo.cin) + 8 * o + 16 * CM * g, geo.H) + ih) *
+                                         (uint32_t)geo.W +
+                                     2u * pp
                                : 0u;
-            l_off[j] = l_ok ? (uint32_t)(__umul24(o, plan.ps) + (__umul24(pr, plan.pw) + 2 * pp + geo.pad) * 16)
+            l_off[j] = l_ok ? (uint32_t)(2 * g * plan.pbuf_bytes + __umul24(o, plan.ps) +
+                                         (__umul24(pr, plan.pw) + 2 * pp + geo.pad) * 16)
                             : (uint32_t)(plan.pbuf_bytes - 32);   // a spare slot
         }
     }
     const __amdgpu_buffer_rsrc_t xr = buffer_rsrc(X, (uint64_t)plan.x_bytes);
     uint32_t stg[UPL][8];
-    // 8 channels x 2 pixels per unit; chunks past the last read zeros
-    auto stage_load = [&](int c) {
-        const bool cv = c < plan.nchunk;
+    // 8 channels x 2 pixels per unit of iteration it; chunks past the last read zeros
+    auto stage_load = [&](int it) {
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
-            const uint32_t base = g_ok[j] & cv ? (g_off[j] + (uint32_t)(c * 16 * CM) * (uint32_t)HW) * 2u : kOutOfRange;
+            const bool cv = WK * it + u_chunk[j] < plan.nchunk;
+            const uint32_t base =
+                g_ok[j] & cv ? (g_off[j] + (uint32_t)(WK * it * 16 * CM) * (uint32_t)HW) * 2u : kOutOfRange;
 #pragma unroll
             for (int e = 0; e < 8; ++e)
                 stg[j][e] = __builtin_amdgcn_raw_buffer_load_b32(xr, base + (uint32_t)(e * HW * 2), 0, 0);
         }
     };
-    auto stage_store = [&](uint8_t* buf) {
+    auto stage_store = [&](uint8_t* buf) {   // buf: the parity's buffer of chunk 0
 #pragma unroll
         for (int j = 0; j < UPL; ++j) {
             u32x4 p0, p1;   // pixel 0 / pixel 1, channels 0..7
@@ -179,7 +193,8 @@ rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const
         // output row r: block r / rpb, whose row (r % rpb) * stride is kernel row 0
         const int blk = qdiv_rc(r, plan.rpb, plan.inv_rpb), rr = r - __umul24(blk, plan.rpb);
         const int R0 = __umul24(blk, plan.sr) + __umul24(rr, geo.stride);
-        a_base[a] = (uint32_t)(q * plan.ps + (__umul24(R0, plan.pw) + __umul24(ow, geo.stride)) * 16);
+        a_base[a] = (uint32_t)(2 * wk * plan.pbuf_bytes + q * plan.ps +
+                               (__umul24(R0, plan.pw) + __umul24(ow, geo.stride)) * 16);
     }
     auto frag = [&](u32x4 (&dst)[TM], const uint8_t* buf, int s) {
         uint32_t soff;
@@ -201,7 +216,9 @@ rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const
         roff[b] = (uint32_t)((n * 2 + q) * 16);
     }
     u32x4 rc[D][TN];
-    auto rec_load = [&](u32x4 (&dst)[TN], int c, int s) {
+    // records of step s of this wave's chunk of iteration it
+    auto rec_load = [&](u32x4 (&dst)[TN], int it, int s) {
+        const int c = WK * it + wk;
         const bool cv = c < plan.nchunk;
 #pragma unroll
         for (int b = 0; b < TN; ++b)
@@ -220,32 +237,34 @@ rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const
             asm volatile("" : "=a"(acc[a][b]) : "0"(z));   // accumulators live in AGPRs
         }
 
-    // ---- prologue: chunk 0 staged, the first D - 1 steps' records in flight ----
+    // ---- prologue: iteration 0 staged, the first D - 1 steps' records in flight ----
     stage_load(0);
 #pragma unroll
     for (int i = 0; i < D - 1; ++i) rec_load(rc[i], 0, i);
     __builtin_amdgcn_sched_barrier(0);
     {
-        // zero padding columns of both buffers: (buffer, plane, staged row, pad column)
+        // zero padding columns of every buffer: (buffer, plane, staged row, pad column)
         const int padc = plan.pw - geo.W;
-        const int nrow = 2 * 2 * CM * plan.pr;
+        const int nrow = 2 * WK * 2 * CM * plan.pr;
         for (int i = tid; i < nrow * padc; i += 256) {
             const int row = i / padc, pcx = i - row * padc;
-            const int bsel = row & 1, rest = row >> 1;
+            const int bsel = row % (2 * WK), rest = row / (2 * WK);
             const int o = rest / plan.pr, pr = rest - o * plan.pr;
             const int pcol = pcx < geo.pad ? pcx : geo.W + pcx;
-            uint8_t* dst = (bsel ? buf1 : buf0) + o * plan.ps + (pr * plan.pw + pcol) * 16;
+            uint8_t* dst = lds + bsel * plan.pbuf_bytes + o * plan.ps + (pr * plan.pw + pcol) * 16;
             *reinterpret_cast<u32x4*>(dst) = u32x4{0u, 0u, 0u, 0u};
         }
     }
+    uint8_t* buf0 = lds;
+    uint8_t* buf1 = lds + plan.pbuf_bytes;
     stage_store(buf0);
     lds_barrier();
     u32x4 af[2][TM];
     frag(af[0], buf0, 0);
 
-    // One chunk c of parity P: step s uses fragment set (s + P NS) & 1 (the
-    // sets alternate across chunk boundaries for odd NS too) and record set
-    // (s + P NS) % D.
+    // One iteration c of parity P (this wave's chunk WK c + wk): step s uses
+    // fragment set (s + P NS) & 1 (the sets alternate across iterations for
+    // odd NS too) and record set (s + P NS) % D.
     auto body = [&](auto pc, int c) {
         constexpr int P = decltype(pc)::value;
         const uint8_t* cur = P ? buf1 : buf0;
@@ -278,12 +297,42 @@ rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const
         lds_barrier();
         frag(af[(NS + P * NS) & 1], nxt, 0);
     };
+    const int niter = (plan.nchunk + WK - 1) / WK;
     int c = 0;
-    for (; c + 1 < plan.nchunk; c += 2) {
+    for (; c + 1 < niter; c += 2) {
         body(std::integral_constant<int, 0>{}, c);
         body(std::integral_constant<int, 1>{}, c + 1);
     }
-    if (c < plan.nchunk) body(std::integral_constant<int, 0>{}, c);
+    if (c < niter) body(std::integral_constant<int, 0>{}, c);
+
+    if constexpr (WK == 2) {
+        // the second reduction half's partial tiles meet the first's in LDS
+        // (the staging buffers are free once every wave is past this barrier)
+        lds_barrier();
+        floatx4* red = reinterpret_cast<floatx4*>(lds) + (WN / (32 * TN)) * (TM * TN * 4 * 64);
+        if (wk == 1) {
+#pragma unroll
+            for (int a = 0; a < TM; ++a)
+#pragma unroll
+                for (int b = 0; b < TN; ++b)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        red[((a * TN + b) * 4 + i) * 64 + lane] =
+                            floatx4{acc[a][b][4 * i], acc[a][b][4 * i + 1], acc[a][b][4 * i + 2], acc[a][b][4 * i + 3]};
+        }
+        lds_barrier();
+        if (wk == 1) return;
+#pragma unroll
+        for (int a = 0; a < TM; ++a)
+#pragma unroll
+            for (int b = 0; b < TN; ++b)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const floatx4 o = red[((a * TN + b) * 4 + i) * 64 + lane];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[a][b][4 * i + e] += o[e];
+                }
+    }
 
     // ---- epilogue: scale, round, store 4 consecutive tokens of one channel per quad ----
     const __amdgpu_buffer_rsrc_t sr = buffer_rsrc(scales, (uint64_t)geo.C_out * 4u);
@@ -324,46 +373,65 @@ rec_conv_kernel(Geom geo, FusedPlan plan, const uint8_t* __restrict__ rec, const
         }
 }
 
-template <int KIND, int TM, int TN, int UPL, int D>
+template <int KIND, int WK, int TM, int TN, int UPL, int D>
 hipError_t rec_conv_cfg(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
-    auto kern = rec_conv_kernel<KIND, TM, TN, UPL, D>;
+    auto kern = rec_conv_kernel<KIND, WK, TM, TN, UPL, D>;
     hipError_t e = ensure_dynamic_lds((const void*)kern, plan.lds_bytes);
     if (e != hipSuccess) return e;
     if (fl.occupancy) return hipOccupancyMaxActiveBlocksPerMultiprocessor(fl.occupancy, kern, 256, plan.lds_bytes);
     const dim3 grid((unsigned)plan.ntiles);
     kern<<<grid, 256, plan.lds_bytes, fl.stream>>>(geo, plan, fl.crec, fl.scales, fl.X, fl.Y, fl.y_dtype);
-    note_launch(fl.stream, "rec_conv_kernel", {KIND, TM, TN, UPL, D});
+    note_launch(fl.stream, "rec_conv_kernel", {KIND, WK, TM, TN, UPL, D});
     return hipGetLastError();
 }
 
-template <int TN, int D>
+// Instantiated (UPL, D) per tile: what fits 256 registers per lane without
+// spills (192 channels: six record sets with one staging unit per thread; the
+// two-wave reduction: three record sets, and at most two units for 192 channels).
+template <int WK, int TN, int D>
 hipError_t rec_conv3_upl(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
-    if (plan.upl == 1) return rec_conv_cfg<1, 2, TN, 1, D>(geo, plan, fl);
+    if (plan.upl == 1) return rec_conv_cfg<1, WK, 2, TN, 1, D>(geo, plan, fl);
     if constexpr (TN == 3 && D == 6) {
-        // 192 channels with six record sets: only one staging unit per thread
-        // fits 256 registers per lane
         return hipErrorInvalidConfiguration;
     } else {
-        if (plan.upl == 2) return rec_conv_cfg<1, 2, TN, 2, D>(geo, plan, fl);
-        if (plan.upl == 3) return rec_conv_cfg<1, 2, TN, 3, D>(geo, plan, fl);
-        return hipErrorInvalidConfiguration;
+        if (plan.upl == 2) return rec_conv_cfg<1, WK, 2, TN, 2, D>(geo, plan, fl);
+        if constexpr (WK == 2 && TN == 3) {
+            return hipErrorInvalidConfiguration;
+        } else {
+            if (plan.upl == 3) return rec_conv_cfg<1, WK, 2, TN, 3, D>(geo, plan, fl);
+            return hipErrorInvalidConfiguration;
+        }
+    }
+}
+
+template <int WK>
+hipError_t rec_conv_wk(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
+    if (plan.kind == 2) {
+        // 1x1: 64 (3 - WK) tokens stage 8 planes x 64 pixels per chunk, two
+        // units per thread; records three steps ahead (four sets)
+        if (plan.upl != 2 || plan.rdepth != 4) return hipErrorInvalidConfiguration;
+        return plan.bn == 192 ? rec_conv_cfg<2, WK, 2, 3, 2, 4>(geo, plan, fl)
+                              : rec_conv_cfg<2, WK, 2, 2, 2, 4>(geo, plan, fl);
+    }
+    if (plan.kind != 1) return hipErrorInvalidConfiguration;
+    if constexpr (WK == 2) {
+        if (plan.rdepth != 3) return hipErrorInvalidConfiguration;
+        return plan.bn == 192 ? rec_conv3_upl<2, 3, 3>(geo, plan, fl) : rec_conv3_upl<2, 2, 3>(geo, plan, fl);
+    } else {
+        if (plan.rdepth != 3 && plan.rdepth != 6) return hipErrorInvalidConfiguration;
+        if (plan.bn == 192)
+            return plan.rdepth == 6 ? rec_conv3_upl<1, 3, 6>(geo, plan, fl) : rec_conv3_upl<1, 3, 3>(geo, plan, fl);
+        return plan.rdepth == 6 ? rec_conv3_upl<1, 2, 6>(geo, plan, fl) : rec_conv3_upl<1, 2, 3>(geo, plan, fl);
     }
 }
 
 }  // namespace
 
 hipError_t launch_rec_conv(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {
-    if (plan.bm != 128 || plan.dec != FUSED_DEC_REC || (plan.bn != 128 && plan.bn != 192))
-        return hipErrorInvalidConfiguration;
-    if (plan.kind == 2) {
-        // 1x1: 128 tokens stage 8 planes x 128 pixels, two units per thread;
-        // records three steps ahead (four sets)
-        if (plan.upl != 2 || plan.rdepth != 4) return hipErrorInvalidConfiguration;
-        return plan.bn == 192 ? rec_conv_cfg<2, 2, 3, 2, 4>(geo, plan, fl) : rec_conv_cfg<2, 2, 2, 2, 4>(geo, plan, fl);
-    }
-    if (plan.kind != 1 || (plan.rdepth != 3 && plan.rdepth != 6)) return hipErrorInvalidConfiguration;
-    if (plan.bn == 192) return plan.rdepth == 6 ? rec_conv3_upl<3, 6>(geo, plan, fl) : rec_conv3_upl<3, 3>(geo, plan, fl);
-    return plan.rdepth == 6 ? rec_conv3_upl<2, 6>(geo, plan, fl) : rec_conv3_upl<2, 3>(geo, plan, fl);
+    if (plan.dec != FUSED_DEC_REC || (plan.bn != 128 && plan.bn != 192)) return hipErrorInvalidConfiguration;
+    if (plan.bm == 128) return rec_conv_wk<1>(geo, plan, fl);
+    if (plan.bm == 64) return rec_conv_wk<2>(geo, plan, fl);
+    return hipErrorInvalidConfiguration;
 }
 
 }  // namespace aq
