@@ -437,6 +437,8 @@ def lut_regime_bench(a, torch, P, W):
     shapes = sorted(set((s.K, s.C_out, s.M) for s in W.lut_regime_specs()))
     if a.lut_k:
         shapes = [sh for sh in shapes if sh[0] == a.lut_k]
+    if a.lut_m:
+        shapes = [sh for sh in shapes if sh[2] == a.lut_m]
     tiny = torch.zeros(1, device="cuda")
     floor_us = _graph_time_us(torch, lambda: tiny.add_(1.0), reps=20)
     rows = []
@@ -598,6 +600,7 @@ def main(argv=None):
     ap.add_argument("--table", default="", help="sweep: write the per-layer table (markdown) here")
     ap.add_argument("--lut-ns", default="", help="lutregime: token counts, comma separated (default 1..32)")
     ap.add_argument("--lut-k", type=int, default=0, help="lutregime: only the shapes with this K")
+    ap.add_argument("--lut-m", type=int, default=0, help="lutregime: only the shapes with this M")
     ap.add_argument("--op", default="forward", choices=["forward", "grad"],
                     help="grad: the codebook gradient of the named layer instead of its forward")
     a = ap.parse_args(argv)
