@@ -346,6 +346,48 @@ def sweep_bench(a, torch, P, W):
 
     # per-launch kernel durations inside the same pass (events around every launch)
     per_layer, tmode, pass_us_ev = launch_times(torch, items)
+
+    # weight source of every forward: in-loop decode (W never in memory), records
+    # (the decompress-then-compute route: unscaled fp16 W written and read back
+    # every forward) or the table path; then the same pass with the in-loop
+    # decode forced wherever the format has one
+    src_t, src_n, rec_bytes = {}, {}, 0
+    for i, (layer, _) in enumerate(items):
+        d = layer.describe(specs[i].n)
+        k = "table" if d.get("path") == "lut" else "records" if d.get("weights") == "records" else "in-loop"
+        src_t[k] = src_t.get(k, 0.0) + sum(t for _, t in per_layer[i])
+        src_n[k] = src_n.get(k, 0) + 1
+        rec_bytes += int(d.get("records_bytes", 0))
+    for layer, _ in items:
+        layer.set_option("weights", 1)
+    n_inloop = sum(1 for i, (layer, _) in enumerate(items) if layer.describe(specs[i].n).get("weights") != "records")
+    run_pass()
+    torch.cuda.synchronize()
+    graph_il = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(stream):
+        with torch.cuda.graph(graph_il, stream=stream):
+            run_pass()
+    torch.cuda.current_stream().wait_stream(stream)
+    for _ in range(max(0, a.warmup)):
+        graph_il.replay()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(a.steps):
+        graph_il.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    inloop_us = start.elapsed_time(stop) * 1e3 / a.steps
+    del graph_il
+    for layer, _ in items:
+        layer.set_option("weights", 0)
+    ttot = sum(src_t.values())
+    weights = {"time_frac": {k: round(v / ttot, 4) for k, v in sorted(src_t.items())},
+               "layers": dict(sorted(src_n.items())), "record_bytes_per_pass": rec_bytes,
+               "in_loop_pass": {"ms_per_step": round(inloop_us / 1e3, 6),
+                                "value": round(total_flops / (inloop_us * 1e-6) / 1e12, 3),
+                                "layers_in_loop": n_inloop,
+                                "note": "the same pass with the in-loop decode forced on every layer whose format "
+                                        "has one: W is never written to memory"}}
     flops = [sp.dense_flops for sp in specs]
     kname, k_us, k_n, k_flops, ktable = dominant_kernel(per_layer, flops)
     workload = f"unet_sweep_b8_{a.variant}{'_full' if a.full else ''}_chained"
@@ -366,6 +408,11 @@ def sweep_bench(a, torch, P, W):
                     f"Per-layer times below: each forward alone in a HIP graph (sum "
                     f"{sum(t for lay in per_layer for _, t in lay):.1f} us), split among its launches by "
                     f"timing events (eager pass with events: {pass_us_ev:.1f} us).\n\n")
+            f.write("Weight source (share of the per-layer time; layers): " +
+                    ", ".join(f"{k} {weights['time_frac'][k]:.3f} ({weights['layers'][k]})" for k in weights["layers"]) +
+                    f"; records written and read back per pass: {rec_bytes / 1e6:.1f} MB.  The same pass with the "
+                    f"in-loop decode forced wherever the format has one ({n_inloop} of {len(items)} layers; W never in "
+                    f"memory): {inloop_us:.1f} us ({total_flops / (inloop_us * 1e-6) / 1e12:.1f} TFLOP/s).\n\n")
             f.write("Per kernel (sum over the pass):\n\n| kernel | launches | total us | share | TFLOP/s |\n"
                     "|---|---|---|---|---|\n")
             ksum = sum(r[1] for r in ktable)
@@ -406,6 +453,7 @@ def sweep_bench(a, torch, P, W):
                      "kernel_avg_us": round(k_us / k_n, 3), "kernel_flops": k_flops, "timing": tmode,
                      "pass_frac": round(total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS, 4)},
         "kernels": [{"kernel": n, "launches": c, "total_us": round(t, 2)} for n, t, c, _ in ktable[:6]],
+        "weights": weights,
         "activation_rms": [round(min(rms), 4), round(max(rms), 4)],
     }
     if a.copy_bytes > 0:
