@@ -33,6 +33,11 @@ CASES = [
     (LayerSpec(name="st_dense", C_out=200, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 24, 16)),
      {"weights": 2, "record_product": 2}, 1),
     (LayerSpec(name="st_kaq", C_out=96, K=32 * 9, g=9, M=2, B=8, n=2, conv=ConvGeom(32, 3, 3, 1, 1, 16, 16)), {}, 1),
+    # the wave-split convolution kernel: one wave per reduction (3x3), two waves per reduction (1x1)
+    (LayerSpec(name="st_ws_conv3", C_out=192, K=64 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(64, 3, 3, 1, 1, 16, 16)),
+     {"weights": 2, "record_product": 3}, 1),
+    (LayerSpec(name="st_ws2_conv1", C_out=128, K=128, g=8, M=2, B=8, n=4, conv=ConvGeom(128, 1, 1, 1, 0, 16, 16)),
+     {"weights": 2, "record_product": 3, "fused_tile": "64x128"}, 2),
 ]
 
 
