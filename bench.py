@@ -323,26 +323,59 @@ def sweep_bench(a, torch, P, W):
         for _, fn in items:
             fn()
 
-    # the timed steps: whole passes replayed from one graph
-    stream = torch.cuda.Stream()
-    stream.wait_stream(torch.cuda.current_stream())
-    run_pass()
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.stream(stream):
-        with torch.cuda.graph(graph, stream=stream):
-            run_pass()
-    torch.cuda.current_stream().wait_stream(stream)
-    for _ in range(max(0, a.warmup)):
-        graph.replay()
-    torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(a.steps):
-        graph.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    pass_us = start.elapsed_time(stop) * 1e3 / a.steps
+    side = torch.cuda.Stream()
+
+    def run_pass_overlapped():
+        # every forward's weight records (where its route has them) decoded on a
+        # second stream, in layer order, overlapped with the products of earlier
+        # layers; each forward waits for its own layer's records only
+        main = torch.cuda.current_stream()
+        ahead = a.records_ahead
+
+        def prep(j):
+            side.wait_stream(main)              # issued once layer j - ahead's forward is queued
+            items[j][0].prepare(specs[j].n, stream=side.cuda_stream)
+            ev = torch.cuda.Event()
+            ev.record(side)
+            return ev
+
+        ready = {j: prep(j) for j in range(min(ahead, len(items)))}
+        for i, (_, fn) in enumerate(items):
+            main.wait_event(ready.pop(i))
+            if i + ahead < len(items):
+                ready[i + ahead] = prep(i + ahead)
+            fn()
+        main.wait_stream(side)
+
+    def time_graph(body):
+        stream = torch.cuda.Stream()
+        stream.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(stream):
+            body()
+        torch.cuda.current_stream().wait_stream(stream)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(stream):
+            with torch.cuda.graph(g, stream=stream):
+                body()
+        torch.cuda.current_stream().wait_stream(stream)
+        for _ in range(max(0, a.warmup)):
+            g.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(a.steps):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) * 1e3 / a.steps
+
+    # the timed steps: whole passes replayed from one graph on one stream;
+    # --records-overlap also times the schedule that decodes records on a
+    # second stream ahead of their forwards (measured slower: the replayed
+    # graph's cross-stream dependencies cost more than they hide)
+    pass_us = time_graph(run_pass)
+    overlap_us = time_graph(run_pass_overlapped) if a.records_overlap else None
 
     # per-launch kernel durations inside the same pass (events around every launch)
     per_layer, tmode, pass_us_ev = launch_times(torch, items)
@@ -361,23 +394,7 @@ def sweep_bench(a, torch, P, W):
     for layer, _ in items:
         layer.set_option("weights", 1)
     n_inloop = sum(1 for i, (layer, _) in enumerate(items) if layer.describe(specs[i].n).get("weights") != "records")
-    run_pass()
-    torch.cuda.synchronize()
-    graph_il = torch.cuda.CUDAGraph()
-    with torch.cuda.stream(stream):
-        with torch.cuda.graph(graph_il, stream=stream):
-            run_pass()
-    torch.cuda.current_stream().wait_stream(stream)
-    for _ in range(max(0, a.warmup)):
-        graph_il.replay()
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(a.steps):
-        graph_il.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    inloop_us = start.elapsed_time(stop) * 1e3 / a.steps
-    del graph_il
+    inloop_us = time_graph(run_pass)
     for layer, _ in items:
         layer.set_option("weights", 0)
     ttot = sum(src_t.values())
@@ -407,7 +424,10 @@ def sweep_bench(a, torch, P, W):
                     f"{total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS:.3f} of 2.5 PFLOP/s).  "
                     f"Per-layer times below: each forward alone in a HIP graph (sum "
                     f"{sum(t for lay in per_layer for _, t in lay):.1f} us), split among its launches by "
-                    f"timing events (eager pass with events: {pass_us_ev:.1f} us).\n\n")
+                    f"timing events (eager pass with events: {pass_us_ev:.1f} us)." +
+                    ("" if overlap_us is None else
+                     f"  With record decodes on a second stream {a.records_ahead} layer(s) ahead: {overlap_us:.1f} us.")
+                    + "\n\n")
             f.write("Weight source (share of the per-layer time; layers): " +
                     ", ".join(f"{k} {weights['time_frac'][k]:.3f} ({weights['layers'][k]})" for k in weights["layers"]) +
                     f"; records written and read back per pass: {rec_bytes / 1e6:.1f} MB.  The same pass with the "
@@ -454,6 +474,11 @@ def sweep_bench(a, torch, P, W):
                      "pass_frac": round(total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS, 4)},
         "kernels": [{"kernel": n, "launches": c, "total_us": round(t, 2)} for n, t, c, _ in ktable[:6]],
         "weights": weights,
+        "schedule": {"streams": 1,
+                     "ms_per_step_records_ahead": None if overlap_us is None else round(overlap_us / 1e3, 6),
+                     "records_ahead": a.records_ahead if a.records_overlap else None,
+                     "note": "records_ahead: per-forward record decodes on a second stream, that many layers ahead "
+                             "of their forwards (aq_layer_prepare), every decode still inside the timed pass"},
         "activation_rms": [round(min(rms), 4), round(max(rms), 4)],
     }
     if a.copy_bytes > 0:
@@ -649,6 +674,10 @@ def main(argv=None):
     ap.add_argument("--lut-ns", default="", help="lutregime: token counts, comma separated (default 1..32)")
     ap.add_argument("--lut-k", type=int, default=0, help="lutregime: only the shapes with this K")
     ap.add_argument("--lut-m", type=int, default=0, help="lutregime: only the shapes with this M")
+    ap.add_argument("--records-ahead", type=int, default=1,
+                    help="sweep: layers ahead of the current forward whose records the second stream decodes")
+    ap.add_argument("--records-overlap", action="store_true",
+                    help="sweep: also time the pass with record decodes on a second stream (--records-ahead)")
     ap.add_argument("--op", default="forward", choices=["forward", "grad"],
                     help="grad: the codebook gradient of the named layer instead of its forward")
     a = ap.parse_args(argv)

@@ -115,6 +115,24 @@ aq_status aq_layer_forward(aq_layer* layer, const void* X, const float* x_scales
                            void* stream);
 
 /*
+ * Decode the per-forward weight records of a forward over n tokens (linear)
+ * or images (convolution) ahead of that forward, on `stream` (row a4 on the
+ * pre-decoded route: the unscaled fp16 weights of Sec. 2.4 eq. (4), written
+ * to the layer's record buffer).  The decode depends on the weights alone,
+ * so a caller may run it on another stream, overlapped with other work (the
+ * previous layer's product, say).  The next aq_layer_forward of this layer
+ * with the same n then launches only its product kernel.  Ordering is the
+ * caller's: that forward must be stream-ordered after this call's work (its
+ * stream waits for `stream`, with an event), and no earlier forward of this
+ * layer may still be reading the record buffer when this call's decode runs.
+ * A route without pre-decoded records launches nothing and leaves the
+ * forward unchanged; a forward with another n, and the allocation-free
+ * forward, decode their own records.  Errors: AQ_ERR_INVALID_ARGUMENT (null
+ * layer, n < 1, tokens beyond max_tokens), AQ_ERR_DEVICE (launch failed).
+ */
+aq_status aq_layer_prepare(aq_layer* layer, int64_t n, void* stream);
+
+/*
  * Allocation-free forward, for callers that cannot allocate device memory
  * during the call or keep per-layer workspace (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation).  Arguments,

@@ -29,7 +29,8 @@ OPTION_CODES = {"lut_max_tokens": 1, "weights": 2, "generic": 3, "record_product
                 "grad_splits": 11, "grad_regs": 12, "grad_tile": 13, "table_one_launch": 14}
 _TILE_OPTIONS = ("fused_tile", "dense_tile", "grad_tile")
 
-EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_decode", "aq_layer_codebook_grad",
+EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_prepare", "aq_layer_decode",
+            "aq_layer_codebook_grad",
             "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
             "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy",
             "aq_last_error", "aq_version")
@@ -76,6 +77,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_create.argtypes = [ctypes.POINTER(aq_layer_desc), vp, vp, vp, i32, i32, i32, ctypes.POINTER(vp)]
     lib.aq_layer_forward.argtypes = [vp, vp, vp, vp, i64, vp]
     lib.aq_layer_forward_static.argtypes = [vp, vp, vp, vp, i64, vp]
+    lib.aq_layer_prepare.argtypes = [vp, i64, vp]
     lib.aq_layer_decode.argtypes = [vp, vp, vp]
     lib.aq_layer_codebook_grad.argtypes = [vp, vp, vp, i32, vp, i64, vp]
     lib.aq_layer_set_path.argtypes = [vp, i32]
@@ -86,7 +88,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_describe.argtypes = [vp, i64, ctypes.c_char_p, i64]
     lib.aq_layer_choose_path.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_int)]
     lib.aq_layer_destroy.argtypes = [vp]
-    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_decode", "aq_layer_codebook_grad",
+    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_prepare", "aq_layer_decode",
+              "aq_layer_codebook_grad",
               "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
               "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy"):
         getattr(lib, f).restype = ctypes.c_int
@@ -138,6 +141,10 @@ def aq_layer_forward(handle: int, X: int, x_scales: int, Y: int, n: int, stream:
 
 def aq_layer_forward_static(handle: int, X: int, x_scales: int, Y: int, n: int, stream: int) -> None:
     _check(load_library().aq_layer_forward_static(handle, X, x_scales, Y, n, stream))
+
+
+def aq_layer_prepare(handle: int, n: int, stream: int) -> None:
+    _check(load_library().aq_layer_prepare(handle, n, stream))
 
 
 def aq_layer_decode(handle: int, W: int, stream: int) -> None:
@@ -310,6 +317,18 @@ class AQLayer:
         return out
 
     __call__ = forward
+
+    def prepare(self, n=None, stream=None):
+        """Decode the weight records of the next forward over ``n`` tokens or
+        images (default: the spec's n) on ``stream`` (a raw stream handle;
+        default: the current stream), ahead of that forward; see
+        ``aq_layer_prepare`` for the ordering the caller owes."""
+        import torch
+        n = self.spec.n if n is None else n
+        if not isinstance(n, int) or n < 1:
+            raise ValueError("n must be a positive int")
+        st = stream if stream is not None else torch.cuda.current_stream(self.device).cuda_stream
+        aq_layer_prepare(self.handle, n, st)
 
     def decode(self, out=None, stream=None):
         import torch

@@ -55,6 +55,8 @@ struct aq_layer {
     std::vector<hipEvent_t> events;   // caller's timing events (aq_layer_set_launch_events)
     int32_t last_launches;            // kernel launches of the last traced call
     std::string last_names;           // and their kernels, one per line
+    int64_t prepared_n;               // aq_layer_prepare decoded the records of a forward of this
+                                      // many tokens / images into d_wrec (0: none pending)
 };
 
 namespace aq {
@@ -824,6 +826,13 @@ aq_status check_forward(const aq_layer* L, const void* X, const float* x_scales,
     return AQ_OK;
 }
 
+// Whether aq_layer_prepare already decoded this forward's records into the
+// layer's own buffer (and the forward uses that buffer).  Any forward on the
+// layer's workspace consumes the pending preparation.
+bool records_prepared(aq_layer* L, const Workspace& wk, int64_t n) {
+    return wk.wrec == L->d_wrec && L->prepared_n == n;
+}
+
 aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X, const float* x_scales, void* Y,
                     int64_t n, hipStream_t st, const Workspace& wk) {
     const aq_layer_desc& d = L->desc;
@@ -845,7 +854,7 @@ aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X,
         e = aq::launch_mfma_forward(geo, w, X, d.x_dtype, xs, Y, d.y_dtype, d.tile_dtype, st);
         break;
     case Route::DENSE: {
-        e = aq::launch_operand_records(geo, fp, w, wk.wrec, st);
+        if (!records_prepared(L, wk, n)) e = aq::launch_operand_records(geo, fp, w, wk.wrec, st);
         const aq::FusedLaunch fl{nullptr, static_cast<const uint8_t*>(wk.wrec), L->d_scales, X, xs, Y,
                                  d.y_dtype, d.x_dtype, st, nullptr, nullptr};
         if (e == hipSuccess) e = aq::launch_rec_gemm(geo, fp, fl, wk.xpack, L->d_zero);
@@ -857,7 +866,7 @@ aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X,
                                                            : L->d_cbtile;
         const uint8_t* recs = L->d_crec;
         if (fp.dec == aq::FUSED_DEC_REC) {
-            e = aq::launch_operand_records(geo, fp, w, wk.wrec, st);
+            if (!records_prepared(L, wk, n)) e = aq::launch_operand_records(geo, fp, w, wk.wrec, st);
             recs = static_cast<const uint8_t*>(wk.wrec);
         }
         fp.x_bytes = geo.conv ? n * (int64_t)geo.cin * geo.H * geo.W * 2
@@ -870,6 +879,7 @@ aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X,
         break;
     }
     }
+    if (wk.wrec == L->d_wrec) L->prepared_n = 0;
     if (e != hipSuccess) return hip_fail(e, "forward launch");
     if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
     return AQ_OK;
@@ -1155,6 +1165,28 @@ aq_status aq_layer_forward(aq_layer* L, const void* X, const float* x_scales, vo
     if (s != AQ_OK) return s;
     const Workspace wk{L->d_ws, L->d_lut_arrivals, L->d_wrec, L->d_part, L->d_arrivals, L->d_xpack};
     return run_route(L, geo, r, X, x_scales, Y, n, static_cast<hipStream_t>(stream), wk);
+}
+
+aq_status aq_layer_prepare(aq_layer* L, int64_t n, void* stream) {
+    if (!L) return fail(AQ_ERR_INVALID_ARGUMENT, "null layer");
+    if (n < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "n must be >= 1");
+    const Geom geo = make_geom(L, n);
+    if (geo.tokens > L->desc.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens");
+    const Route r = plan_route(L, geo);
+    L->prepared_n = 0;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    TraceScope trace(L, st);
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
+    const bool rec = (r.kind == Route::FUSED || r.kind == Route::REC_LINEAR || r.kind == Route::DENSE) &&
+                     r.fp.dec == aq::FUSED_DEC_REC;
+    if (!rec) return AQ_OK;                      // nothing of this forward depends on the weights alone
+    const aq_layer_desc& d = L->desc;
+    const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, d.codebook_dtype};
+    const hipError_t e = aq::launch_operand_records(geo, r.fp, w, L->d_wrec, st);
+    if (e != hipSuccess) return hip_fail(e, "records launch");
+    if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
+    L->prepared_n = n;
+    return AQ_OK;
 }
 
 aq_status aq_layer_forward_static(aq_layer* L, const void* X, const float* x_scales, void* Y, int64_t n,

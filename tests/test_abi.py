@@ -165,6 +165,7 @@ def test_null_handles_are_rejected():
     buf = ctypes.create_string_buffer(64)
     assert lib.aq_layer_describe(None, 4, buf, 64) == A.AQ_ERR_INVALID_ARGUMENT
     assert lib.aq_layer_set_launch_events(None, None, 0) == A.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layer_prepare(None, 1, None) == A.AQ_ERR_INVALID_ARGUMENT
     n = ctypes.c_int32()
     assert lib.aq_layer_last_launches(None, ctypes.byref(n), buf, 64) == A.AQ_ERR_INVALID_ARGUMENT
 

@@ -393,6 +393,82 @@ def test_wave_split_conv_staging_and_fallback():
         assert O.rel_err_inf(y, O.forward(odd, inp)) <= 2e-3
 
 
+# aq_layer_prepare: the records route's weight decode issued ahead of the forward
+PREPARE = [
+    (WSPLIT[0], {"weights": 2, "record_product": 3}, "rec_conv_kernel"),
+    (LayerSpec(name="prep_lin", C_out=256, K=512, g=8, M=2, B=8, n=2048), {"weights": 2}, "rec_linear_kernel"),
+    (LayerSpec(name="prep_fused_rec", C_out=96, K=32 * 9, g=8, M=4, B=8, n=2, conv=ConvGeom(32, 3, 3, 1, 1, 16, 16)),
+     {"weights": 2, "record_product": 1}, "fused_fwd_kernel"),
+    (LayerSpec(name="prep_in_loop", C_out=64, K=64 * 9, g=8, M=2, B=8, n=2, conv=ConvGeom(64, 3, 3, 1, 1, 16, 16)),
+     {"weights": 1}, None),
+]
+
+
+@pytest.mark.parametrize("spec,opts,product", PREPARE, ids=[c[0].name for c in PREPARE])
+def test_prepare_decodes_records_ahead(spec, opts, product):
+    """A forward after aq_layer_prepare (same stream, another stream ordered by an event, or both captured in a
+    graph) launches only its product and gives the plain forward's bits; a forward over another n, or a route
+    without records, decodes as usual."""
+    import paper_2506_05960_amd as P
+    inp = generate(spec, 515)
+    layer = P.AQLayer(spec, inp)
+    for k, v in opts.items():
+        layer.set_option(k, v)
+    x = _dev(inp["x"], spec.x_dtype)
+    ref = layer.forward(x).clone()
+    n_plain, _ = layer.last_launches()
+    torch.cuda.synchronize()
+    layer.prepare(spec.n)
+    n_prep, _ = layer.last_launches()
+    y = layer.forward(x)
+    n_fwd, names = layer.last_launches()
+    torch.cuda.synchronize()
+    _say(f"prepare {spec.name}: plain {n_plain} launches, prepare {n_prep}, forward after it {n_fwd} {names}")
+    assert torch.equal(y, ref)
+    if product:
+        assert n_prep == 1 and n_fwd == n_plain - 1 and names[-1].startswith(product)
+    else:
+        assert n_prep == 0 and n_fwd == n_plain
+    # prepared on another stream, ordered by an event
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    side.wait_stream(main)
+    layer.prepare(spec.n, stream=side.cuda_stream)
+    ev = torch.cuda.Event()
+    ev.record(side)
+    main.wait_event(ev)
+    assert torch.equal(layer.forward(x), ref)
+    # a forward over another n decodes its own records; the next plain forward is unchanged
+    n2 = max(1, spec.n // 2)
+    ref2 = layer.forward(x[:n2]).clone()
+    layer.prepare(spec.n)
+    assert torch.equal(layer.forward(x[:n2]), ref2)
+    assert torch.equal(layer.forward(x), ref)
+    # both streams captured in one graph, replayed with eager forwards in between
+    out = torch.zeros_like(ref)
+    cap = torch.cuda.Stream()
+    cap.wait_stream(main)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            side.wait_stream(cap)
+            layer.prepare(spec.n, stream=side.cuda_stream)
+            e2 = torch.cuda.Event()
+            e2.record(side)
+            cap.wait_event(e2)
+            layer.forward(x, out=out)
+    main.wait_stream(cap)
+    for rep in range(3):
+        out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), rep
+        assert torch.equal(layer.forward(x), ref)
+        torch.cuda.synchronize()
+    layer.close()
+
+
 GEMM_CASES = [
     LayerSpec(name="g_conv3", C_out=200, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 24, 16)),
     LayerSpec(name="g_conv3_img8", C_out=150, K=48 * 9, g=8, M=1, B=16, n=5, conv=ConvGeom(48, 3, 3, 1, 1, 8, 8)),
