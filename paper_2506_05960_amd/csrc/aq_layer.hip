@@ -752,7 +752,8 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
     //    x 384 channels: 3-8 % faster than the fused kernel, 3x3 and 1x1);
     //  * else, for 1x1 layers with M >= 4, 128-token tiles from 128 of them
     //    (the in-loop decode gathers 4 codewords per group).
-    // Fewer tiles leave compute units idle: the fused kernel stays ahead.  1x1
+    // Fewer tiles leave compute units idle: the fused kernel stays ahead; so
+    // does it for output rows under 16 tokens (the rule needs OW >= 16).  1x1
     // layers switch to records for it even where the in-loop decode was
     // chosen.  AQ_OPT_RECORD_PRODUCT = 3 forces the kernel where it applies
     // (a forced 64-token AQ_OPT_FUSED_TILE selects the two-wave reduction), 1
@@ -770,7 +771,9 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
         const aq::FusedPlan* pick = nullptr;
         if (opt.rec_product == 3 && !ws_1x1) {
             if (opt.fused_bm == 64 ? ok2 : ok1) pick = opt.fused_bm == 64 ? &w2 : &w1;
-        } else if (opt.rec_product == 0) {
+        } else if (opt.rec_product == 0 && geo.OW >= 16) {
+            // (output rows under 16 tokens: this kernel does not widen its staged
+            // rows, and its fragment reads conflict; 8 x 8 images measured slower)
             if (ok1 && w1.ntiles >= (fp.kind == 1 ? 192 : 256)) pick = &w1;
             else if (ok2 && w2.ntiles >= 256 && fp.nchunk >= 8) pick = &w2;
             else if (ok1 && fp.kind == 2 && geo.M >= 4 && w1.ntiles >= 128) pick = &w1;
