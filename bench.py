@@ -821,6 +821,29 @@ def main(argv=None):
         "roofline": roof,
         "kernels": [{"kernel": n, "launches": c // 10, "avg_us": round(t / c, 3)} for n, t, c, _ in ktable],
     }
+    if path == "decode":
+        # weight source of this forward; on the records route (W written to
+        # memory every forward) the in-loop decode (W never in memory) is timed
+        # beside it the same way
+        d = layer.describe(spec.n)
+        wsrc = {"source": "records" if d.get("weights") == "records" else "in-loop",
+                "record_bytes": int(d.get("records_bytes", 0))}
+        if wsrc["source"] == "records":
+            layer.set_option("weights", 1)
+            if layer.describe(spec.n).get("weights") != "records":
+                g_il = capture(per_graph)
+                t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                t0.record()
+                for _ in range(max(1, nfull)):
+                    g_il.replay()
+                t1.record()
+                torch.cuda.synchronize()
+                ms_il = t0.elapsed_time(t1) / (max(1, nfull) * per_graph)
+                wsrc["in_loop"] = {"ms_per_step": round(ms_il, 6), "value": round(flops / (ms_il * 1e-3) / 1e12, 3),
+                                   "route": layer.describe(spec.n).get("route"),
+                                   "tile": layer.describe(spec.n).get("tile")}
+            layer.set_option("weights", 0)
+        out["weights"] = wsrc
     if not a.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(spec, inp)
     layer.close()
