@@ -753,14 +753,16 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
     //  * else, for 1x1 layers with M >= 4, 128-token tiles from 128 of them
     //    (the in-loop decode gathers 4 codewords per group).
     // Fewer tiles leave compute units idle: the fused kernel stays ahead; so
-    // does it for output rows under 16 tokens (the rule needs OW >= 16).  1x1
-    // layers switch to records for it even where the in-loop decode was
-    // chosen.  AQ_OPT_RECORD_PRODUCT = 3 forces the kernel where it applies
-    // (a forced 64-token AQ_OPT_FUSED_TILE selects the two-wave reduction), 1
-    // and 2 exclude it; AQ_OPT_WEIGHTS = 1 keeps a 1x1 layer on the in-loop decode.
+    // does it for output rows under 16 tokens (the rule needs OW >= 16).
+    // Layers switch to records for it even where the in-loop decode was chosen
+    // (3x3 at 8192 tokens, M = 2: 23.6 -> 20.8 us at K = 1728 -> 192 with
+    // stride 2, 24.1 -> 21.7 us at K = 1728 -> 384).  AQ_OPT_RECORD_PRODUCT =
+    // 3 forces the kernel where it applies (a forced 64-token AQ_OPT_FUSED_TILE
+    // selects the two-wave reduction), 1 and 2 exclude it; AQ_OPT_WEIGHTS = 1
+    // keeps a layer on the in-loop decode.
     bool planned = false;
-    const bool ws_1x1 = fp.kind == 2 && fp.dec != aq::FUSED_DEC_REC && opt.weights == 0;
-    if (L->fused_ok && fits31 && opt.generic != 1 && fp.kind != 0 && (fp.dec == aq::FUSED_DEC_REC || ws_1x1) &&
+    const bool ws_switch = fp.kind != 0 && fp.dec != aq::FUSED_DEC_REC && opt.weights == 0;
+    if (L->fused_ok && fits31 && opt.generic != 1 && fp.kind != 0 && (fp.dec == aq::FUSED_DEC_REC || ws_switch) &&
         (opt.rec_product == 3 || opt.rec_product == 0)) {
         aq::FusedPlan rp = fp;
         rp.dec = aq::FUSED_DEC_REC;
@@ -769,7 +771,7 @@ Route plan_route(const aq_layer* L, const Geom& geo) {
         aq::FusedPlan w1 = rp, w2 = rp;
         const bool ok1 = wsplit_plan(geo, opt, 1, &w1), ok2 = wsplit_plan(geo, opt, 2, &w2);
         const aq::FusedPlan* pick = nullptr;
-        if (opt.rec_product == 3 && !ws_1x1) {
+        if (opt.rec_product == 3 && !ws_switch) {
             if (opt.fused_bm == 64 ? ok2 : ok1) pick = opt.fused_bm == 64 ? &w2 : &w1;
         } else if (opt.rec_product == 0 && geo.OW >= 16) {
             // (output rows under 16 tokens: this kernel does not widen its staged
