@@ -218,6 +218,72 @@ operand_records_f16_kernel(const u32x4* __restrict__ cb, const CodeT* __restrict
     }
 }
 
+// Records of a 3x3 chunk in the kernel-aware format (g = 9: one group per
+// input channel's 3x3 filter) from fp16 codebooks padded to 16 values per row:
+// a codeword is one 16-byte and one 4-byte load, every load of a thread is
+// issued before any sum, and the M codewords of a group are summed in fp16 in
+// ascending m (the same IEEE fp16 sums as operand_records_kernel).  A record
+// (chunk c, position s, channel n, lane half q) holds tap s of the 8 input
+// channels 16c + 8q + e; two threads share it, each decoding 4 channels and
+// writing its 8-byte half.
+template <typename CodeT, int MC>
+__global__ void __launch_bounds__(256)
+operand_records_g9_f16_kernel(const uint8_t* __restrict__ cbp, const CodeT* __restrict__ codes,
+                              uint8_t* __restrict__ rec, int nchunk, int C_out, int Gn, int B) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // (chunk, channel, half, quarter)
+    if (idx >= (int64_t)nchunk * C_out * 4) return;
+    const int hq = (int)(idx & 1);
+    const int64_t rid = idx >> 1;
+    const int c = (int)(rid / (2 * C_out));
+    const int rem = (int)(rid - (int64_t)c * 2 * C_out);
+    const int n = rem >> 1, q = rem & 1;
+    const uint32_t rows = 1u << B;
+    const int j0 = 16 * c + 8 * q + 4 * hq;
+    uint32_t code[4][MC];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int jc = j0 + e < Gn ? j0 + e : Gn - 1;   // groups past the end of K are zeroed below
+#pragma unroll
+        for (int m = 0; m < MC; ++m) code[e][m] = codes[((int64_t)n * Gn + jc) * MC + m];
+    }
+    u32x4 lo[4][MC];
+    uint32_t hi[4][MC];
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+        for (int m = 0; m < MC; ++m) {
+            const uint8_t* row = cbp + ((size_t)m * rows + code[e][m]) * 32u;
+            lo[e][m] = *reinterpret_cast<const u32x4*>(row);
+            hi[e][m] = *reinterpret_cast<const uint32_t*>(row + 16);
+        }
+    uint16_t v[4][9];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        _Float16 h[9];
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            const uint32_t w = t < 8 ? lo[e][0][t >> 1] : hi[e][0];
+            h[t] = __builtin_bit_cast(_Float16, (uint16_t)(w >> (16 * (t & 1))));
+        }
+#pragma unroll
+        for (int m = 1; m < MC; ++m)
+#pragma unroll
+            for (int t = 0; t < 9; ++t) {
+                const uint32_t w = t < 8 ? lo[e][m][t >> 1] : hi[e][m];
+                h[t] = h[t] + __builtin_bit_cast(_Float16, (uint16_t)(w >> (16 * (t & 1))));
+            }
+        const bool in = j0 + e < Gn;
+#pragma unroll
+        for (int t = 0; t < 9; ++t) v[e][t] = in ? __builtin_bit_cast(uint16_t, h[t]) : (uint16_t)0;
+    }
+    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+    for (int s = 0; s < 9; ++s) {
+        const u32x2 o{(uint32_t)v[0][s] | ((uint32_t)v[1][s] << 16), (uint32_t)v[2][s] | ((uint32_t)v[3][s] << 16)};
+        *reinterpret_cast<u32x2*>(rec + ((((int64_t)c * 9 + s) * C_out + n) * 2 + q) * 16 + 8 * hq) = o;
+    }
+}
+
 size_t operand_record_bytes(const Geom& geo, const FusedPlan& plan) {
     const int ns = plan.kind == 1 ? 9 : plan.cm;
     return (size_t)plan.nchunk * ns * geo.C_out * 2 * 16;
@@ -247,6 +313,20 @@ static hipError_t records_dispatch(const Geom& geo, const FusedPlan& plan, const
         }
 #undef AQ_REC16
         note_launch(st, "operand_records_f16_kernel", {8 * (int)sizeof(CodeT), plan.kind == 1, geo.M});
+        return hipGetLastError();
+    }
+    if (w.cb_dtype == AQ_F16 && geo.g == 9 && plan.kind == 1 && w.cb9 && (geo.M == 1 || geo.M == 2 || geo.M == 4)) {
+        const uint8_t* cbp = static_cast<const uint8_t*>(w.cb9);
+        const dim3 grid9((unsigned)((2 * n + 255) / 256));   // two threads per record
+        uint8_t* r8 = static_cast<uint8_t*>(rec);
+#define AQ_REC9(MC)                                                                                       \
+    operand_records_g9_f16_kernel<CodeT, MC><<<grid9, block, 0, st>>>(cbp, codes, r8, plan.nchunk, geo.C_out, \
+                                                                      geo.G, geo.B)
+        if (geo.M == 1) AQ_REC9(1);
+        else if (geo.M == 2) AQ_REC9(2);
+        else AQ_REC9(4);
+#undef AQ_REC9
+        note_launch(st, "operand_records_g9_f16_kernel", {8 * (int)sizeof(CodeT), geo.M});
         return hipGetLastError();
     }
 #define AQ_REC(CBT)                                                                                             \

@@ -59,6 +59,7 @@ struct DeviceWeights {
     const uint8_t* codes_lut;     // [nchunk][C_out][jc*M] uint8 (B <= 8), zero padded past G
     const float* scales;          // [C_out]
     int cb_dtype;                 // aq_dtype
+    const void* cb9;              // g = 9 fp16 codebooks padded to 16 values per row [M][2^B][16], else null
 };
 
 // LUT-path blocking chosen at create time.

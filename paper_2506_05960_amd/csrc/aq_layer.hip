@@ -26,6 +26,7 @@ struct aq_layer {
     void* d_cb;
     float* d_cb32;
     void* d_cbtile;
+    void* d_cb9;              // g = 9 fp16 codebooks padded to 16 values per row (records kernel)
     void* d_codes;
     uint8_t* d_codes_lut;
     float* d_scales;
@@ -239,7 +240,7 @@ void free_layer(aq_layer* L) {
     if (!L) return;
     void* ptrs[] = {L->d_cb,     L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales,
                     L->d_ws,     L->d_crec, L->d_wrec,   L->d_xpack, L->d_zero, L->d_gidx_offs,
-                    L->d_gidx_ent, L->d_gpart, L->d_part, L->d_arrivals, L->d_lut_arrivals};
+                    L->d_gidx_ent, L->d_gpart, L->d_part, L->d_arrivals, L->d_lut_arrivals, L->d_cb9};
     for (void* p : ptrs)
         if (p) (void)hipFree(p);
     delete L;
@@ -842,7 +843,8 @@ aq_status run_route(aq_layer* L, const Geom& geo, const Route& r, const void* X,
                     int64_t n, hipStream_t st, const Workspace& wk) {
     const aq_layer_desc& d = L->desc;
     const float* xs = d.x_dtype == AQ_I8 ? x_scales : nullptr;
-    const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, d.codebook_dtype};
+    const DeviceWeights w{L->d_cb,         L->d_cb32,   L->d_cbtile,      L->d_codes,
+                          L->d_codes_lut, L->d_scales, d.codebook_dtype, L->d_cb9};
     TraceScope trace(L, st);
     if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
     hipError_t e = hipSuccess;
@@ -1061,6 +1063,13 @@ aq_status aq_layer_create(const aq_layer_desc* desc, const void* codebooks, cons
     AQ_TRY(dev_upload(&L->d_cb32, nullptr, cb_elems * sizeof(float), "codebooks fp32"));
     const bool want_tile_cb = B > 8 && M == 1 && desc->tile_dtype != AQ_F32;
     if (want_tile_cb) AQ_TRY(dev_upload(&L->d_cbtile, nullptr, cb_elems * 2, "codebook tile"));
+    if (g == 9 && desc->codebook_dtype == AQ_F16) {
+        // 18-byte codewords padded to 32 bytes: one 16- and one 4-byte load each
+        std::vector<uint16_t> pad((size_t)M * nk * 16, 0);
+        const uint16_t* src = static_cast<const uint16_t*>(codebooks);
+        for (size_t r = 0; r < (size_t)M * nk; ++r) std::memcpy(&pad[r * 16], src + r * 9, 9 * sizeof(uint16_t));
+        AQ_TRY(dev_upload(&L->d_cb9, pad.data(), pad.size() * sizeof(uint16_t), "padded codebooks"));
+    }
     AQ_TRY(dev_upload(&L->d_codes, codes, code_bytes, "codes"));
     AQ_TRY(dev_upload(&L->d_scales, scales, (size_t)C_out * sizeof(float), "scales"));
 
@@ -1186,7 +1195,8 @@ aq_status aq_layer_prepare(aq_layer* L, int64_t n, void* stream) {
                      r.fp.dec == aq::FUSED_DEC_REC;
     if (!rec) return AQ_OK;                      // nothing of this forward depends on the weights alone
     const aq_layer_desc& d = L->desc;
-    const DeviceWeights w{L->d_cb, L->d_cb32, L->d_cbtile, L->d_codes, L->d_codes_lut, L->d_scales, d.codebook_dtype};
+    const DeviceWeights w{L->d_cb,         L->d_cb32,   L->d_cbtile,      L->d_codes,
+                          L->d_codes_lut, L->d_scales, d.codebook_dtype, L->d_cb9};
     const hipError_t e = aq::launch_operand_records(geo, r.fp, w, L->d_wrec, st);
     if (e != hipSuccess) return hip_fail(e, "records launch");
     if (trace.error() != hipSuccess) return hip_fail(trace.error(), "launch event");
