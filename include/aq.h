@@ -222,9 +222,11 @@ aq_status aq_layer_set_path(aq_layer* layer, aq_path path);
  *   AQ_OPT_FUSED_TILE       fused kernel tile BM * 1000 + BN (0 = planner);
  *                           a tile that does not fit falls back to the planner
  *   AQ_OPT_DENSE_TILE       dense product tile BM * 1000 + BN (0 = planner)
- *   AQ_OPT_REC_LINEAR_TILE  wave-split linear kernel: 0 = 128 x 128 in 2 x 2
- *                           waves, 1 = 256 x 128 in 2 x 2, 2 = 128 x 128 in
- *                           1 x 4 (bit-identical outputs)
+ *   AQ_OPT_REC_LINEAR_TILE  wave-split linear kernel: 0 = planner (128 x 128
+ *                           with the four waves side by side along the
+ *                           channels), 1 = 256 x 128 in 2 x 2 waves, 2 = 128 x
+ *                           128 side by side, 3 = 128 x 128 in 2 x 2
+ *                           (bit-identical outputs)
  *   AQ_OPT_TILE_ORDER       workgroup order: 0 auto, 1 token tiles slowest,
  *                           2 channel tiles slowest (bit-identical outputs)
  *   AQ_OPT_STAGE_ROWS       convolution staging: 0 each input row once per

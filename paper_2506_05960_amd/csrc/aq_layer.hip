@@ -1401,7 +1401,7 @@ aq_status aq_layer_set_option(aq_layer* L, int32_t option, int64_t value) {
     case AQ_OPT_DENSE_TILE:
         return tile(&o.dense_bm, &o.dense_bn) ? AQ_OK : bad();
     case AQ_OPT_REC_LINEAR_TILE:
-        if (!in(0, 2)) return bad();
+        if (!in(0, 3)) return bad();
         o.rlin_tile = (int)value;
         return AQ_OK;
     case AQ_OPT_TILE_ORDER:

@@ -377,14 +377,18 @@ bool rec_linear_supported(const Geom& geo, const FusedPlan& plan, int x_dtype) {
 
 // Tile variant: 0 = 128 x 128 in a 2 x 2 wave split, 1 = 256 x 128 in a 2 x 2
 // split, 2 = 128 x 128 with the four waves side by side along the channels.
+// `forced` is the option value (0 planner, 1 = variant 1, 2 = variant 2,
+// 3 = variant 0).  The planner takes variant 2: each wave then reads one
+// channel block of records and all four token blocks of the activations per
+// step, and measured 3-6 % faster than the 2 x 2 split on every linear shape
+// here (U-Net 8192 tokens x 384 -> 1152: 19.2 vs 20.2 us per forward; 8192 x
+// 576 -> 1728 int8: 29.4-31.5 vs 31.3-33.3 us); the 256-token tile is slower
+// (one workgroup per compute unit).
 int rec_linear_tile(const Geom& geo, int forced) {
-    if (forced >= 1 && forced <= 2) return forced;
-    // The 128-token tiles fit 256 registers per lane, so two workgroups share a
-    // compute unit and overlap one's prologue and epilogue with the other's
-    // products; measured faster than the 256-token tile on the 8192-token qkv
-    // layer (34.0 vs 36.2 us per forward).
     (void)geo;
-    return 0;
+    if (forced == 1 || forced == 2) return forced;
+    if (forced == 3) return 0;
+    return 2;
 }
 
 hipError_t launch_rec_linear(const Geom& geo, const FusedPlan& plan, const FusedLaunch& fl) {

@@ -610,12 +610,13 @@ def test_rec_linear_tiles(spec):
     inp = generate(spec, 41)
     y_ref = O.forward(spec, inp)
     ys = {}
-    for tile, var in (("256", 1), ("128", 0), ("128w", 2)):
+    for tile, var in (("256", 1), ("128", 3), ("128w", 2), ("auto", 0)):
         ys[tile] = _run(spec, inp, "decode", opts={"weights": 2, "rec_linear_tile": var})
         err = O.rel_err_inf(ys[tile], y_ref)
         _say(f"rec linear {spec.name} tile {tile} err={err:.3e}")
         assert err <= 2e-3
     assert np.array_equal(ys["256"], ys["128"]) and np.array_equal(ys["128w"], ys["128"])
+    assert np.array_equal(ys["auto"], ys["128"])
 
 
 # ---------------------------------------------------------------------------
