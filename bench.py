@@ -246,10 +246,10 @@ def measured_traffic_kernel(workload: str, kernel: str):
     return ent.get("traffic_bytes")
 
 
-def sweep_cpu_baseline(specs, seeds, budget_s: float = 20.0):
-    """The fp64 oracle over a bounded, stratified sample of the pass's layers
-    (every 6th layer, in order, until the budget is spent), each with its own
-    weights and a seeded N(0, 1) input of the full batch."""
+def sweep_cpu_baseline(specs, seeds, budget_s: float = 25.0, stride: int = 1):
+    """The fp64 oracle over the pass's layers (every ``stride``-th, in order,
+    until the budget is spent: the whole pass takes about 16 s on 16 threads),
+    each with its own weights and a seeded N(0, 1) input of the full batch."""
     import numpy as np
 
     import oracle as O
@@ -257,7 +257,7 @@ def sweep_cpu_baseline(specs, seeds, budget_s: float = 20.0):
 
     hi = host_info()
     done, flops, t_all = [], 0, 0.0
-    for i in range(0, len(specs), 6):
+    for i in range(0, len(specs), stride):
         spec = specs[i]
         inp = W.generate(spec, seeds[i])
         t0 = time.perf_counter()
@@ -272,7 +272,8 @@ def sweep_cpu_baseline(specs, seeds, budget_s: float = 20.0):
         "unit": "TFLOP/s",
         "cores": int(hi["threads"]),
         "kind": "oracle",
-        "sample": f"{len(done)} of the pass's {len(specs)} layers (every 6th, {flops / 1e9:.1f} GFLOP): fp64 "
+        "sample": f"{len(done)} of the pass's {len(specs)} layers ({'every layer' if stride == 1 else f'every {stride}th'}"
+                  f", in order, {flops / 1e9:.1f} GFLOP): fp64 "
                   f"dequantize + im2col + BLAS matmul, one run each, {t_all:.2f} s",
         "cpu": hi["cpu"],
         "blas": hi["blas"],
@@ -322,6 +323,18 @@ def sweep_bench(a, torch, P, W):
     def run_pass():
         for _, fn in items:
             fn()
+
+    layer_objs, layer_ns = [it[0] for it in items], [sp.n for sp in specs]
+
+    def decode_all():
+        P.AQLayer.prepare_all(layer_objs, layer_ns)
+
+    def run_pass_batched():
+        # every record decode of the pass first, one launch per records kernel
+        # and 32 layers (aq_layers_prepare), then the forwards, each of which
+        # launches its product only; the decodes stay inside the timed pass
+        decode_all()
+        run_pass()
 
     side = torch.cuda.Stream()
 
@@ -374,8 +387,13 @@ def sweep_bench(a, torch, P, W):
     # --records-overlap also times the schedule that decodes records on a
     # second stream ahead of their forwards (measured slower: the replayed
     # graph's cross-stream dependencies cost more than they hide)
-    pass_us = time_graph(run_pass)
+    batched = a.records == "batched"
+    pass_us = time_graph(run_pass_batched if batched else run_pass)
+    other_us = time_graph(run_pass if batched else run_pass_batched)
     overlap_us = time_graph(run_pass_overlapped) if a.records_overlap else None
+    decode_us = time_graph(decode_all)          # the batched decodes alone
+    run_pass()                                  # consumes the preparations the last capture left pending
+    torch.cuda.synchronize()
 
     # per-launch kernel durations inside the same pass (events around every launch)
     per_layer, tmode, pass_us_ev = launch_times(torch, items)
@@ -421,7 +439,10 @@ def sweep_bench(a, torch, P, W):
             f.write(f"{len(layers)} layers, {sum(s is not None for s in src)} reading the previous layer's output; "
                     f"{total_flops / 1e9:.1f} dense-equivalent GFLOP.  Whole pass in one HIP graph: "
                     f"{pass_us:.1f} us ({total_flops / (pass_us * 1e-6) / 1e12:.1f} TFLOP/s, "
-                    f"{total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS:.3f} of 2.5 PFLOP/s).  "
+                    f"{total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS:.3f} of 2.5 PFLOP/s; "
+                    f"record decodes {'batched at the start of the pass' if batched else 'in each forward'}; "
+                    f"with them {'in each forward' if batched else 'batched'}: {other_us:.1f} us; the batched "
+                    f"decodes alone: {decode_us:.1f} us).  "
                     f"Per-layer times below: each forward alone in a HIP graph (sum "
                     f"{sum(t for lay in per_layer for _, t in lay):.1f} us), split among its launches by "
                     f"timing events (eager pass with events: {pass_us_ev:.1f} us)." +
@@ -474,11 +495,16 @@ def sweep_bench(a, torch, P, W):
                      "pass_frac": round(total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS, 4)},
         "kernels": [{"kernel": n, "launches": c, "total_us": round(t, 2)} for n, t, c, _ in ktable[:6]],
         "weights": weights,
-        "schedule": {"streams": 1,
+        "schedule": {"streams": 1, "records": a.records,
+                     "ms_per_step_records_batched": round((pass_us if batched else other_us) / 1e3, 6),
+                     "ms_per_step_records_per_forward": round((other_us if batched else pass_us) / 1e3, 6),
+                     "batched_decodes_us": round(decode_us, 2),
                      "ms_per_step_records_ahead": None if overlap_us is None else round(overlap_us / 1e3, 6),
                      "records_ahead": a.records_ahead if a.records_overlap else None,
-                     "note": "records_ahead: per-forward record decodes on a second stream, that many layers ahead "
-                             "of their forwards (aq_layer_prepare), every decode still inside the timed pass"},
+                     "note": "records batched: every record decode of the pass launched first, one launch per "
+                             "records kernel and 32 layers (aq_layers_prepare), then the forwards; per_forward: each "
+                             "forward decodes its own; records_ahead: per-forward decodes on a second stream, that "
+                             "many layers ahead (aq_layer_prepare); every decode is inside the timed pass"},
         "activation_rms": [round(min(rms), 4), round(max(rms), 4)],
     }
     if a.copy_bytes > 0:
@@ -676,6 +702,9 @@ def main(argv=None):
     ap.add_argument("--lut-m", type=int, default=0, help="lutregime: only the shapes with this M")
     ap.add_argument("--records-ahead", type=int, default=1,
                     help="sweep: layers ahead of the current forward whose records the second stream decodes")
+    ap.add_argument("--records", default="batched", choices=["batched", "per-forward"],
+                    help="sweep: the timed pass decodes every layer's records first in batched launches "
+                         "(aq_layers_prepare), or each forward decodes its own")
     ap.add_argument("--records-overlap", action="store_true",
                     help="sweep: also time the pass with record decodes on a second stream (--records-ahead)")
     ap.add_argument("--op", default="forward", choices=["forward", "grad"],

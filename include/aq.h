@@ -133,6 +133,29 @@ aq_status aq_layer_forward(aq_layer* layer, const void* X, const float* x_scales
 aq_status aq_layer_prepare(aq_layer* layer, int64_t n, void* stream);
 
 /*
+ * aq_layer_prepare for `count` layers at once: layers[i] is prepared for a
+ * forward over n[i] tokens (linear) or images (convolution).  The result, and
+ * the ordering the caller owes each layer, are those of calling
+ * aq_layer_prepare on every entry; but the record decodes of all layers whose
+ * format shares one records kernel (fp16 codebooks, g = 8 or the kernel-aware
+ * g = 9, M in {1, 2, 4}) go out as one launch per 32 layers, so that a whole
+ * network's decodes (each one short and latency-bound) fill the chip
+ * together.  Each layer's records land in its own buffer, bit-identical to
+ * its own decode.  Other formats get one launch per layer.
+ *   layers     host array [count] of layer handles, each listed at most once,
+ *              all created on the current device
+ *   n          host array [count]
+ *   count      >= 0 (0: nothing to do)
+ *   stream     the stream every decode is launched on
+ * Every entry is checked before anything is launched; errors:
+ * AQ_ERR_INVALID_ARGUMENT (null array or layer, n < 1, tokens beyond
+ * max_tokens, a layer listed twice or created on another device),
+ * AQ_ERR_DEVICE (launch failed; the layers launched before the failure stay
+ * prepared).
+ */
+aq_status aq_layers_prepare(aq_layer* const* layers, const int64_t* n, int32_t count, void* stream);
+
+/*
  * Allocation-free forward, for callers that cannot allocate device memory
  * during the call or keep per-layer workspace (code under HIP graph capture,
  * tight serving loops, harnesses that forbid allocation).  Arguments,

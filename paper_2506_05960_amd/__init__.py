@@ -14,6 +14,8 @@ from .aq import (  # noqa: F401
     aq_layer_create,
     aq_layer_forward,
     aq_layer_forward_static,
+    aq_layer_prepare,
+    aq_layers_prepare,
     aq_layer_decode,
     aq_layer_codebook_grad,
     aq_layer_set_path,

@@ -29,7 +29,8 @@ OPTION_CODES = {"lut_max_tokens": 1, "weights": 2, "generic": 3, "record_product
                 "grad_splits": 11, "grad_regs": 12, "grad_tile": 13, "table_one_launch": 14}
 _TILE_OPTIONS = ("fused_tile", "dense_tile", "grad_tile")
 
-EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_prepare", "aq_layer_decode",
+EXPORTED = ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_prepare", "aq_layers_prepare",
+            "aq_layer_decode",
             "aq_layer_codebook_grad",
             "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
             "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy",
@@ -78,6 +79,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_forward.argtypes = [vp, vp, vp, vp, i64, vp]
     lib.aq_layer_forward_static.argtypes = [vp, vp, vp, vp, i64, vp]
     lib.aq_layer_prepare.argtypes = [vp, i64, vp]
+    lib.aq_layers_prepare.argtypes = [ctypes.POINTER(vp), ctypes.POINTER(i64), i32, vp]
     lib.aq_layer_decode.argtypes = [vp, vp, vp]
     lib.aq_layer_codebook_grad.argtypes = [vp, vp, vp, i32, vp, i64, vp]
     lib.aq_layer_set_path.argtypes = [vp, i32]
@@ -88,7 +90,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.aq_layer_describe.argtypes = [vp, i64, ctypes.c_char_p, i64]
     lib.aq_layer_choose_path.argtypes = [vp, i64, ctypes.POINTER(ctypes.c_int)]
     lib.aq_layer_destroy.argtypes = [vp]
-    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_prepare", "aq_layer_decode",
+    for f in ("aq_layer_create", "aq_layer_forward", "aq_layer_forward_static", "aq_layer_prepare",
+              "aq_layers_prepare", "aq_layer_decode",
               "aq_layer_codebook_grad",
               "aq_layer_set_path", "aq_layer_set_option", "aq_layer_get_option", "aq_layer_set_launch_events",
               "aq_layer_last_launches", "aq_layer_describe", "aq_layer_choose_path", "aq_layer_destroy"):
@@ -145,6 +148,15 @@ def aq_layer_forward_static(handle: int, X: int, x_scales: int, Y: int, n: int, 
 
 def aq_layer_prepare(handle: int, n: int, stream: int) -> None:
     _check(load_library().aq_layer_prepare(handle, n, stream))
+
+
+def aq_layers_prepare(handles, ns, stream: int) -> None:
+    count = len(handles)
+    if len(ns) != count:
+        raise ValueError("one n per layer")
+    hs = (ctypes.c_void_p * max(1, count))(*handles)
+    nv = (ctypes.c_int64 * max(1, count))(*ns)
+    _check(load_library().aq_layers_prepare(hs, nv, count, stream))
 
 
 def aq_layer_decode(handle: int, W: int, stream: int) -> None:
@@ -329,6 +341,24 @@ class AQLayer:
             raise ValueError("n must be a positive int")
         st = stream if stream is not None else torch.cuda.current_stream(self.device).cuda_stream
         aq_layer_prepare(self.handle, n, st)
+
+    @staticmethod
+    def prepare_all(layers, ns=None, stream=None):
+        """``prepare`` for every layer of ``layers`` (each at its ``ns`` entry;
+        default: its spec's n) through one ``aq_layers_prepare`` call, which
+        decodes the records of layers sharing a records kernel in one launch."""
+        import torch
+        layers = list(layers)
+        ns = [lay.spec.n for lay in layers] if ns is None else list(ns)
+        if len(ns) != len(layers) or any(not isinstance(n, int) or n < 1 for n in ns):
+            raise ValueError("one positive int n per layer")
+        if not layers:
+            return
+        dev = layers[0].device
+        if any(lay.device != dev for lay in layers):
+            raise ValueError("layers on different devices")
+        st = stream if stream is not None else torch.cuda.current_stream(dev).cuda_stream
+        aq_layers_prepare([lay.handle for lay in layers], ns, st)
 
     def decode(self, out=None, stream=None):
         import torch

@@ -163,12 +163,11 @@ operand_records_kernel(const void* __restrict__ cb, const CodeT* __restrict__ co
 // adds in ascending m (the same IEEE fp16 sums as above), and every load of a
 // thread is issued before any sum.
 template <typename CodeT, bool K3, int MC>
-__global__ void __launch_bounds__(256)
-operand_records_f16_kernel(const u32x4* __restrict__ cb, const CodeT* __restrict__ codes, u32x4* __restrict__ rec,
-                           int nchunk, int C_out, int Gn, int B) {
+__device__ __forceinline__ void records_f16_body(const u32x4* __restrict__ cb, const CodeT* __restrict__ codes,
+                                                 u32x4* __restrict__ rec, int nchunk, int C_out, int Gn, int B,
+                                                 int64_t idx) {   // idx: (chunk, channel, half)
     constexpr int ns = K3 ? 9 : 4;
     constexpr int NG = K3 ? 9 : 4;                 // groups a thread decodes
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // (chunk, channel, half)
     if (idx >= (int64_t)nchunk * C_out * 2) return;
     const int c = (int)(idx / (2 * C_out));
     const int rem = (int)(idx - (int64_t)c * 2 * C_out);
@@ -218,6 +217,14 @@ operand_records_f16_kernel(const u32x4* __restrict__ cb, const CodeT* __restrict
     }
 }
 
+template <typename CodeT, bool K3, int MC>
+__global__ void __launch_bounds__(256)
+operand_records_f16_kernel(const u32x4* __restrict__ cb, const CodeT* __restrict__ codes, u32x4* __restrict__ rec,
+                           int nchunk, int C_out, int Gn, int B) {
+    records_f16_body<CodeT, K3, MC>(cb, codes, rec, nchunk, C_out, Gn, B,
+                                    (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+}
+
 // Records of a 3x3 chunk in the kernel-aware format (g = 9: one group per
 // input channel's 3x3 filter) from fp16 codebooks padded to 16 values per row:
 // a codeword is one 16-byte and one 4-byte load, every load of a thread is
@@ -227,10 +234,9 @@ operand_records_f16_kernel(const u32x4* __restrict__ cb, const CodeT* __restrict
 // channels 16c + 8q + e; two threads share it, each decoding 4 channels and
 // writing its 8-byte half.
 template <typename CodeT, int MC>
-__global__ void __launch_bounds__(256)
-operand_records_g9_f16_kernel(const uint8_t* __restrict__ cbp, const CodeT* __restrict__ codes,
-                              uint8_t* __restrict__ rec, int nchunk, int C_out, int Gn, int B) {
-    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;   // (chunk, channel, half, quarter)
+__device__ __forceinline__ void records_g9_f16_body(const uint8_t* __restrict__ cbp, const CodeT* __restrict__ codes,
+                                                    uint8_t* __restrict__ rec, int nchunk, int C_out, int Gn, int B,
+                                                    int64_t idx) {   // idx: (chunk, channel, half, quarter)
     if (idx >= (int64_t)nchunk * C_out * 4) return;
     const int hq = (int)(idx & 1);
     const int64_t rid = idx >> 1;
@@ -282,6 +288,46 @@ operand_records_g9_f16_kernel(const uint8_t* __restrict__ cbp, const CodeT* __re
         const u32x2 o{(uint32_t)v[0][s] | ((uint32_t)v[1][s] << 16), (uint32_t)v[2][s] | ((uint32_t)v[3][s] << 16)};
         *reinterpret_cast<u32x2*>(rec + ((((int64_t)c * 9 + s) * C_out + n) * 2 + q) * 16 + 8 * hq) = o;
     }
+}
+
+template <typename CodeT, int MC>
+__global__ void __launch_bounds__(256)
+operand_records_g9_f16_kernel(const uint8_t* __restrict__ cbp, const CodeT* __restrict__ codes,
+                              uint8_t* __restrict__ rec, int nchunk, int C_out, int Gn, int B) {
+    records_g9_f16_body<CodeT, MC>(cbp, codes, rec, nchunk, C_out, Gn, B,
+                                   (int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+}
+
+// Batched forms: one launch decodes the records of several layers that share
+// the kernel; workgroup b belongs to the job whose range [start, next start)
+// holds it (binary search over the kernel argument, uniform per workgroup),
+// and decodes exactly what the single-layer launch's workgroup b - start does.
+__device__ __forceinline__ int record_job_of(const RecordBatch& b, uint32_t blk) {
+    int lo = 0, hi = b.count - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (b.start[mid] <= blk) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
+}
+
+template <typename CodeT, bool K3, int MC>
+__global__ void __launch_bounds__(256) operand_records_f16_batch_kernel(const RecordBatch b) {
+    const int l = record_job_of(b, blockIdx.x);
+    const RecordJob& j = b.job[l];
+    records_f16_body<CodeT, K3, MC>(static_cast<const u32x4*>(j.cb), static_cast<const CodeT*>(j.codes),
+                                    static_cast<u32x4*>(j.rec), j.nchunk, j.C_out, j.G, j.B,
+                                    (int64_t)(blockIdx.x - b.start[l]) * blockDim.x + threadIdx.x);
+}
+
+template <typename CodeT, int MC>
+__global__ void __launch_bounds__(256) operand_records_g9_f16_batch_kernel(const RecordBatch b) {
+    const int l = record_job_of(b, blockIdx.x);
+    const RecordJob& j = b.job[l];
+    records_g9_f16_body<CodeT, MC>(static_cast<const uint8_t*>(j.cb), static_cast<const CodeT*>(j.codes),
+                                   static_cast<uint8_t*>(j.rec), j.nchunk, j.C_out, j.G, j.B,
+                                   (int64_t)(blockIdx.x - b.start[l]) * blockDim.x + threadIdx.x);
 }
 
 size_t operand_record_bytes(const Geom& geo, const FusedPlan& plan) {
@@ -354,6 +400,53 @@ hipError_t launch_operand_records(const Geom& geo, const FusedPlan& plan, const 
                                   hipStream_t stream) {
     if (geo.B <= 8) return records_dispatch<uint8_t>(geo, plan, w, rec, stream);
     return records_dispatch<uint16_t>(geo, plan, w, rec, stream);
+}
+
+int records_batch_key(const Geom& geo, const FusedPlan& plan, const DeviceWeights& w) {
+    if (w.cb_dtype != AQ_F16) return -1;
+    const int mi = geo.M == 1 ? 0 : geo.M == 2 ? 1 : geo.M == 4 ? 2 : -1;
+    if (mi < 0) return -1;
+    const int c16 = geo.B > 8;
+    if (geo.g == 8 && (plan.kind == 1 || plan.cm == 4)) return ((0 * 2 + c16) * 2 + (plan.kind == 1)) * 3 + mi;
+    if (geo.g == 9 && plan.kind == 1 && w.cb9) return ((1 * 2 + c16) * 2 + 1) * 3 + mi;
+    return -1;
+}
+
+RecordJob records_batch_job(const Geom& geo, const FusedPlan& plan, const DeviceWeights& w, void* rec,
+                            uint32_t* blocks) {
+    const int64_t n = (int64_t)plan.nchunk * geo.C_out * (geo.g == 9 ? 4 : 2);   // threads
+    *blocks = (uint32_t)((n + 255) / 256);
+    return RecordJob{geo.g == 9 ? w.cb9 : w.codebooks, w.codes, rec, plan.nchunk, geo.C_out, geo.G, geo.B};
+}
+
+hipError_t launch_operand_records_batch(int key, const RecordBatch& b, hipStream_t st) {
+    if (key < 0 || key >= 24 || b.count < 1 || b.count > kRecordBatchMax) return hipErrorInvalidValue;
+    const dim3 grid(b.start[b.count]), block(256);
+    const int mi = key % 3, k3 = (key / 3) % 2, c16 = (key / 6) % 2, fam = key / 12;
+    const int MC = mi == 0 ? 1 : mi == 1 ? 2 : 4;
+#define AQ_B16(CT, K3, MC) operand_records_f16_batch_kernel<CT, K3, MC><<<grid, block, 0, st>>>(b)
+#define AQ_B9(CT, MC) operand_records_g9_f16_batch_kernel<CT, MC><<<grid, block, 0, st>>>(b)
+#define AQ_BM(CT)                                                                   \
+    if (fam == 1) {                                                                 \
+        if (MC == 1) AQ_B9(CT, 1);                                                  \
+        else if (MC == 2) AQ_B9(CT, 2);                                             \
+        else AQ_B9(CT, 4);                                                          \
+    } else if (k3) {                                                                \
+        if (MC == 1) AQ_B16(CT, true, 1);                                           \
+        else if (MC == 2) AQ_B16(CT, true, 2);                                      \
+        else AQ_B16(CT, true, 4);                                                   \
+    } else {                                                                        \
+        if (MC == 1) AQ_B16(CT, false, 1);                                          \
+        else if (MC == 2) AQ_B16(CT, false, 2);                                     \
+        else AQ_B16(CT, false, 4);                                                  \
+    }
+    if (c16) { AQ_BM(uint16_t) } else { AQ_BM(uint8_t) }
+#undef AQ_BM
+#undef AQ_B9
+#undef AQ_B16
+    if (fam == 1) note_launch(st, "operand_records_g9_f16_batch_kernel", {c16 ? 16 : 8, MC, b.count});
+    else note_launch(st, "operand_records_f16_batch_kernel", {c16 ? 16 : 8, k3, MC, b.count});
+    return hipGetLastError();
 }
 
 hipError_t launch_decode_to_global(const Geom& geo, const DeviceWeights& w, int tile_dtype, void* W,

@@ -151,6 +151,27 @@ size_t rec_gemm_lds_bytes(int kind, int bm, int bn);
 size_t operand_record_bytes(const Geom& geo, const FusedPlan& plan);
 hipError_t launch_operand_records(const Geom& geo, const FusedPlan& plan, const DeviceWeights& w, void* rec,
                                   hipStream_t stream);
+// Several layers' record decodes in one launch (aq_layers_prepare): jobs whose
+// records kernel is the same, passed by value as the kernel argument.
+struct RecordJob {
+    const void* cb;       // fp16 codebooks [M][2^B][8], or the padded g = 9 rows [M][2^B][16]
+    const void* codes;    // [C_out][G][M] uint8 | uint16
+    void* rec;            // the layer's record buffer
+    int nchunk, C_out, G, B;
+};
+constexpr int kRecordBatchMax = 32;
+struct RecordBatch {
+    int count;                              // jobs, 1 .. kRecordBatchMax
+    uint32_t start[kRecordBatchMax + 1];    // first workgroup of each job; start[count] = grid size
+    RecordJob job[kRecordBatchMax];
+};
+// Key of the records kernel of this decode (equal keys batch together), or -1
+// where that kernel has no batched form.
+int records_batch_key(const Geom& geo, const FusedPlan& plan, const DeviceWeights& w);
+// The decode as a batch job, and its workgroup count.
+RecordJob records_batch_job(const Geom& geo, const FusedPlan& plan, const DeviceWeights& w, void* rec,
+                            uint32_t* blocks);
+hipError_t launch_operand_records_batch(int key, const RecordBatch& b, hipStream_t stream);
 // Linear layer over pre-decoded operand records (plan.cm == 4): 2 x 2 wave
 // split of a 256- or 128-token by 128-channel tile, no K split.
 bool rec_linear_supported(const Geom& geo, const FusedPlan& plan, int x_dtype);

@@ -1204,6 +1204,93 @@ aq_status aq_layer_prepare(aq_layer* L, int64_t n, void* stream) {
     return AQ_OK;
 }
 
+aq_status aq_layers_prepare(aq_layer* const* layers, const int64_t* n, int32_t count, void* stream) {
+    if (count < 0) return fail(AQ_ERR_INVALID_ARGUMENT, "count < 0");
+    if (count == 0) return AQ_OK;
+    if (!layers || !n) return fail(AQ_ERR_INVALID_ARGUMENT, "null layer or n array");
+    for (int32_t i = 0; i < count; ++i) {
+        const std::string at = " (entry " + std::to_string(i) + ")";
+        if (!layers[i]) return fail(AQ_ERR_INVALID_ARGUMENT, "null layer" + at);
+        if (n[i] < 1) return fail(AQ_ERR_INVALID_ARGUMENT, "n must be >= 1" + at);
+        for (int32_t j = 0; j < i; ++j)
+            if (layers[j] == layers[i]) return fail(AQ_ERR_INVALID_ARGUMENT, "layer listed twice" + at);
+    }
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    struct Item {
+        aq_layer* L;
+        int64_t n;
+        Geom geo;
+        Route r;
+        int key;
+    };
+    std::vector<Item> items;
+    items.reserve((size_t)count);
+    // every argument is checked before anything is launched
+    for (int32_t i = 0; i < count; ++i) {
+        aq_layer* L = layers[i];
+        const std::string at = " (entry " + std::to_string(i) + ")";
+        if (L->device != dev) return fail(AQ_ERR_INVALID_ARGUMENT, "layer created on another device" + at);
+        const Geom geo = make_geom(L, n[i]);
+        if (geo.tokens > L->desc.max_tokens) return fail(AQ_ERR_INVALID_ARGUMENT, "tokens exceed max_tokens" + at);
+        items.push_back(Item{L, n[i], geo, plan_route(L, geo), -1});
+    }
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    std::vector<int> keys;                     // batched kernels in order of first use
+    for (Item& it : items) {
+        it.L->prepared_n = 0;
+        const bool rec = (it.r.kind == Route::FUSED || it.r.kind == Route::REC_LINEAR || it.r.kind == Route::DENSE) &&
+                         it.r.fp.dec == aq::FUSED_DEC_REC;
+        if (!rec) continue;
+        aq_layer* L = it.L;
+        const DeviceWeights w{L->d_cb,         L->d_cb32,   L->d_cbtile,      L->d_codes,
+                              L->d_codes_lut, L->d_scales, L->desc.codebook_dtype, L->d_cb9};
+        it.key = aq::records_batch_key(it.geo, it.r.fp, w);
+        if (it.key < 0) {                       // no batched form: the layer's own launch
+            e = aq::launch_operand_records(it.geo, it.r.fp, w, L->d_wrec, st);
+            if (e != hipSuccess) return hip_fail(e, "records launch");
+            L->prepared_n = it.n;
+            it.key = -2;
+            continue;
+        }
+        if (std::find(keys.begin(), keys.end(), it.key) == keys.end()) keys.push_back(it.key);
+    }
+    for (int key : keys) {
+        aq::RecordBatch b{};
+        std::vector<Item*> members;
+        auto flush = [&]() -> aq_status {
+            if (b.count == 0) return AQ_OK;
+            const hipError_t fe = aq::launch_operand_records_batch(key, b, st);
+            if (fe != hipSuccess) return hip_fail(fe, "batched records launch");
+            for (Item* m : members) m->L->prepared_n = m->n;
+            b = aq::RecordBatch{};
+            members.clear();
+            return AQ_OK;
+        };
+        for (Item& it : items) {
+            if (it.key != key) continue;
+            aq_layer* L = it.L;
+            const DeviceWeights w{L->d_cb,         L->d_cb32,   L->d_cbtile,      L->d_codes,
+                                  L->d_codes_lut, L->d_scales, L->desc.codebook_dtype, L->d_cb9};
+            uint32_t blocks = 0;
+            const aq::RecordJob job = aq::records_batch_job(it.geo, it.r.fp, w, L->d_wrec, &blocks);
+            if (b.count == aq::kRecordBatchMax ||
+                (uint64_t)b.start[b.count] + blocks > (uint64_t)INT32_MAX) {
+                const aq_status fs = flush();
+                if (fs != AQ_OK) return fs;
+            }
+            b.job[b.count] = job;
+            b.start[b.count + 1] = b.start[b.count] + blocks;
+            ++b.count;
+            members.push_back(&it);
+        }
+        const aq_status fs = flush();
+        if (fs != AQ_OK) return fs;
+    }
+    return AQ_OK;
+}
+
 aq_status aq_layer_forward_static(aq_layer* L, const void* X, const float* x_scales, void* Y, int64_t n,
                                   void* stream) {
     Route r;

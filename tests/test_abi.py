@@ -166,6 +166,21 @@ def test_null_handles_are_rejected():
     assert lib.aq_layer_describe(None, 4, buf, 64) == A.AQ_ERR_INVALID_ARGUMENT
     assert lib.aq_layer_set_launch_events(None, None, 0) == A.AQ_ERR_INVALID_ARGUMENT
     assert lib.aq_layer_prepare(None, 1, None) == A.AQ_ERR_INVALID_ARGUMENT
+    # the batched prepare checks its arrays and entries before touching the device
+    assert lib.aq_layers_prepare(None, None, 0, None) == A.AQ_OK
+    assert lib.aq_layers_prepare(None, None, -1, None) == A.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layers_prepare(None, None, 1, None) == A.AQ_ERR_INVALID_ARGUMENT
+    hs = (ctypes.c_void_p * 2)(None, None)
+    ns = (ctypes.c_int64 * 2)(1, 1)
+    assert lib.aq_layers_prepare(hs, ns, 2, None) == A.AQ_ERR_INVALID_ARGUMENT
+    fake = ctypes.create_string_buffer(16)            # never dereferenced: the duplicate is refused first
+    hs = (ctypes.c_void_p * 2)(ctypes.addressof(fake), ctypes.addressof(fake))
+    assert lib.aq_layers_prepare(hs, ns, 2, None) == A.AQ_ERR_INVALID_ARGUMENT
+    assert b"twice" in lib.aq_last_error()
+    ns = (ctypes.c_int64 * 2)(1, 0)
+    hs = (ctypes.c_void_p * 2)(ctypes.addressof(fake), ctypes.addressof(fake) + 8)
+    assert lib.aq_layers_prepare(hs, ns, 2, None) == A.AQ_ERR_INVALID_ARGUMENT
+    assert b"n must be" in lib.aq_last_error()
     n = ctypes.c_int32()
     assert lib.aq_layer_last_launches(None, ctypes.byref(n), buf, 64) == A.AQ_ERR_INVALID_ARGUMENT
 

@@ -469,6 +469,89 @@ def test_prepare_decodes_records_ahead(spec, opts, product):
     layer.close()
 
 
+def _prepare_batch_cases():
+    cases = [(c[0], c[1]) for c in PREPARE]
+    cases += [(k, {}) for k in KAQ]                                   # g = 9 records, batched
+    cases += [
+        (LayerSpec(name="pb_b16", C_out=150, K=48 * 9, g=8, M=1, B=16, n=5, conv=ConvGeom(48, 3, 3, 1, 1, 8, 8)),
+         {"weights": 2}),                                              # 16-bit codes, batched
+        (LayerSpec(name="pb_m3", C_out=72, K=256, g=8, M=3, B=8, n=300), {}),          # no batched form
+        (LayerSpec(name="pb_m3c", C_out=96, K=32 * 9, g=8, M=3, B=8, n=2,
+                   conv=ConvGeom(32, 3, 3, 1, 1, 12, 12)), {}),                        # another route
+        (LayerSpec(name="pb_bf16", C_out=96, K=32 * 9, g=8, M=2, B=8, n=2, codebook_dtype="bf16",
+                   conv=ConvGeom(32, 3, 3, 1, 1, 12, 12)), {}),                        # a route without records
+    ]
+    # more linear layers of one records kernel than one launch takes (32)
+    cases += [(LayerSpec(name=f"pb_lin{i}", C_out=64 + 16 * (i % 3), K=128 + 64 * (i % 2), g=8, M=2, B=8, n=40 + i),
+               {"weights": 2}) for i in range(35)]
+    return cases
+
+
+def test_prepare_all_batches_record_decodes():
+    """aq_layers_prepare over layers of several formats (batched g = 8 and g = 9 records kernels, 16-bit codes,
+    formats without a batched form, routes without records, more layers of one kernel than one launch takes):
+    every forward after it launches only its product and gives its plain forward's bits, eagerly and replayed
+    from a graph with eager forwards in between."""
+    import paper_2506_05960_amd as P
+    layers, xs, refs, plain, recs = [], [], [], [], []
+    for i, (spec, opts) in enumerate(_prepare_batch_cases()):
+        inp = generate(spec, 600 + i)
+        layer = P.AQLayer(spec, inp)
+        for k, v in opts.items():
+            layer.set_option(k, v)
+        x = _dev(inp["x"], spec.x_dtype)
+        refs.append(layer.forward(x).clone())
+        plain.append(layer.last_launches()[0])
+        recs.append(layer.describe(spec.n).get("weights") == "records")
+        layers.append(layer)
+        xs.append(x)
+    torch.cuda.synchronize()
+    names = [lay.spec.name for lay in layers]
+    _say(f"prepare_all: {len(layers)} layers, {sum(recs)} on records: "
+         f"{[n for n, r in zip(names, recs) if not r]} without")
+    for must in ("kaq_m2", "kaq_m1_b12", "pb_b16", "pb_m3", "pb_lin0", "pb_lin34", "prep_lin"):
+        assert recs[names.index(must)], must
+    assert not recs[names.index("prep_in_loop")] and not recs[names.index("pb_bf16")]
+    P.AQLayer.prepare_all(layers)
+    for i, (layer, x) in enumerate(zip(layers, xs)):
+        y = layer.forward(x)
+        n_fwd, kn = layer.last_launches()
+        assert n_fwd == plain[i] - (1 if recs[i] else 0), (names[i], n_fwd, plain[i], kn)
+        assert torch.equal(y, refs[i]), names[i]
+    torch.cuda.synchronize()
+    # a second batch with every other layer only: the rest decode their own records
+    P.AQLayer.prepare_all(layers[::2])
+    for i, (layer, x) in enumerate(zip(layers, xs)):
+        y = layer.forward(x)
+        assert layer.last_launches()[0] == plain[i] - (1 if recs[i] and i % 2 == 0 else 0), names[i]
+        assert torch.equal(y, refs[i]), names[i]
+    # captured in one graph (one batched prepare, then every forward), replayed with eager forwards between
+    outs = [torch.zeros_like(r) for r in refs]
+    main = torch.cuda.current_stream()
+    cap = torch.cuda.Stream()
+    cap.wait_stream(main)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            P.AQLayer.prepare_all(layers, stream=cap.cuda_stream)
+            for layer, x, o in zip(layers, xs, outs):
+                layer.forward(x, out=o)
+    main.wait_stream(cap)
+    for rep in range(3):
+        for o in outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, o in enumerate(outs):
+            assert torch.equal(o, refs[i]), (rep, names[i])
+        j = rep * 7 % len(layers)
+        assert torch.equal(layers[j].forward(xs[j]), refs[j])
+        torch.cuda.synchronize()
+    for layer in layers:
+        layer.close()
+
+
 GEMM_CASES = [
     LayerSpec(name="g_conv3", C_out=200, K=32 * 9, g=8, M=2, B=8, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 24, 16)),
     LayerSpec(name="g_conv3_img8", C_out=150, K=48 * 9, g=8, M=1, B=16, n=5, conv=ConvGeom(48, 3, 3, 1, 1, 8, 8)),
