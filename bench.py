@@ -280,6 +280,41 @@ def sweep_cpu_baseline(specs, seeds, budget_s: float = 25.0, stride: int = 1):
     }
 
 
+def run_pass_branches(torch, fns, branch, side, first=None):
+    """Launch one U-Net pass: ``fns[i]()`` queues layer i's forward on the
+    current stream.  A layer that reads an earlier layer's input
+    (``branch[i] = j``: a residual block's skip convolution reads the block
+    input, as its first 3x3 convolution j does) goes to the ``side`` stream as
+    soon as that input is ready (just before layer j), and the next layer in
+    order that is not such a branch waits for it; every other layer runs in
+    order on the current stream.  ``first()`` (say, the batched record
+    decodes) runs before anything else, and both streams start after it."""
+    main = torch.cuda.current_stream()
+    if first is not None:
+        first()
+    starts = {}
+    for i, j in enumerate(branch):
+        if j is not None:
+            starts.setdefault(j, []).append(i)
+    joins = []                                   # (first layer that waits, event)
+    for i, fn in enumerate(fns):
+        for k in starts.get(i, ()):
+            side.wait_stream(main)
+            with torch.cuda.stream(side):
+                fns[k]()
+            ev = torch.cuda.Event()
+            ev.record(side)
+            joins.append((k + 1, ev))
+        if branch[i] is not None:
+            continue
+        for t, ev in [je for je in joins if je[0] <= i]:
+            main.wait_event(ev)
+        joins = [je for je in joins if je[0] > i]
+        fn()
+    for _, ev in joins:
+        main.wait_event(ev)
+
+
 def sweep_bench(a, torch, P, W):
     """The LDM-4-shaped U-Net pass at batch 8: every quantized layer, chained.
 
@@ -295,6 +330,7 @@ def sweep_bench(a, torch, P, W):
     M = {"W2": 2, "W4": 4, "W2K": 2, "W4K": 4}[a.variant]
     kaq = a.variant.endswith("K")       # 3x3 convolutions in the kernel-aware format (g = 9)
     src = W.chain_sources(layers, batch=8)
+    branch = W.branch_inputs(layers)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(W.SEED_BASE + 4)
     specs, seeds, objs, items = [], [], [], []
@@ -306,7 +342,10 @@ def sweep_bench(a, torch, P, W):
         wts = W.generate(spec.with_n(1), seed)         # weights are drawn before activations
         layer = P.AQLayer(spec, wts, max_tokens=spec.tokens)
         xshape = layer.in_shape(spec.n)
-        if src[i] is not None:
+        if branch[i] is not None:
+            x = objs[branch[i]][1]                     # the block input, which its first conv reads too
+            assert tuple(x.shape) == tuple(xshape), (spec.name, x.shape, xshape)
+        elif src[i] is not None:
             x = prev_y.view(xshape)
         else:
             x = torch.randn(xshape, generator=gen, device="cuda", dtype=torch.float32).to(torch.float16)
@@ -335,6 +374,14 @@ def sweep_bench(a, torch, P, W):
         # launches its product only; the decodes stay inside the timed pass
         decode_all()
         run_pass()
+
+    side_b = torch.cuda.Stream()
+    fns = [fn for _, fn in items]
+
+    def run_pass_two_streams():
+        # the batched decodes, then the pass with every residual skip
+        # convolution on a second stream beside its block's 3x3 convolutions
+        run_pass_branches(torch, fns, branch, side_b, first=decode_all)
 
     side = torch.cuda.Stream()
 
@@ -388,8 +435,10 @@ def sweep_bench(a, torch, P, W):
     # second stream ahead of their forwards (measured slower: the replayed
     # graph's cross-stream dependencies cost more than they hide)
     batched = a.records == "batched"
-    pass_us = time_graph(run_pass_batched if batched else run_pass)
+    serial_us = time_graph(run_pass_batched if batched else run_pass)
     other_us = time_graph(run_pass if batched else run_pass_batched)
+    two_us = time_graph(run_pass_two_streams) if batched else None
+    pass_us = two_us if (batched and a.streams == 2) else serial_us
     overlap_us = time_graph(run_pass_overlapped) if a.records_overlap else None
     decode_us = time_graph(decode_all)          # the batched decodes alone
     run_pass()                                  # consumes the preparations the last capture left pending
@@ -436,12 +485,17 @@ def sweep_bench(a, torch, P, W):
             f.write(f"# U-Net pass, batch 8, {a.variant} ({fmt}, M={M}, B=8), fp16, chained\n\n")
             f.write(f"Command: `python bench.py --config sweep --variant {a.variant}"
                     f"{' --full' if a.full else ''} --table <this file>`\n\n")
-            f.write(f"{len(layers)} layers, {sum(s is not None for s in src)} reading the previous layer's output; "
+            f.write(f"{len(layers)} layers, {sum(s is not None and b is None for s, b in zip(src, branch))} reading the "
+                    f"previous layer's output, {sum(b is not None for b in branch)} (residual skips) their block's "
+                    f"input; "
                     f"{total_flops / 1e9:.1f} dense-equivalent GFLOP.  Whole pass in one HIP graph: "
                     f"{pass_us:.1f} us ({total_flops / (pass_us * 1e-6) / 1e12:.1f} TFLOP/s, "
                     f"{total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS:.3f} of 2.5 PFLOP/s; "
-                    f"record decodes {'batched at the start of the pass' if batched else 'in each forward'}; "
-                    f"with them {'in each forward' if batched else 'batched'}: {other_us:.1f} us; the batched "
+                    f"record decodes {'batched at the start of the pass' if batched else 'in each forward'}"
+                    f"{', residual skip convolutions on a second stream' if pass_us == two_us else ''}; "
+                    + (f"all on one stream: {serial_us:.1f} us; " if pass_us == two_us else
+                       f"residual skips on a second stream: {two_us:.1f} us; " if two_us is not None else "")
+                    + f"with the decodes {'in each forward' if batched else 'batched'}: {other_us:.1f} us; the batched "
                     f"decodes alone: {decode_us:.1f} us).  "
                     f"Per-layer times below: each forward alone in a HIP graph (sum "
                     f"{sum(t for lay in per_layer for _, t in lay):.1f} us), split among its launches by "
@@ -467,7 +521,8 @@ def sweep_bench(a, torch, P, W):
                 us = sum(t for _, t in per_layer[i])
                 ks = " + ".join(f"`{n.split('<')[0]}` {t:.1f}" for n, t in per_layer[i])
                 f.write(f"| {sp.name} | {lay.kind}{' s2' if lay.stride == 2 else ''} | {sp.tokens} | {sp.K} | "
-                        f"{sp.C_out} | {'prev' if src[i] is not None else 'own'} | {ks} | {us:.2f} | "
+                        f"{sp.C_out} | {'block input' if branch[i] is not None else 'prev' if src[i] is not None else 'own'}"
+                        f" | {ks} | {us:.2f} | "
                         f"{sp.dense_flops / (us * 1e-6) / 1e12:.1f} | {rms[i]:.3f} |\n")
     out = {
         "metric": "dense-equivalent TFLOP/s of the AQ layer forward",
@@ -483,7 +538,9 @@ def sweep_bench(a, torch, P, W):
         "dtype": "f16",
         "data": "synthetic (seeded; LDM-4-shaped U-Net layers at batch 8, random codebooks/codes/activations, "
                 "chained where shapes allow)",
-        "config": {"workload": workload, "layers": len(layers), "chained_inputs": sum(s is not None for s in src),
+        "config": {"workload": workload, "layers": len(layers),
+                   "chained_inputs": sum(s is not None and b is None for s, b in zip(src, branch)),
+                   "branch_inputs": sum(b is not None for b in branch),
                    "launch": "hip graph of the whole pass", "format": f"{a.variant}: g={9 if kaq else 8}/8, M={M}, B=8"},
         "hbm_gbs_algorithmic": round(total_bytes / (pass_us * 1e-6) / 1e9, 3),
         "algorithmic_bytes": total_bytes,
@@ -495,9 +552,10 @@ def sweep_bench(a, torch, P, W):
                      "pass_frac": round(total_flops / (pass_us * 1e-6) / 1e12 / PEAK_MFMA_F16_TFLOPS, 4)},
         "kernels": [{"kernel": n, "launches": c, "total_us": round(t, 2)} for n, t, c, _ in ktable[:6]],
         "weights": weights,
-        "schedule": {"streams": 1, "records": a.records,
-                     "ms_per_step_records_batched": round((pass_us if batched else other_us) / 1e3, 6),
-                     "ms_per_step_records_per_forward": round((other_us if batched else pass_us) / 1e3, 6),
+        "schedule": {"streams": 2 if pass_us == two_us else 1, "records": a.records,
+                     "ms_per_step_two_streams": None if two_us is None else round(two_us / 1e3, 6),
+                     "ms_per_step_records_batched": round((serial_us if batched else other_us) / 1e3, 6),
+                     "ms_per_step_records_per_forward": round((other_us if batched else serial_us) / 1e3, 6),
                      "batched_decodes_us": round(decode_us, 2),
                      "ms_per_step_records_ahead": None if overlap_us is None else round(overlap_us / 1e3, 6),
                      "records_ahead": a.records_ahead if a.records_overlap else None,
@@ -705,6 +763,11 @@ def main(argv=None):
     ap.add_argument("--records", default="batched", choices=["batched", "per-forward"],
                     help="sweep: the timed pass decodes every layer's records first in batched launches "
                          "(aq_layers_prepare), or each forward decodes its own")
+    ap.add_argument("--streams", type=int, default=1, choices=[1, 2],
+                    help="sweep: the timed pass in layer order on one stream (1), or with every residual skip "
+                         "convolution on a second stream beside its block's 3x3 convolutions (2, with --records "
+                         "batched; measured slower: the graph's cross-stream edges cost more than the overlap "
+                         "hides); both are always timed and reported")
     ap.add_argument("--records-overlap", action="store_true",
                     help="sweep: also time the pass with record decodes on a second stream (--records-ahead)")
     ap.add_argument("--op", default="forward", choices=["forward", "grad"],

@@ -80,3 +80,20 @@ def test_sweep_specs_are_valid():
             assert s.K % s.g == 0
             if s.conv is not None:
                 assert s.conv.OH == l.res // l.stride
+
+
+def test_branch_inputs_are_the_residual_skips():
+    """Every residual skip convolution (and nothing else) shares the input of its block's first 3x3 convolution,
+    which comes before it and has the same input shape."""
+    for full in (False, True):
+        layers = W.sweep_layers(full)
+        br = W.branch_inputs(layers)
+        assert [i for i, j in enumerate(br) if j is not None] == [i for i, l in enumerate(layers) if l.role == "res_skip"]
+        assert sum(j is not None for j in br) == 15
+        for i, j in enumerate(br):
+            if j is None:
+                continue
+            a, b = layers[i], layers[j]
+            assert j < i and b.name == a.name.rsplit(".", 1)[0] + ".conv1" and b.kind == "conv3x3"
+            assert (a.cin, a.res, a.stride) == (b.cin, b.res, b.stride)
+            assert W.sweep_io_elems(a, 8)[0] == W.sweep_io_elems(b, 8)[0]

@@ -17,6 +17,7 @@ from .layers import (  # noqa: F401
     sweep_spec,
     sweep_io_elems,
     chain_sources,
+    branch_inputs,
     chain_codebook_std,
     lut_regime_specs,
     SEED_BASE,

@@ -389,6 +389,24 @@ def chain_sources(layers: List[SweepLayer], batch: int = 8) -> List[Optional[int
     return src
 
 
+def branch_inputs(layers: List[SweepLayer]) -> List[Optional[int]]:
+    """For a chained pass over ``layers``: entry i is the index of the earlier
+    layer whose input buffer layer i reads too, else None.  A residual block's
+    1x1 skip convolution reads the block's input, as the block's first 3x3
+    convolution does; it depends on nothing in between, so it may run
+    concurrently with the block's two 3x3 convolutions, and the layer after
+    it (which reads the block's output, the sum of the two branches) waits for
+    both."""
+    idx = {lay.name: i for i, lay in enumerate(layers)}
+    out: List[Optional[int]] = []
+    for lay in layers:
+        if lay.role == "res_skip":
+            out.append(idx[lay.name.rsplit(".", 1)[0] + ".conv1"])
+        else:
+            out.append(None)
+    return out
+
+
 def chain_codebook_std(M: int, K: int) -> float:
     """Codebook standard deviation that keeps a chained layer's output at unit
     scale for unit-scale input: with scales U(0.5, 1.5) (mean square 13/12),
