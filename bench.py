@@ -280,6 +280,28 @@ def sweep_cpu_baseline(specs, seeds, budget_s: float = 25.0, stride: int = 1):
     }
 
 
+def dense_gemm_reference(torch, specs, gen):
+    """Each layer of a pass as a dense fp16 GEMM through torch.matmul (hipBLASLt):
+    [tokens, K] x [K, C_out] with the weights stored [C_out, K] (the faster of
+    the two weight layouts there), seeded N(0, 1) operands, fp16 output, im2col
+    not counted.  A comparator for what unquantized fp16 weights cost in the
+    vendor library on the same shapes, not a step of the method.  Returns the
+    per-layer matmul callables."""
+    mx_a = max(sp.tokens * sp.K for sp in specs)
+    mx_w = max(sp.K * sp.C_out for sp in specs)
+    mx_y = max(sp.tokens * sp.C_out for sp in specs)
+    A = torch.randn(mx_a, generator=gen, device="cuda", dtype=torch.float16)
+    Wt = torch.randn(mx_w, generator=gen, device="cuda", dtype=torch.float16)
+    Yd = torch.empty(mx_y, device="cuda", dtype=torch.float16)
+    fns = []
+    for sp in specs:
+        a = A[:sp.tokens * sp.K].view(sp.tokens, sp.K)
+        w = Wt[:sp.C_out * sp.K].view(sp.C_out, sp.K)
+        y = Yd[:sp.tokens * sp.C_out].view(sp.tokens, sp.C_out)
+        fns.append(lambda a=a, w=w, y=y: torch.matmul(a, w.t(), out=y))
+    return fns
+
+
 def run_pass_branches(torch, fns, branch, side, first=None):
     """Launch one U-Net pass: ``fns[i]()`` queues layer i's forward on the
     current stream.  A layer that reads an earlier layer's input
@@ -447,6 +469,18 @@ def sweep_bench(a, torch, P, W):
     # per-launch kernel durations inside the same pass (events around every launch)
     per_layer, tmode, pass_us_ev = launch_times(torch, items)
 
+    # the same products as dense fp16 GEMMs in the vendor library (comparator)
+    dense_ref = None
+    if not a.no_dense_ref:
+        dfns = dense_gemm_reference(torch, specs, gen)
+        dense_pass_us = time_graph(lambda: [f() for f in dfns])
+        dense_layer_us = [_graph_time_us(torch, f, reps=10) for f in dfns]
+        dense_ref = {"kind": "torch.matmul fp16 (hipBLASLt): every layer's [tokens x K] x [K x C_out] product, "
+                             "seeded N(0, 1) operands, weights stored [C_out, K], im2col not counted",
+                     "ms_per_step": round(dense_pass_us / 1e3, 6),
+                     "value": round(total_flops / (dense_pass_us * 1e-6) / 1e12, 3),
+                     "aq_pass_speedup": round(dense_pass_us / pass_us, 3)}
+
     # weight source of every forward: in-loop decode (W never in memory), records
     # (the decompress-then-compute route: unscaled fp16 W written and read back
     # every forward) or the table path; then the same pass with the in-loop
@@ -508,6 +542,10 @@ def sweep_bench(a, torch, P, W):
                     f"; records written and read back per pass: {rec_bytes / 1e6:.1f} MB.  The same pass with the "
                     f"in-loop decode forced wherever the format has one ({n_inloop} of {len(items)} layers; W never in "
                     f"memory): {inloop_us:.1f} us ({total_flops / (inloop_us * 1e-6) / 1e12:.1f} TFLOP/s).\n\n")
+            if dense_ref is not None:
+                f.write(f"Dense fp16 comparator ({dense_ref['kind']}): the pass's products in one graph "
+                        f"{dense_pass_us:.1f} us ({dense_ref['value']:.1f} TFLOP/s); the AQ pass is "
+                        f"{dense_ref['aq_pass_speedup']:.2f}x that speed.\n\n")
             f.write("Per kernel (sum over the pass):\n\n| kernel | launches | total us | share | TFLOP/s |\n"
                     "|---|---|---|---|---|\n")
             ksum = sum(r[1] for r in ktable)
@@ -515,15 +553,16 @@ def sweep_bench(a, torch, P, W):
                 f.write(f"| `{n}` | {c} | {t:.1f} | {t / ksum:.3f} | "
                         f"{(fl / (t * 1e-6) / 1e12) if fl else 0:.1f} |\n")
             f.write("\nPer layer (kernels in launch order, us each):\n\n"
-                    "| layer | kind | tokens | K | C_out | input | launches | us | TFLOP/s | out rms |\n"
-                    "|---|---|---|---|---|---|---|---|---|---|\n")
+                    "| layer | kind | tokens | K | C_out | input | launches | us | TFLOP/s | out rms | dense fp16 GEMM us |\n"
+                    "|---|---|---|---|---|---|---|---|---|---|---|\n")
             for i, (lay, sp) in enumerate(zip(layers, specs)):
                 us = sum(t for _, t in per_layer[i])
                 ks = " + ".join(f"`{n.split('<')[0]}` {t:.1f}" for n, t in per_layer[i])
                 f.write(f"| {sp.name} | {lay.kind}{' s2' if lay.stride == 2 else ''} | {sp.tokens} | {sp.K} | "
                         f"{sp.C_out} | {'block input' if branch[i] is not None else 'prev' if src[i] is not None else 'own'}"
                         f" | {ks} | {us:.2f} | "
-                        f"{sp.dense_flops / (us * 1e-6) / 1e12:.1f} | {rms[i]:.3f} |\n")
+                        f"{sp.dense_flops / (us * 1e-6) / 1e12:.1f} | {rms[i]:.3f} | "
+                        f"{'' if dense_ref is None else f'{dense_layer_us[i]:.2f}'} |\n")
     out = {
         "metric": "dense-equivalent TFLOP/s of the AQ layer forward",
         "value": round(total_flops / (pass_us * 1e-6) / 1e12, 3),
@@ -564,6 +603,7 @@ def sweep_bench(a, torch, P, W):
                              "forward decodes its own; records_ahead: per-forward decodes on a second stream, that "
                              "many layers ahead (aq_layer_prepare); every decode is inside the timed pass"},
         "activation_rms": [round(min(rms), 4), round(max(rms), 4)],
+        "dense_reference": dense_ref,
     }
     if a.copy_bytes > 0:
         src_b = torch.empty(a.copy_bytes, dtype=torch.uint8, device="cuda")
@@ -748,6 +788,8 @@ def main(argv=None):
                                                       "qkv16, conv8")
     ap.add_argument("--path", default="auto", choices=["auto", "lut", "decode"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense-ref", action="store_true",
+                    help="sweep: skip the dense fp16 GEMM comparator (torch.matmul on the same shapes)")
     ap.add_argument("--no-graph", action="store_true", help="launch every step from Python instead of a HIP graph")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="after timing, run one plain device copy of this many bytes (counter calibration)")
