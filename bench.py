@@ -429,7 +429,7 @@ def sweep_bench(a, torch, P, W):
             fn()
         main.wait_stream(side)
 
-    def time_graph(body):
+    def time_graph(body, extra_trials=0):
         stream = torch.cuda.Stream()
         stream.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(stream):
@@ -444,23 +444,28 @@ def sweep_bench(a, torch, P, W):
         for _ in range(max(0, a.warmup)):
             g.replay()
         torch.cuda.synchronize()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0.record()
-        for _ in range(a.steps):
-            g.replay()
-        t1.record()
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1) * 1e3 / a.steps
+        times = []
+        for _ in range(1 + extra_trials):
+            # the first trial is the timed steps; extra trials repeat them for the spread
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0.record()
+            for _ in range(a.steps):
+                g.replay()
+            t1.record()
+            torch.cuda.synchronize()
+            times.append(t0.elapsed_time(t1) * 1e3 / a.steps)
+        return (times[0], times) if extra_trials else times[0]
 
     # the timed steps: whole passes replayed from one graph on one stream;
     # --records-overlap also times the schedule that decodes records on a
     # second stream ahead of their forwards (measured slower: the replayed
     # graph's cross-stream dependencies cost more than they hide)
     batched = a.records == "batched"
-    serial_us = time_graph(run_pass_batched if batched else run_pass)
+    serial_us, serial_trials = time_graph(run_pass_batched if batched else run_pass, extra_trials=4)
     other_us = time_graph(run_pass if batched else run_pass_batched)
     two_us = time_graph(run_pass_two_streams) if batched else None
     pass_us = two_us if (batched and a.streams == 2) else serial_us
+    trials_us = serial_trials if pass_us == serial_us else [pass_us]
     overlap_us = time_graph(run_pass_overlapped) if a.records_overlap else None
     decode_us = time_graph(decode_all)          # the batched decodes alone
     run_pass()                                  # consumes the preparations the last capture left pending
@@ -603,6 +608,9 @@ def sweep_bench(a, torch, P, W):
                              "forward decodes its own; records_ahead: per-forward decodes on a second stream, that "
                              "many layers ahead (aq_layer_prepare); every decode is inside the timed pass"},
         "activation_rms": [round(min(rms), 4), round(max(rms), 4)],
+        "trials": {"n": len(trials_us), "median_ms": round(statistics.median(trials_us) / 1e3, 6),
+                   "min_ms": round(min(trials_us) / 1e3, 6),
+                   "note": "the timed steps, then the same steps repeated, each trial a.steps graph replays"},
         "dense_reference": dense_ref,
     }
     if a.copy_bytes > 0:
@@ -889,20 +897,24 @@ def main(argv=None):
             tail_graph = capture(tail)
     steps = a.steps
 
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    if graph is not None:
-        for _ in range(nfull):
-            graph.replay()
-        if tail_graph is not None:
-            tail_graph.replay()
-    else:
-        for _ in range(steps):
-            layer.forward(x, xs, out=y)
-    stop.record()
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(stop) / steps
+    def timed_steps():
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        if graph is not None:
+            for _ in range(nfull):
+                graph.replay()
+            if tail_graph is not None:
+                tail_graph.replay()
+        else:
+            for _ in range(steps):
+                layer.forward(x, xs, out=y)
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / steps
+
+    ms = timed_steps()
+    trials_ms = [ms] + [timed_steps() for _ in range(4)]     # the timed steps, then four repeats for the spread
 
     # The dominant kernel's own duration: timing events around every launch of
     # ten forwards in one graph (a pre-decoded forward is two launches, records
@@ -953,6 +965,9 @@ def main(argv=None):
         "algorithmic_bytes": algorithmic_bytes(spec),
         "dense_flops": flops,
         "roofline": roof,
+        "trials": {"n": len(trials_ms), "median_ms": round(statistics.median(trials_ms), 6),
+                   "min_ms": round(min(trials_ms), 6),
+                   "note": "the timed steps, then the same steps repeated four times"},
         "kernels": [{"kernel": n, "launches": c // 10, "avg_us": round(t / c, 3)} for n, t, c, _ in ktable],
     }
     if path == "decode":
