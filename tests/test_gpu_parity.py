@@ -996,3 +996,38 @@ def test_split_k_graph_replays():
         assert torch.equal(layer.forward(x), eager)
         torch.cuda.synchronize()
     layer.close()
+
+
+def test_refused_calls_launch_nothing():
+    """Calls outside a layer's limits are refused before any launch: tokens past max_tokens, n = 0 (forward,
+    prepare, batched prepare, whose every entry is checked first), and the layer's next forward is unchanged."""
+    import paper_2506_05960_amd as P
+    spec = LayerSpec(name="refuse_lin", C_out=128, K=256, g=8, M=2, B=8, n=64)
+    inp = generate(spec, 77)
+    layer = P.AQLayer(spec, inp, max_tokens=64)
+    other = P.AQLayer(spec, inp, max_tokens=64)
+    layer.set_option("weights", 2)
+    other.set_option("weights", 2)
+    x = _dev(inp["x"], spec.x_dtype)
+    ref = layer.forward(x).clone()
+    n_ref = layer.last_launches()[0]
+    torch.cuda.synchronize()
+    big = torch.zeros((65, spec.K), dtype=torch.float16, device="cuda")
+    y_big = torch.zeros((65, spec.C_out), dtype=torch.float16, device="cuda")
+    lib = P.load_library()
+    st = torch.cuda.current_stream().cuda_stream
+    assert lib.aq_layer_forward(layer.handle, big.data_ptr(), None, y_big.data_ptr(), 65, st) == P.aq.AQ_ERR_INVALID_ARGUMENT
+    assert lib.aq_layer_forward(layer.handle, x.data_ptr(), None, y_big.data_ptr(), 0, st) == P.aq.AQ_ERR_INVALID_ARGUMENT
+    with pytest.raises(P.AQError, match="INVALID_ARGUMENT"):
+        layer.prepare(65)
+    # the batched prepare refuses the whole list: the valid first entry is not prepared either
+    with pytest.raises(P.AQError, match="INVALID_ARGUMENT"):
+        P.AQLayer.prepare_all([other, layer], [64, 65])
+    y = other.forward(x)
+    assert other.last_launches()[0] == n_ref                 # decoded its own records: nothing was pending
+    torch.cuda.synchronize()
+    assert torch.equal(y, ref)
+    assert torch.count_nonzero(y_big).item() == 0            # no refused call wrote anything
+    assert torch.equal(layer.forward(x), ref) and layer.last_launches()[0] == n_ref
+    layer.close()
+    other.close()
