@@ -1031,3 +1031,54 @@ def test_refused_calls_launch_nothing():
     assert torch.equal(layer.forward(x), ref) and layer.last_launches()[0] == n_ref
     layer.close()
     other.close()
+
+
+def test_two_host_threads_forward_concurrently():
+    """Two host threads, each with its own layers and stream, create and run forwards at the same time (first
+    launches included, so the per-device kernel attribute and occupancy caches are filled concurrently); every
+    output equals the same forward run alone, and each thread's launch trace names its own kernels."""
+    import threading
+    import paper_2506_05960_amd as P
+    specs = [
+        [LayerSpec(name="thr_conv_a", C_out=192, K=64 * 9, g=8, M=2, B=8, n=2, conv=ConvGeom(64, 3, 3, 1, 1, 32, 32)),
+         LayerSpec(name="thr_lin_a", C_out=256, K=512, g=8, M=4, B=8, n=1024)],
+        [LayerSpec(name="thr_conv_b", C_out=128, K=32 * 9, g=8, M=1, B=12, n=3, conv=ConvGeom(32, 3, 3, 1, 1, 16, 16)),
+         LayerSpec(name="thr_lin_b", C_out=96, K=264, g=8, M=2, B=8, n=3)],            # 3 tokens: table path
+    ]
+    inps = [[generate(s, 700 + 10 * t + i) for i, s in enumerate(ss)] for t, ss in enumerate(specs)]
+    results, errors, names = [None, None], [], [None, None]
+
+    def work(t):
+        try:
+            torch.cuda.set_device(0)
+            st = torch.cuda.Stream()
+            out, nm = [], []
+            with torch.cuda.stream(st):
+                for s, inp in zip(specs[t], inps[t]):
+                    layer = P.AQLayer(s, inp)
+                    if s.name == "thr_lin_b":
+                        layer.set_path("lut")
+                    x = _dev(inp["x"], s.x_dtype)
+                    ys = [layer.forward(x).clone() for _ in range(20)]
+                    nm.append(layer.last_launches()[1])
+                    st.synchronize()
+                    out.append(ys)
+                    layer.close()
+            results[t], names[t] = out, nm
+        except Exception as e:            # reported from the main thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(2)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=120)
+    assert not errors, errors
+    assert all(not th.is_alive() for th in threads)
+    for t in range(2):
+        for i, (s, inp) in enumerate(zip(specs[t], inps[t])):
+            alone = _run(s, inp, "lut" if s.name == "thr_lin_b" else "auto")
+            for y in results[t][i]:
+                assert np.array_equal(y.float().cpu().numpy().astype(np.float64), alone), (s.name,)
+    _say(f"threads: {names}")
+    assert any("lut" in n for n in names[1][1]) and not any("lut" in n for n in names[0][1])
