@@ -39,7 +39,8 @@
  *   - Return value is an aq_status; nothing aborts or throws across the ABI.
  *     On failure aq_last_error() returns a message (thread-local, valid until
  *     the next failing call on the same thread).
- *   - Arguments are validated on the host before any HIP call.
+ *   - Arguments are validated on the host before any launch, allocation or
+ *     copy (a call may first query the current device).
  *   - "host" pointers are read synchronously during the call; "device"
  *     pointers must be HIP device allocations on the layer's device.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
@@ -239,9 +240,11 @@ aq_status aq_layer_set_path(aq_layer* layer, aq_path path);
  *                           fused kernel's own pre-decoded loop (outputs
  *                           bit-identical to its in-loop decode), 2 the
  *                           dense product with both operands staged in LDS,
- *                           3 the wave-split 3x3 convolution kernel where it
- *                           applies (128-token tiles, image planes a multiple
- *                           of 4 pixels)
+ *                           3 the wave-split convolution kernel (3x3 and
+ *                           1x1) where it applies (image planes a multiple
+ *                           of 4 pixels): 128-token tiles, or, with a
+ *                           64-token AQ_OPT_FUSED_TILE, 64-token tiles with
+ *                           two waves per reduction
  *   AQ_OPT_FUSED_TILE       fused kernel tile BM * 1000 + BN (0 = planner);
  *                           a tile that does not fit falls back to the planner
  *   AQ_OPT_DENSE_TILE       dense product tile BM * 1000 + BN (0 = planner)
@@ -296,7 +299,8 @@ aq_status aq_layer_get_option(const aq_layer* layer, int32_t option, int64_t* va
 /*
  * Launch timing without a profiler.  After aq_layer_set_launch_events with n
  * events (hipEvent_t handles created by the caller with timing enabled), each
- * later aq_layer_forward or aq_layer_codebook_grad call on the layer records
+ * later aq_layer_forward, aq_layer_prepare or aq_layer_codebook_grad call on
+ * the layer (not aq_layers_prepare, whose launches serve several layers) records
  * events[0] on its stream before its first kernel launch and events[k] right
  * after its k-th launch (k < n; further launches are not bracketed).  Calls
  * on a stream under graph capture record no events (the runtime has no
@@ -304,8 +308,8 @@ aq_status aq_layer_get_option(const aq_layer* layer, int32_t option, int64_t* va
  * the duration of launch k (plus the gap before it).  n = 0 stops
  * the recording; n is at most 64.  The events stay owned by the caller and
  * must outlive their use.
- * aq_layer_last_launches reports how many kernels the layer's last forward or
- * gradient call launched and, in `names` (truncated to names_size - 1 bytes
+ * aq_layer_last_launches reports how many kernels the layer's last forward,
+ * prepare or gradient call launched and, in `names` (truncated to names_size - 1 bytes
  * and terminated), their kernels one per line, as name<template arguments>
  * with the arguments as integers (a code type as its bit width).
  */
