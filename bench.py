@@ -825,8 +825,8 @@ def main(argv=None):
     a = ap.parse_args(argv)
 
     if a.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {a.gpus}); the AQ layer forward is not sharded "
-              "across GPUs in this build", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for {a.gpus}): the AQ layer forward here runs each "
+              "layer on one GPU and is not sharded across GPUs", file=sys.stderr)
         return 2
 
     if a.steps is None:

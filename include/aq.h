@@ -59,7 +59,7 @@ typedef struct aq_layer aq_layer; /* opaque, owned by the library */
 typedef enum {
     AQ_OK = 0,
     AQ_ERR_INVALID_ARGUMENT = 1, /* bad pointer, size, dtype, alignment or code value */
-    AQ_ERR_UNSUPPORTED = 2,      /* valid request this build has no kernel for       */
+    AQ_ERR_UNSUPPORTED = 2,      /* valid request the library has no kernel for      */
     AQ_ERR_OUT_OF_MEMORY = 3,    /* device allocation failed                          */
     AQ_ERR_DEVICE = 4            /* any other HIP error (or no GPU present)           */
 } aq_status;
