@@ -1082,3 +1082,35 @@ def test_two_host_threads_forward_concurrently():
                 assert np.array_equal(y.float().cpu().numpy().astype(np.float64), alone), (s.name,)
     _say(f"threads: {names}")
     assert any("lut" in n for n in names[1][1]) and not any("lut" in n for n in names[0][1])
+
+
+def test_past_32_bit_offsets_takes_the_64_bit_kernel():
+    """A forward whose element offsets reach 2^31 bytes (131072 tokens x K = 4096: X alone is 1 GiB) leaves the
+    32-bit-offset kernels for the generic matrix-core kernel, which indexes in 64 bits; sampled outputs (the
+    first and last tokens and channels, tile edges, random positions) match the oracle on the GPU's own input,
+    and a second forward gives the same bits."""
+    import paper_2506_05960_amd as P
+    spec = LayerSpec(name="past_2e31", C_out=64, K=4096, g=8, M=2, B=8, n=131072)
+    wts = generate(spec.with_n(1), 91)
+    layer = P.AQLayer(spec, wts, max_tokens=spec.n)
+    d = layer.describe(spec.n)
+    _say(f"past 2^31: {d}")
+    assert d["route"] == "generic"
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(W.SEED_BASE + 91)
+    x = torch.empty((spec.n, spec.K), dtype=torch.float16, device="cuda")
+    for r0 in range(0, spec.n, 16384):                 # seeded N(0, 1), drawn in slices
+        x[r0:r0 + 16384] = torch.randn((16384, spec.K), generator=gen, device="cuda").half()
+    y = layer.forward(x)
+    y2 = layer.forward(x)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    tok, ch = edge_samples(spec, np.random.default_rng(91))
+    tok = np.unique(np.concatenate([tok, [spec.n // 2 - 1, spec.n // 2, spec.n - 2]]))
+    t_idx = torch.from_numpy(tok).cuda()
+    inp = dict(wts)
+    inp["x"] = x[t_idx].cpu().numpy()                   # the sampled rows, re-indexed 0 .. len(tok) - 1
+    inp["x_scales"] = None
+    got = y[t_idx][:, torch.from_numpy(ch).cuda()].float().cpu().numpy().astype(np.float64)
+    check_against_oracle(spec, inp, got, np.arange(len(tok)), ch, "decode", 2e-3)
+    layer.close()
