@@ -1114,3 +1114,37 @@ def test_past_32_bit_offsets_takes_the_64_bit_kernel():
     got = y[t_idx][:, torch.from_numpy(ch).cuda()].float().cpu().numpy().astype(np.float64)
     check_against_oracle(spec, inp, got, np.arange(len(tok)), ch, "decode", 2e-3)
     layer.close()
+
+
+def test_conv_past_32_bit_offsets_takes_the_64_bit_kernel():
+    """The same for a 3x3 convolution whose input passes 2^31 bytes (16 images x 256 channels x 512 x 512 fp16):
+    sampled outputs of the first and last images (corners, edges, interior) against the oracle on those images."""
+    import paper_2506_05960_amd as P
+    spec = LayerSpec(name="conv_past_2e31", C_out=64, K=256 * 9, g=8, M=2, B=8, n=16,
+                     conv=ConvGeom(256, 3, 3, 1, 1, 512, 512))
+    wts = generate(spec.with_n(1), 92)
+    layer = P.AQLayer(spec, wts, max_tokens=spec.tokens)
+    d = layer.describe(spec.n)
+    _say(f"conv past 2^31: {d}")
+    assert d["route"] == "generic"
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(W.SEED_BASE + 92)
+    x = torch.empty((spec.n, 256, 512, 512), dtype=torch.float16, device="cuda")
+    for b in range(spec.n):
+        x[b] = torch.randn((256, 512, 512), generator=gen, device="cuda").half()
+    y = layer.forward(x)
+    torch.cuda.synchronize()
+    imgs = [0, spec.n - 1]
+    rng = np.random.default_rng(92)
+    pos = [(0, 0), (0, 511), (511, 0), (511, 511), (0, 255), (255, 0), (511, 256), (256, 511)]
+    pos += [(int(rng.integers(0, 512)), int(rng.integers(0, 512))) for _ in range(24)]
+    tok_sub = np.array([(i * 512 + oh) * 512 + ow for i in range(len(imgs)) for oh, ow in pos])
+    ch = np.array(sorted({0, 31, 32, 63} | {int(c) for c in rng.integers(0, 64, 12)}))
+    sub = dataclasses.replace(spec, n=len(imgs))
+    inp = dict(wts)
+    inp["x"] = x[imgs].cpu().numpy()
+    inp["x_scales"] = None
+    yi = y[imgs].float().cpu().numpy().astype(np.float64)
+    got = sampled_outputs(sub, yi, tok_sub, ch)
+    check_against_oracle(sub, inp, got, tok_sub, ch, "decode", 2e-3)
+    layer.close()
