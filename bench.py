@@ -795,6 +795,9 @@ def main(argv=None):
     ap.add_argument("--config", default="sweep", help="sweep (default), lutregime, or one layer: tiny, conv64, "
                                                       "qkv16, conv8")
     ap.add_argument("--path", default="auto", choices=["auto", "lut", "decode"])
+    ap.add_argument("--weights", default="auto", choices=["auto", "in-loop", "records"],
+                    help="one layer: the decode path's weight source (in-loop: W never in memory; records: the "
+                         "unscaled decoded weights written and read back every forward)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense-ref", action="store_true",
                     help="sweep: skip the dense fp16 GEMM comparator (torch.matmul on the same shapes)")
@@ -859,6 +862,9 @@ def main(argv=None):
     layer = P.AQLayer(spec, inp)
     if a.path != "auto":
         layer.set_path(a.path)
+    if a.weights != "auto":       # the decode path's weight source forced (AQ_OPT_WEIGHTS)
+        layer.set_option("weights", 1 if a.weights == "in-loop" else 2)
+    wsuffix = "" if a.weights == "auto" else "_" + a.weights.replace("-", "")
     path = layer.choose_path(spec.tokens)
     x = torch.from_numpy(np.ascontiguousarray(inp["x"])).cuda()
     xs = None if inp["x_scales"] is None else torch.from_numpy(inp["x_scales"]).cuda()
@@ -932,7 +938,7 @@ def main(argv=None):
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
-    traffic = measured_traffic_kernel(a.config, kname)
+    traffic = measured_traffic_kernel(a.config + wsuffix, kname)
     if path == "decode" and spec.tile_dtype != "f32":
         roof = {"bound": "mfma", "achieved": round(k_tflops, 3), "peak": PEAK_MFMA_F16_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(k_tflops / PEAK_MFMA_F16_TFLOPS, 4), "traffic": traffic}
@@ -959,7 +965,7 @@ def main(argv=None):
         "vs_baseline": None,
         "dtype": spec.tile_dtype if path == "decode" else "f32",
         "data": "synthetic (seeded; LDM-4-shaped layer, random codebooks/codes/activations)",
-        "config": {"workload": spec.name, "path": path, "launch": "eager" if graph is None else f"hip graph of {per_graph} steps", "tokens": spec.tokens, "K": spec.K, "C_out": spec.C_out,
+        "config": {"workload": spec.name + wsuffix, "path": path, "launch": "eager" if graph is None else f"hip graph of {per_graph} steps", "tokens": spec.tokens, "K": spec.K, "C_out": spec.C_out,
                    "g": spec.g, "M": spec.M, "B": spec.B, "x_dtype": spec.x_dtype, "y_dtype": spec.y_dtype},
         "hbm_gbs_algorithmic": round(gbs, 3),
         "algorithmic_bytes": algorithmic_bytes(spec),
